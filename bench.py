@@ -1,0 +1,246 @@
+"""Benchmark of the pruned-and-skipped multimodal prefill on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llava15_7b] [--keep 128]
+
+One step = the whole hot path over one batch of synthetic LLaVA-shaped input
+already resident in HBM: multi-layer scoring of the vision tokens
+(spider_score), quota/selection/assembly of [kept visual | text]
+(spider_select), one device-to-host copy of the sample boundaries, the skip
+plan on the host, and the skip-aware decoder prefill (spider_prefill).
+
+Prints one JSON line.  `value` is decoder rows (kept visual + text tokens)
+prefilled per second; `roofline` reports the dominant kernel class against
+its roofline (kernel times from HIP events recorded around every launch on
+the launch stream, over the timed steps); `cpu_baseline` times the CPU oracle
+on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+FP32_PEAK_TFLOPS = 157.3
+METRIC = "pruned+skipped prefill tokens/s and ms/sample; % MFMA peak, % HBM peak"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="llava15_7b")
+    p.add_argument("--keep", type=int, default=None)
+    p.add_argument("--layers", type=int, default=None)
+    p.add_argument("--skip-p", type=float, default=None)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-layers", type=int, default=8)
+    return p.parse_args()
+
+
+def build_inputs(w, dev):
+    from synth.decoder_inputs import layer_weights, text_rows, visual_src
+    from synth.skip_inputs import (adaptive_scores, layer_mask, policy_lists, slc_tables)
+    from synth.vision import vision_inputs
+    from paper_2609_34977_amd import _lib
+    from paper_2609_34977_amd.pipeline import SkipPolicy
+
+    attn, feats = vision_inputs(w.score, w.seed)
+    attn, feats = attn.to(dev), [f.to(dev) for f in feats]
+    src, text = visual_src(w, dev), text_rows(w, dev)
+    W = [layer_weights(w.dec, l, w.seed, dev) for l in range(w.dec.L)]
+    if w.skip["kind"] in ("random_layer", "mask"):
+        pol = SkipPolicy(kind="layer_mask", layer_mask=layer_mask(w))
+    else:
+        L = w.dec.L
+        sa, sf = slc_tables(policy_lists(w.skip["policy"], L, w.seed), L)
+        sel, tgt = _lib.slc_policy(sa, sf)
+        cap = min(w.score.n, w.score.keep + w.score.K)
+        pol = SkipPolicy(kind="adaptive", s_sa=adaptive_scores(w, w.tiles_per_sample * cap),
+                         slc_sel=sel, target=tgt, w1=w.skip["w1"], w2=w.skip["w2"],
+                         T_skip=w.skip["T_skip"])
+    return attn, feats, src, text, W, pol
+
+
+def algorithmic(w, cu, codes):
+    """Per kernel class: (bytes, flops) summed over one step, from the per-layer row counts."""
+    d, f, L, dh = w.dec.d, w.dec.d_ff, w.dec.L, w.dec.dh
+    rows = int(cu[-1])
+    out = {k: [0.0, 0.0] for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "attention")}
+    pos = np.concatenate([np.arange(cu[b + 1] - cu[b]) for b in range(len(cu) - 1)])
+    for l in range(L):
+        A = codes[l] & 1 == 0
+        F = codes[l] & 2 == 0
+        nA, nF = int(A.sum()), int(F.sum())
+        if nA:
+            out["gemm_qkv"][0] += 3 * d * d * 2 + rows * d * 2 + (nA + 2 * rows) * d * 2
+            out["gemm_qkv"][1] += 2.0 * d * d * (nA + 2 * rows)
+            out["gemm_o"][0] += d * d * 2 + nA * d * 2 + nA * d * 4
+            out["gemm_o"][1] += 2.0 * d * d * nA
+            out["attention"][0] += nA * d * 2 * 2 + 2 * rows * d * 2
+            out["attention"][1] += 4.0 * d * float((pos[A] + 1).sum())
+        if nF:
+            out["gemm_gateup"][0] += 2 * f * d * 2 + nF * d * 2 + nF * f * 2
+            out["gemm_gateup"][1] += 2.0 * 2 * f * d * nF
+            out["gemm_down"][0] += d * f * 2 + nF * f * 2 + nF * d * 4
+            out["gemm_down"][1] += 2.0 * d * f * nF
+    return out
+
+
+def cpu_baseline(w, n_layers: int, W_dev=None):
+    """Oracle (as it is) on a bounded sample: scoring+selection of every tile and
+    n_layers of the decoder, scaled to one step.  Decoder weights are the
+    benchmark's own (copied to host memory) when given."""
+    import threadpoolctl
+    from oracle import decoder as odec
+    from oracle import msv_prune as mp
+    from synth.decoder_inputs import layer_weights, text_rows, visual_src
+    from synth.vision import vision_inputs
+    from synth.skip_inputs import layer_mask
+
+    cores = len(os.sched_getaffinity(0))
+    attn, feats = vision_inputs(w.score, w.seed)
+    A = attn.numpy()
+    Fs = [f.float().numpy() for f in feats]
+    src, text = visual_src(w).float().numpy(), text_rows(w).float().numpy()
+    if W_dev is not None:
+        Wl = [{k: v.float().cpu().numpy() for k, v in W_dev[l].items()} for l in range(n_layers)]
+    else:
+        Wl = [{k: v.float().numpy() for k, v in layer_weights(w.dec, l, w.seed).items()}
+              for l in range(n_layers)]
+    with threadpoolctl.threadpool_limits(cores):
+        torch.set_num_threads(cores)
+        t0 = time.perf_counter()
+        tiles = [mp.prune_tile(A[g], [f[g] for f in Fs], w.score.keep, w.score.r_num,
+                               w.score.r_den, w.score.K, w.score.kmeans_iter)
+                 for g in range(w.score.G)]
+        x, cu = mp.assemble(src, [t["idx"] for t in tiles], text, w.tiles_per_sample)
+        t1 = time.perf_counter()
+        m = layer_mask(w) if w.skip["kind"] in ("random_layer", "mask") else np.zeros((w.dec.L, 2), bool)
+        col = (m[:, 0].astype(np.uint8) | (m[:, 1].astype(np.uint8) << 1))
+        codes = np.zeros((w.dec.L, int(cu[-1])), np.uint8)
+        for b in range(w.B):
+            n_vis = int(cu[b + 1] - cu[b]) - w.n_text
+            codes[:, cu[b]:cu[b] + n_vis] = col[:, None]
+        odec.prefill(x.astype(np.float32), Wl, cu, codes, w.dec, recipe="bf16",
+                     dtype=np.float32, n_layers=n_layers)
+        t2 = time.perf_counter()
+    t_step = (t1 - t0) + (t2 - t1) * w.dec.L / n_layers
+    rows = int(cu[-1])
+    return {"value": rows / t_step, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "ms_per_step_extrapolated": t_step * 1e3,
+            "sample": (f"oracle scoring+selection of all {w.score.G} tile(s) "
+                       f"({(t1 - t0):.2f} s) plus decoder layers 0..{n_layers - 1} of {w.dec.L} "
+                       f"({(t2 - t1):.2f} s, float32 with the bf16 rounding recipe), decoder "
+                       f"time scaled by {w.dec.L}/{n_layers}; {rows} rows")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see the sharding notes in DESIGN.md); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    from synth import get_workload
+    from paper_2609_34977_amd import _lib
+    from paper_2609_34977_amd.pipeline import Pipeline
+
+    w = get_workload(args.workload, keep=args.keep, L=args.layers, skip_p=args.skip_p)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t_setup = time.perf_counter()
+    attn, feats, src, text, W, pol = build_inputs(w, dev)
+    sc, dec = w.score, w.dec
+    cfg = _lib.decoder_cfg(dec.L, dec.d, dec.H, dec.d_ff,
+                           _lib.BF16 if dec.dtype == "bf16" else _lib.F32, dec.eps, dec.theta)
+    pipe = Pipeline(G=sc.G, n=sc.n, K=sc.K, keep=sc.keep, r_num=sc.r_num, r_den=sc.r_den,
+                    kmeans_iter=sc.kmeans_iter, tiles_per_sample=w.tiles_per_sample,
+                    n_text=w.n_text, quota_mode=w.quota_mode, dec=cfg, weights=W, device=dev)
+    torch.cuda.synchronize()
+    print(f"# setup {time.perf_counter() - t_setup:.1f} s", file=sys.stderr, flush=True)
+
+    out = None
+    for i in range(args.warmup):
+        out = pipe.step(attn, feats, src, text, pol)
+    torch.cuda.synchronize()
+    print("# warmup done", file=sys.stderr, flush=True)
+
+    _lib.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        out = pipe.step(attn, feats, src, text, pol)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = _lib.profile_read()
+    _lib.profile_enable(False)
+    print("# timed steps done", file=sys.stderr, flush=True)
+
+    ms = (t1 - t0) * 1e3 / args.steps
+    cu, codes = out["cu"], out["codes"]
+    rows = int(cu[-1])
+    B = w.B
+    alg = algorithmic(w, cu, codes)
+    kernel_ms = {k: v[1] / args.steps for k, v in prof.items() if v[0]}
+    launches = {k: v[0] // args.steps for k, v in prof.items() if v[0]}
+    dom = max(kernel_ms, key=kernel_ms.get)
+    per_step_ms = kernel_ms[dom]
+    bf16 = dec.dtype == "bf16"
+    if dom in alg:
+        byts, flops = alg[dom]
+        intensity = flops / max(byts, 1.0)
+        ridge = (BF16_PEAK_TFLOPS if bf16 else FP32_PEAK_TFLOPS) * 1e12 / (HBM_PEAK_GBS * 1e9)
+        if dom != "attention" and intensity < ridge:
+            ach = byts / (per_step_ms * 1e-3) / 1e9
+            roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": ach / HBM_PEAK_GBS}
+        else:
+            pk = BF16_PEAK_TFLOPS if bf16 else FP32_PEAK_TFLOPS
+            ach = flops / (per_step_ms * 1e-3) / 1e12
+            roof = {"bound": "mfma", "achieved": ach, "peak": pk, "unit": "TFLOP/s", "frac": ach / pk}
+    else:
+        roof = {"bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": None}
+    roof.update({"kernel": dom, "launches_per_step": launches.get(dom),
+                 "avg_launch_us": per_step_ms * 1e3 / max(launches.get(dom, 1), 1),
+                 "traffic": None})
+    prefill_flops = sum(v[1] for v in alg.values())
+    res = {
+        "metric": METRIC,
+        "value": rows / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": dec.dtype, "data": "synthetic",
+        "config": {"workload": f"{w.name}_keep{sc.keep}", "batch": B, "tiles": sc.G,
+                   "visual_tokens_per_tile": sc.n, "keep_per_tile": sc.keep,
+                   "text_tokens": w.n_text, "decoder_rows": rows, "decoder_layers": dec.L,
+                   "d_model": dec.d, "heads": dec.H, "d_ff": dec.d_ff,
+                   "skip": w.skip.get("kind"), "skip_p": w.skip.get("p"),
+                   "skipped_sublayer_slots": float((codes[:, :rows] != 0).mean()),
+                   "parallelism": "single GPU"},
+        "ms_per_sample": ms / B,
+        "effective_tokens_per_s": B * (sc.n * w.tiles_per_sample + w.n_text) / (ms * 1e-3),
+        "prefill_tflop_per_step": prefill_flops / 1e12,
+        "roofline": roof,
+        "kernel_ms_per_step": {k: round(v, 4) for k, v in kernel_ms.items()},
+        "launches_per_step": launches,
+    }
+    if not args.no_cpu_baseline:
+        print("# cpu baseline", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(w, min(args.cpu_layers, dec.L), W)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

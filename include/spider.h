@@ -1,0 +1,252 @@
+/*
+ * spider.h - C ABI of the MI355X (gfx950) implementation of SPIDER's
+ * pruned-and-skipped multimodal prefill (multi-layer semantic token pruning,
+ * Sec. 4.1, and adaptive sub-layer skipping, Sec. 4.2-4.3 / Algorithm 1).
+ *
+ * Conventions for every entry point:
+ *   - All device buffers are owned by the caller.  The library never
+ *     allocates or frees device memory; scratch space comes from a
+ *     caller-provided workspace whose size is given by the matching
+ *     *_workspace_size() query.  Host arrays are read before the call
+ *     returns and may be freed afterwards.
+ *   - Arguments are validated before any HIP call.  On error nothing is
+ *     enqueued, outputs are untouched, a non-zero spider_status is returned
+ *     and a thread-local message is available from spider_last_error().
+ *     A failed kernel launch returns SPIDER_ERR_HIP.  Faults inside kernels
+ *     surface at the caller's next synchronisation of the stream.
+ *   - All device work is enqueued on `stream` (a hipStream_t; NULL means the
+ *     default stream).  Calls are asynchronous unless stated otherwise.
+ *   - Strides are in elements, not bytes.  Row-major everywhere.
+ *   - Identical inputs give bitwise-identical outputs on the same GPU (no
+ *     floating-point atomics).
+ *   - Calls on distinct workspaces are independent; the library keeps no
+ *     per-call state except the thread-local error message, the optional
+ *     profiler and a per-thread pinned staging buffer used by
+ *     spider_prefill to upload its row tables.
+ */
+#ifndef SPIDER_H
+#define SPIDER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPIDER_OK = 0,
+  SPIDER_ERR_INVALID_ARG = 1,  /* null pointer, negative size, bad enum     */
+  SPIDER_ERR_SHAPE = 2,        /* inconsistent sizes (keep > n, cap small)  */
+  SPIDER_ERR_UNSUPPORTED = 3,  /* valid but not implemented (e.g. dh != 128 in bf16) */
+  SPIDER_ERR_WORKSPACE = 4,    /* workspace null or smaller than required   */
+  SPIDER_ERR_HIP = 5           /* a HIP runtime call or launch failed       */
+} spider_status;
+
+typedef enum { SPIDER_F32 = 0, SPIDER_BF16 = 1 } spider_dtype;
+
+/* Opaque stream handle: pass a hipStream_t (or NULL for the default stream). */
+typedef void* spider_stream;
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* spider_last_error(void);
+
+/* ABI version (major * 100 + minor). */
+int spider_version(void);
+
+/* ------------------------------------------------------------------------
+ * Token budget (Sec. 4.1.1-4.1.2).  Host only, no HIP call.
+ * The anchor budget n*R*r of Sec. 4.1.1 is taken per tile as
+ * n_anchor = floor(keep * r_num / r_den) in exact integer arithmetic and the
+ * complementary budget n*R*(1-r) of Sec. 4.1.2 as n_cmp = keep - n_anchor.
+ * Requires keep >= 0, r_den > 0, 0 <= r_num <= r_den.
+ * ------------------------------------------------------------------------ */
+spider_status spider_budget(int keep, int r_num, int r_den, int* n_anchor, int* n_cmp);
+
+/* ------------------------------------------------------------------------
+ * spider_score - MSV-Prune scoring of G independent tiles (Sec. 4.1, Eq. 1
+ * and Eq. 3, Algorithm 1 stage 1).  For every tile g and patch i < n:
+ *   a[g,i]       = (sum over heads h = 0..H-1, in order, in fp32, of
+ *                   cls_attn[g,h,attn_col0+i]) / H                (Sec. 4.1.1)
+ *   anchors      = the n_anchor patches with the largest a, ties to the
+ *                  lower index (Eq. 1 read as Algorithm 1's top-nRr)
+ *   cluster[g,i] = -1 for anchors; otherwise the K-means cluster of the
+ *                  patch's last-layer feature (Sec. 4.1.2): Euclidean Lloyd
+ *                  iterations on the raw rows of F^L (the last entry of
+ *                  feats), centroids initialised at the non-anchor rows
+ *                  floor(k*m/K) (m = non-anchor count, rows in ascending
+ *                  patch order), at most kmeans_max_iter assignment passes
+ *                  with early exit when no assignment changes, ties to the
+ *                  lower cluster, empty clusters keep their centroid; fp32.
+ *   m[g,i]       = max over anchors p of cos(F^L_i, F^L_p)   (0 if none)
+ *   s[g,i]       = mean over j in the cluster of i of the Eq. 3 score
+ *                  S_ij = sum over tapped layers l of cos(F^l_i, F^l_j)
+ *                         + m_i + m_j,
+ *                  +inf for anchors.  Cosine with a zero row is 0.
+ * Inputs:
+ *   cls_attn  device fp32; element (g,h,c) at cls_attn[g*attn_stride_g +
+ *             h*attn_stride_h + c]; patch i is column attn_col0 + i (the CLS
+ *             row of the last tapped layer's attention, column 0 = CLS).
+ *   feats     HOST array of n_layers device pointers (tapped layers, the last
+ *             one is F^L), each of dtype feat_dtype; patch i of tile g is row
+ *             feat_row0 + i: element (g,row,c) at feats[l][g*feat_stride_g +
+ *             row*feat_stride_row + c].
+ *   Limits: 1 <= n <= 4096, 1 <= H, 1 <= d_v <= 2048, 1 <= n_layers <= 8,
+ *   1 <= K <= 8, 0 <= n_anchor <= n, kmeans_max_iter >= 1.
+ * Outputs (device, [G,n], row stride n): a_out fp32, cluster_out int32,
+ *   s_out fp32, m_out fp32 (may be NULL).
+ * Workspace: spider_score_workspace_size(G, n, d_v, n_layers, K) bytes,
+ *   256-byte aligned device memory; contents on entry are ignored.
+ * ------------------------------------------------------------------------ */
+size_t spider_score_workspace_size(int G, int n, int d_v, int n_layers, int K);
+
+spider_status spider_score(int G, int n, int H, int d_v, int n_layers,
+                           const float* cls_attn, int64_t attn_stride_g,
+                           int64_t attn_stride_h, int attn_col0,
+                           const void* const* feats, spider_dtype feat_dtype,
+                           int64_t feat_stride_g, int64_t feat_stride_row, int feat_row0,
+                           int n_anchor, int K, int kmeans_max_iter,
+                           float* a_out, int32_t* cluster_out, float* s_out, float* m_out,
+                           void* workspace, size_t workspace_bytes, spider_stream stream);
+
+/* ------------------------------------------------------------------------
+ * spider_select - quotas, complementary selection, spatial-order union
+ * (Sec. 4.1.2, Eq. 2; Sec. 4.1) and optional assembly of the decoder input.
+ * Per tile g (cluster/s as written by spider_score, row stride n):
+ *   |C_k|   = number of patches with cluster == k (k < K);
+ *   N_k     = quota_mode 0 (Eq. 2 literally): 0 for an empty cluster, else
+ *             min(|C_k|, max(1, round_half_even(n_cmp*|C_k| / sum_j |C_j|)))
+ *             computed exactly in integers (the total may differ from n_cmp);
+ *             quota_mode 1: largest-remainder apportionment of exactly
+ *             min(n_cmp, sum|C_j|) tokens, ties to the lower cluster;
+ *             all quotas are 0 when n_cmp == 0;
+ *   kept    = anchors (cluster == -1) plus, per cluster, the N_k patches
+ *             with the smallest s (ties to the lower index; -0.0 == +0.0);
+ *   idx_out[g, 0..count-1] = kept patch indices ascending; the rest of the
+ *             row (up to cap) is -1; count_out[g] = count.
+ *   cap must be >= min(n, n_anchor + n_cmp + K) (the largest count Eq. 2 can
+ *   produce when n_anchor patches are anchors).
+ * Assembly (skipped when src == NULL): B = G / tiles_per_sample samples; the
+ *   packed decoder input x_out holds, per sample b, the kept rows of its
+ *   tiles in tile order (row i of tile g = src[g*src_stride_g + i*d_model])
+ *   followed by its n_text text rows (text[b*n_text*d_model + t*d_model]),
+ *   samples one after another; cu_seqlens_out[0..B] (device int32) gets the
+ *   sample boundaries.  src/text/x_out have dtype act_dtype.  x_out must hold
+ *   B*(tiles_per_sample*cap + n_text) rows of d_model.  In quota_mode 0 the
+ *   caller reads cu_seqlens_out (one device-to-host copy) to size the
+ *   prefill; in quota_mode 1 every count is n_anchor + min(n_cmp, n - n_anchor).
+ * No workspace.  Limits: 1 <= n <= 4096, 1 <= K <= 8, tiles_per_sample >= 1
+ * dividing G, d_model % 8 == 0 when assembling.
+ * ------------------------------------------------------------------------ */
+spider_status spider_select(int G, int n, const int32_t* cluster, const float* s,
+                            int n_anchor, int n_cmp, int K, int quota_mode,
+                            int32_t* idx_out, int32_t* count_out, int cap,
+                            int tiles_per_sample, const void* src, int64_t src_stride_g,
+                            int d_model, spider_dtype act_dtype, const void* text, int n_text,
+                            void* x_out, int32_t* cu_seqlens_out, spider_stream stream);
+
+/* ------------------------------------------------------------------------
+ * Offline sub-layer contribution policy (Sec. 4.2.2, Eq. 5).  Host only.
+ *   norm_f(l) = 1 - (slc_f(l) - min_l slc_f) / (max_l slc_f - min_l slc_f + eps)
+ * for each family f in {attention, FFN}, in double precision; the per-layer
+ * skip target is target_out[l] = 1 (FFN) if norm_ffn(l) > norm_attn(l) else
+ * 0 (attention: ties go to attention), and slc_sel_out[l] = norm of that
+ * target.  slc_attn/slc_ffn: host [L] floats.  Outputs host [L].
+ * ------------------------------------------------------------------------ */
+spider_status spider_slc_policy(int L, const float* slc_attn, const float* slc_ffn, double eps,
+                                double* slc_sel_out, uint8_t* target_out);
+
+/* ------------------------------------------------------------------------
+ * spider_plan_skips - admission rule of Algorithm 1 / Eq. 6 for one sample.
+ * Host only.  For layers l = 0 .. floor(L/2)-1 (the decision window,
+ * 1-indexed l <= L/2) and every visual token i not yet in skip mode:
+ *   acc_i += w1 * s_sa[l*s_sa_stride + i] + w2 * slc_sel[l]   (double)
+ *   if acc_i >= T_skip: token i enters skip mode at layer l with its target
+ *   frozen to target[l] (0 attention, 1 FFN).
+ * A token admitted at layer l bypasses its target in layers l .. L-1:
+ *   codes_out[l2*codes_stride + i] = 1 (attention) or 2 (FFN), else 0.
+ * admit_out (may be NULL) receives the admission layer or -1.
+ * s_sa: host [floor(L/2), s_sa_stride] floats; slc_sel: host [L] doubles;
+ * target: host [L] bytes; codes_out: host [L, codes_stride] bytes.
+ * ------------------------------------------------------------------------ */
+spider_status spider_plan_skips(int L, int n_vis, const float* s_sa, int s_sa_stride,
+                                const double* slc_sel, const uint8_t* target,
+                                double w1, double w2, double T_skip,
+                                uint8_t* codes_out, int codes_stride, int32_t* admit_out);
+
+/* ------------------------------------------------------------------------
+ * spider_prefill - LLaMA-style decoder prefill over packed samples with
+ * per-row sub-layer bypass (VSkip-Attn / VSkip-FFN of Sec. 3.2, the forward
+ * step of Algorithm 1).  Per layer l and row r (codes[l*rows + r]):
+ *   bit 0 clear: h_r += Wo * Attn(RMSNorm(h; attn_norm))_r   (row is a query)
+ *   bit 1 clear: h_r += Wd (silu(Wg x) * (Wu x)), x = RMSNorm(h; ffn_norm)_r
+ * A row with bit 0 set gets no attention update but still provides keys and
+ * values (computed from its current h); a row with bit 1 set gets no FFN
+ * update; a bypassed row keeps its value exactly.  Attention is causal within
+ * each sample (rows cu_seqlens[b] .. cu_seqlens[b+1]-1, positions restarting
+ * at 0), multi-head with dh = d/H, scale 1/sqrt(dh), rotate-half RoPE with
+ * base theta on queries and keys.  RMSNorm(x) = x / sqrt(mean(x^2) + eps) * w.
+ * No work is launched for bypassed rows; a sub-layer with no active row in
+ * a layer launches nothing (keys/values are not computed when no row of any
+ * sample is a query).
+ * Precision (dtype SPIDER_BF16): weights, x and activations bf16; residual h
+ *   fp32; RMSNorm outputs, Q/K after RoPE, V, attention outputs and
+ *   silu(g)*u rounded to bf16 (round-to-nearest-even) from fp32; GEMMs
+ *   accumulate in fp32 (MFMA); O and down outputs are added to h in fp32;
+ *   softmax in fp32.  Requires dh == 128, d % 64 == 0, d_ff % 64 == 0.
+ * dtype SPIDER_F32: everything fp32 (any dh <= 256 with dh even).
+ * Inputs: cfg; layers = HOST array [L] of per-layer device weight pointers
+ *   (matrices in nn.Linear layout [out, in], norms fp32 [d]); cu_seqlens =
+ *   HOST int32 [B+1] (cu[0] = 0, non-decreasing); x = device [rows, d] in
+ *   cfg->dtype with rows = cu_seqlens[B]; codes = HOST uint8 [L, rows].
+ * Output: h_out device fp32 [rows, d] (the residual stream after layer L-1,
+ *   before any final norm).  x and h_out must not overlap.
+ * Workspace: spider_prefill_workspace_size(cfg, B, rows) bytes.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int L;            /* decoder layers                      */
+  int d;            /* model width                         */
+  int H;            /* attention heads (dh = d / H)        */
+  int d_ff;         /* SwiGLU hidden width                 */
+  float eps;        /* RMSNorm epsilon                     */
+  float theta;      /* RoPE base                           */
+  spider_dtype dtype;
+} spider_decoder_cfg;
+
+typedef struct {
+  const float* attn_norm;   /* [d] fp32                    */
+  const void* wq;           /* [d, d]                      */
+  const void* wk;           /* [d, d]                      */
+  const void* wv;           /* [d, d]                      */
+  const void* wo;           /* [d, d]                      */
+  const float* ffn_norm;    /* [d] fp32                    */
+  const void* wg;           /* [d_ff, d]                   */
+  const void* wu;           /* [d_ff, d]                   */
+  const void* wd;           /* [d, d_ff]                   */
+} spider_layer_weights;
+
+size_t spider_prefill_workspace_size(const spider_decoder_cfg* cfg, int B, int rows);
+
+spider_status spider_prefill(const spider_decoder_cfg* cfg, const spider_layer_weights* layers,
+                             int B, const int32_t* cu_seqlens, const void* x,
+                             const uint8_t* codes, float* h_out,
+                             void* workspace, size_t workspace_bytes, spider_stream stream);
+
+/* ------------------------------------------------------------------------
+ * Kernel-class profiler (process-global, not thread-safe; for benchmarks).
+ * When enabled, every launch of the library records a pair of HIP events on
+ * its stream.  spider_profile_read() synchronises on the recorded events and
+ * returns, for kernel class `cls` (0 .. spider_profile_classes()-1), the
+ * number of launches and the summed kernel time in milliseconds since the
+ * last reset.  spider_profile_enable(0) stops recording; (1) starts it and
+ * resets the counters.
+ * ------------------------------------------------------------------------ */
+spider_status spider_profile_enable(int enable);
+int spider_profile_classes(void);
+const char* spider_profile_class_name(int cls);
+spider_status spider_profile_read(int cls, int64_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPIDER_H */

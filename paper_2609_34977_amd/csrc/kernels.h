@@ -1,0 +1,61 @@
+// Internal launch interfaces of the decoder kernels (GEMM, attention).
+#pragma once
+
+#include "common.h"
+
+namespace spider {
+
+// One GEMM problem of a grouped launch: out = A[rows] x W^T (nn.Linear layout).
+struct GemmGroup {
+  const void* A;          // activations [*, K] row-major, row stride lda
+  const int32_t* a_rows;  // optional: A row of output row m (gather); null = identity
+  int M;                  // output rows
+  const void* W;          // weights [N, K] row-major
+  const void* W2;         // second weights for the dual (SwiGLU) epilogue, else null
+  int N;                  // output columns
+  void* out;              // see GemmArgs::epilogue
+  int64_t ldo;            // row stride of out (elements)
+  int64_t split_stride;   // elements between split-K slabs of out
+  int tiles_m, tiles_n;   // filled by the launcher
+  int tile_begin;         // filled by the launcher
+};
+
+enum GemmEpilogue {
+  EPI_PARTIAL_F32 = 0,  // out fp32 [split][M][N]: this split's partial sums
+  EPI_SWIGLU = 1        // out act dtype [M][N] = silu(A W^T) * (A W2^T); split must be 1
+};
+
+struct GemmArgs {
+  GemmGroup g[3];
+  int ngroups;
+  int K;
+  int64_t lda;
+  int split;
+  int k_per_split;
+  int epilogue;
+  int total_tiles;
+};
+
+// Chooses tiles and split-K for the groups (all with the same K) and launches.
+// `split_max` bounds split-K (partial buffers are sized for it).
+hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st);
+hipError_t launch_gemm_f32(GemmArgs& a, int split_max, hipStream_t st);
+
+// Split-K factor the launcher will use for a group of M rows, N columns, K depth.
+int gemm_split_for(int M, int N, int K, bool dual, bool bf16, int split_max);
+
+// Causal attention over packed samples for a compacted list of query rows.
+struct AttnArgs {
+  const void* q;           // [nq, d] (row a = query a)
+  const int32_t* q_rows;   // [nq] packed row of query a
+  const void* k;           // [rows, d]
+  const void* v;           // [rows, d]
+  const int32_t* row_start;  // [rows] first row of the sample that owns the row
+  void* o;                 // [nq, d]
+  int nq, rows, H, dh, d;
+  float scale;             // 1/sqrt(dh)
+};
+hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t st);
+hipError_t launch_attention_f32(const AttnArgs& a, int max_seq, hipStream_t st);
+
+}  // namespace spider

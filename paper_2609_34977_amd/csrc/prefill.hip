@@ -1,0 +1,495 @@
+// Skip-aware decoder prefill driver (the per-layer forward of Algorithm 1
+// with VSkip-Attn / VSkip-FFN rows, Sec. 3.2) and its small kernels.
+//
+// Per layer l (host loop; row lists built on the host from the codes):
+//   A_l = rows that do not bypass attention (queries), F_l = rows that do not
+//   bypass the FFN.
+//   if A_l non-empty:
+//     rmsnorm   every row: h += pending residual partials; xn = bf16(norm(h))
+//     gemm_qkv  one grouped launch: Q over A_l (gathered rows of xn), K and V
+//               over every row (bypassing rows still provide keys/values)
+//     qkv_fin   sum split-K partials, RoPE (table built in double), round
+//     attention causal, compacted queries A_l
+//     gemm_o    O rows of A_l -> fp32 split-K partials (pending residual)
+//   if F_l non-empty:
+//     rmsnorm   every row: h += pending; rows of F_l -> compact xf
+//     gemm_gateup fused SwiGLU over F_l -> act
+//     gemm_down act -> fp32 split-K partials (pending residual)
+//   Nothing is launched for an empty set.  After the last layer a residual
+//   kernel applies what is still pending.  Residual partials are summed in
+//   fixed split order by the consuming kernel (deterministic, no atomics).
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+
+namespace spider {
+namespace {
+
+template <typename AT>
+struct Act;
+template <>
+struct Act<float> {
+  __device__ static inline void store(float* p, float v) { *p = v; }
+  __device__ static inline float load(const float* p) { return *p; }
+};
+template <>
+struct Act<uint16_t> {
+  __device__ static inline void store(uint16_t* p, float v) { *p = f32_to_bf16_bits(v); }
+  __device__ static inline float load(const uint16_t* p) { return bf16_bits_to_f32(*p); }
+};
+
+// h = float(x)
+template <typename AT>
+__global__ void __launch_bounds__(256) embed_kernel(const AT* __restrict__ x, float* __restrict__ h,
+                                                    int64_t total) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < total) h[i] = Act<AT>::load(x + i);
+}
+
+// cos/sin table for RoPE: tab[p*half + i] = (cos, sin)(p * theta^(-2i/dh)), double math.
+__global__ void __launch_bounds__(256) rope_table_kernel(float2* __restrict__ tab, int max_pos,
+                                                         int half, int dh, double log2_theta) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)max_pos * half) return;
+  const int p = (int)(t / half), i = (int)(t % half);
+  const double inv = exp2(-(2.0 * i / dh) * log2_theta);
+  const double ang = (double)p * inv;
+  tab[t] = make_float2((float)cos(ang), (float)sin(ang));
+}
+
+// One block per row: apply pending residual partials (h[r] += sum_s P[s][pslot[r]])
+// then, if the row is selected, out[nslot[r]] = round(h * rsqrt(mean(h^2) + eps) * w).
+template <typename AT>
+__global__ void __launch_bounds__(256) norm_kernel(float* __restrict__ h, int d,
+                                                   const float* __restrict__ P, int psplit,
+                                                   int64_t pstride, const int32_t* __restrict__ pslot,
+                                                   const float* __restrict__ w, float eps,
+                                                   const int32_t* __restrict__ nslot, int all_rows,
+                                                   AT* __restrict__ out) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  float* hr = h + (int64_t)r * d;
+  const int ps = (P && pslot) ? pslot[r] : -1;
+  const int ns = all_rows ? r : (nslot ? nslot[r] : -1);
+  if (ps < 0 && ns < 0) return;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    float v = hr[c];
+    if (ps >= 0) {
+      float add = 0.f;
+      for (int s = 0; s < psplit; ++s) add += P[s * pstride + (int64_t)ps * d + c];
+      v += add;
+      hr[c] = v;
+    }
+    ss = fmaf(v, v, ss);
+  }
+  if (ns < 0) return;
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  AT* o = out + (int64_t)ns * d;
+  for (int c = threadIdx.x; c < d; c += 256) Act<AT>::store(o + c, hr[c] * inv * w[c]);
+}
+
+// Blocks [0, nq): Q rows, [nq, nq+R): K rows, [nq+R, nq+2R): V rows.
+// Sums split partials, applies rotate-half RoPE to Q and K, stores act dtype.
+template <typename AT>
+__global__ void __launch_bounds__(256) qkv_finalize_kernel(
+    const float* __restrict__ Pq, const float* __restrict__ Pk, const float* __restrict__ Pv,
+    int split, int64_t pstride, int nq, int R, int d, int dh, const int32_t* __restrict__ q_rows,
+    const int32_t* __restrict__ pos, const float2* __restrict__ rope, AT* __restrict__ Q,
+    AT* __restrict__ K, AT* __restrict__ V) {
+  int b = blockIdx.x;
+  const float* P;
+  AT* out;
+  int prow, p = -1;
+  if (b < nq) {
+    P = Pq;
+    out = Q;
+    prow = b;
+    p = pos[q_rows[b]];
+  } else if (b < nq + R) {
+    P = Pk;
+    out = K;
+    prow = b - nq;
+    p = pos[prow];
+  } else {
+    P = Pv;
+    out = V;
+    prow = b - nq - R;
+  }
+  const int half = dh / 2;
+  const float* src = P + (int64_t)prow * d;
+  AT* dst = out + (int64_t)prow * d;
+  for (int t = threadIdx.x; t < d / 2; t += 256) {
+    const int head = t / half, i = t - head * half;
+    const int c0 = head * dh + i, c1 = c0 + half;
+    float x0 = 0.f, x1 = 0.f;
+    for (int s = 0; s < split; ++s) {
+      x0 += src[s * pstride + c0];
+      x1 += src[s * pstride + c1];
+    }
+    if (p >= 0) {
+      const float2 cs = rope[(int64_t)p * half + i];
+      const float y0 = x0 * cs.x - x1 * cs.y;
+      const float y1 = x1 * cs.x + x0 * cs.y;
+      x0 = y0;
+      x1 = y1;
+    }
+    Act<AT>::store(dst + c0, x0);
+    Act<AT>::store(dst + c1, x1);
+  }
+}
+
+// ------------------------------------------------------------------ host side
+struct LayerTables {
+  int nA = 0, nF = 0;
+  int offA = -1, offF = -1;         // offsets of the row lists (ints)
+  int offSlotA = -1, offSlotF = -1;  // offsets of the row -> slot maps
+};
+
+// Pinned host buffer for the row tables of one thread's prefill calls.  It is
+// reused across calls once the previous upload has completed (event), and is
+// deliberately not released at thread exit (the HIP runtime may already be
+// shut down then); the OS reclaims it with the process.
+struct Staging {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t ev = nullptr;
+  bool pending = false;
+};
+thread_local Staging g_stage;
+
+int split_max_for_rows(int R) { return std::max(1, std::min(4, 2048 / std::max(1, R))); }
+
+struct PrefillWs {
+  int32_t* tables;
+  float2* rope;
+  void *xn, *q, *k, *v, *o, *act;
+  float *Pq, *Pk, *Pv, *Pres;
+  size_t bytes;
+};
+
+size_t table_ints_bound(int L, int R) { return (size_t)R * 2 + (size_t)L * 4 * R + 64; }
+
+PrefillWs prefill_layout(const spider_decoder_cfg& c, int R, char* base) {
+  PrefillWs w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes, 256);
+    return base ? base + o : nullptr;
+  };
+  const size_t es = c.dtype == SPIDER_BF16 ? 2 : 4;
+  const int dh = c.d / c.H;
+  const int sm = split_max_for_rows(R);
+  w.tables = reinterpret_cast<int32_t*>(take(table_ints_bound(c.L, R) * 4));
+  w.rope = reinterpret_cast<float2*>(take((size_t)R * (dh / 2) * sizeof(float2)));
+  w.xn = take((size_t)R * c.d * es);
+  w.q = take((size_t)R * c.d * es);
+  w.k = take((size_t)R * c.d * es);
+  w.v = take((size_t)R * c.d * es);
+  w.o = take((size_t)R * c.d * es);
+  w.act = take((size_t)R * c.d_ff * es);
+  w.Pq = reinterpret_cast<float*>(take((size_t)sm * R * c.d * 4));
+  w.Pk = reinterpret_cast<float*>(take((size_t)sm * R * c.d * 4));
+  w.Pv = reinterpret_cast<float*>(take((size_t)sm * R * c.d * 4));
+  w.Pres = reinterpret_cast<float*>(take((size_t)sm * R * c.d * 4));
+  w.bytes = off;
+  return w;
+}
+
+spider_status validate_cfg(const spider_decoder_cfg* cfg) {
+  SPIDER_REQUIRE(cfg, SPIDER_ERR_INVALID_ARG, "spider_prefill: cfg is null");
+  SPIDER_REQUIRE(cfg->L >= 1 && cfg->d >= 1 && cfg->H >= 1 && cfg->d_ff >= 1,
+                 SPIDER_ERR_INVALID_ARG, "spider_prefill: L, d, H, d_ff must be >= 1");
+  SPIDER_REQUIRE(cfg->d % cfg->H == 0, SPIDER_ERR_SHAPE, "spider_prefill: d must be divisible by H");
+  const int dh = cfg->d / cfg->H;
+  SPIDER_REQUIRE(dh % 2 == 0, SPIDER_ERR_SHAPE, "spider_prefill: dh must be even");
+  SPIDER_REQUIRE(cfg->dtype == SPIDER_F32 || cfg->dtype == SPIDER_BF16, SPIDER_ERR_INVALID_ARG,
+                 "spider_prefill: bad dtype");
+  SPIDER_REQUIRE(std::isfinite(cfg->eps) && cfg->eps >= 0.f && std::isfinite(cfg->theta) &&
+                     cfg->theta > 0.f,
+                 SPIDER_ERR_INVALID_ARG, "spider_prefill: eps must be >= 0 and theta > 0");
+  if (cfg->dtype == SPIDER_BF16) {
+    SPIDER_REQUIRE(dh == 128, SPIDER_ERR_UNSUPPORTED, "spider_prefill: bf16 path needs dh == 128");
+    SPIDER_REQUIRE(cfg->d % 64 == 0 && cfg->d_ff % 64 == 0, SPIDER_ERR_UNSUPPORTED,
+                   "spider_prefill: bf16 path needs d and d_ff multiples of 64");
+  } else {
+    SPIDER_REQUIRE(dh <= 256, SPIDER_ERR_UNSUPPORTED, "spider_prefill: fp32 path needs dh <= 256");
+  }
+  return SPIDER_OK;
+}
+
+template <typename AT>
+spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weights* W, int B,
+                          const int32_t* cu, const void* x, const uint8_t* codes, float* h,
+                          const PrefillWs& ws, hipStream_t st) {
+  const bool bf16 = c.dtype == SPIDER_BF16;
+  const int R = cu[B];
+  const int d = c.d, dh = d / c.H, half = dh / 2;
+  // ---- host tables
+  std::vector<int32_t> tab;
+  tab.reserve(table_ints_bound(c.L, R));
+  const int off_pos = 0, off_start = R;
+  tab.resize(2 * R);
+  int max_s = 1;
+  for (int b = 0; b < B; ++b) {
+    max_s = std::max(max_s, cu[b + 1] - cu[b]);
+    for (int r = cu[b]; r < cu[b + 1]; ++r) {
+      tab[off_pos + r] = r - cu[b];
+      tab[off_start + r] = cu[b];
+    }
+  }
+  std::vector<LayerTables> lt(c.L);
+  std::map<std::string, std::pair<int, int>> seen[2];  // column -> (list offset, slot offset)
+  for (int l = 0; l < c.L; ++l) {
+    const uint8_t* col = codes + (size_t)l * R;
+    for (int which = 0; which < 2; ++which) {
+      const uint8_t bit = which == 0 ? 1 : 2;
+      std::string key(R, '\0');
+      int cnt = 0;
+      for (int r = 0; r < R; ++r) {
+        const bool active = !(col[r] & bit);
+        key[r] = active ? 1 : 0;
+        cnt += active;
+      }
+      auto it = seen[which].find(key);
+      std::pair<int, int> offs;
+      if (it != seen[which].end()) {
+        offs = it->second;
+      } else {
+        const int off_list = (int)tab.size();
+        for (int r = 0; r < R; ++r)
+          if (key[r]) tab.push_back(r);
+        const int off_slot = (int)tab.size();
+        int s = 0;
+        for (int r = 0; r < R; ++r) tab.push_back(key[r] ? s++ : -1);
+        offs = {off_list, off_slot};
+        seen[which][key] = offs;
+      }
+      if (which == 0) {
+        lt[l].nA = cnt;
+        lt[l].offA = offs.first;
+        lt[l].offSlotA = offs.second;
+      } else {
+        lt[l].nF = cnt;
+        lt[l].offF = offs.first;
+        lt[l].offSlotF = offs.second;
+      }
+    }
+  }
+  // ---- upload through the pinned staging buffer
+  const size_t tbytes = tab.size() * sizeof(int32_t);
+  if (g_stage.pending) {
+    SPIDER_HIP(hipEventSynchronize(g_stage.ev));
+    g_stage.pending = false;
+  }
+  if (g_stage.cap < tbytes) {
+    if (g_stage.host) SPIDER_HIP(hipHostFree(g_stage.host));
+    g_stage.host = nullptr;
+    g_stage.cap = 0;
+    SPIDER_HIP(hipHostMalloc(&g_stage.host, tbytes));
+    g_stage.cap = tbytes;
+  }
+  if (!g_stage.ev) SPIDER_HIP(hipEventCreateWithFlags(&g_stage.ev, hipEventDisableTiming));
+  std::memcpy(g_stage.host, tab.data(), tbytes);
+  SPIDER_HIP(hipMemcpyAsync(ws.tables, g_stage.host, tbytes, hipMemcpyHostToDevice, st));
+  SPIDER_HIP(hipEventRecord(g_stage.ev, st));
+  g_stage.pending = true;
+
+  const int32_t* dpos = ws.tables + off_pos;
+  const int32_t* dstart = ws.tables + off_start;
+  // ---- rope table and residual init
+  {
+    const int64_t n = (int64_t)max_s * half;
+    rope_table_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(ws.rope, max_s, half, dh,
+                                                                  std::log2((double)c.theta));
+    SPIDER_LAUNCHED("rope_table");
+  }
+  {
+    ProfScope ps(KC_EMBED, st);
+    const int64_t n = (int64_t)R * d;
+    embed_kernel<AT><<<(unsigned)((n + 255) / 256), 256, 0, st>>>(reinterpret_cast<const AT*>(x), h, n);
+    SPIDER_LAUNCHED("embed");
+  }
+  const int split_max = split_max_for_rows(R);
+  const int64_t pstride = (int64_t)R * d;
+  // pending residual partials
+  int pend_split = 0;
+  const int32_t* pend_slot = nullptr;
+  AT* xn = reinterpret_cast<AT*>(ws.xn);
+  AT* qb = reinterpret_cast<AT*>(ws.q);
+  AT* kb = reinterpret_cast<AT*>(ws.k);
+  AT* vb = reinterpret_cast<AT*>(ws.v);
+  AT* ob = reinterpret_cast<AT*>(ws.o);
+  AT* act = reinterpret_cast<AT*>(ws.act);
+  auto gemm = [&](GemmArgs& ga) {
+    return bf16 ? launch_gemm_bf16(ga, split_max, st) : launch_gemm_f32(ga, split_max, st);
+  };
+
+  for (int l = 0; l < c.L; ++l) {
+    const spider_layer_weights& w = W[l];
+    const LayerTables& T = lt[l];
+    if (T.nA > 0) {
+      {
+        ProfScope ps(KC_RMSNORM, st);
+        norm_kernel<AT><<<R, 256, 0, st>>>(h, d, ws.Pres, pend_split, pstride, pend_slot,
+                                           w.attn_norm, c.eps, nullptr, 1, xn);
+        SPIDER_LAUNCHED("rmsnorm(attn)");
+        pend_split = 0;
+        pend_slot = nullptr;
+      }
+      GemmArgs ga{};
+      ga.ngroups = 3;
+      ga.K = d;
+      ga.lda = d;
+      ga.epilogue = EPI_PARTIAL_F32;
+      ga.g[0] = GemmGroup{xn, ws.tables + T.offA, T.nA, w.wq, nullptr, d, ws.Pq, d, pstride, 0, 0, 0};
+      ga.g[1] = GemmGroup{xn, nullptr, R, w.wk, nullptr, d, ws.Pk, d, pstride, 0, 0, 0};
+      ga.g[2] = GemmGroup{xn, nullptr, R, w.wv, nullptr, d, ws.Pv, d, pstride, 0, 0, 0};
+      {
+        ProfScope ps(KC_GEMM_QKV, st);
+        hipError_t e = gemm(ga);
+        SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_qkv: %s", hipGetErrorString(e));
+      }
+      {
+        ProfScope ps(KC_QKV_FINALIZE, st);
+        qkv_finalize_kernel<AT><<<T.nA + 2 * R, 256, 0, st>>>(ws.Pq, ws.Pk, ws.Pv, ga.split, pstride,
+                                                              T.nA, R, d, dh, ws.tables + T.offA,
+                                                              dpos, ws.rope, qb, kb, vb);
+        SPIDER_LAUNCHED("qkv_finalize");
+      }
+      {
+        ProfScope ps(KC_ATTENTION, st);
+        AttnArgs aa{qb, ws.tables + T.offA, kb, vb, dstart, ob, T.nA, R, c.H, dh, d,
+                    (float)(1.0 / std::sqrt((double)dh))};
+        hipError_t e = bf16 ? launch_attention_bf16(aa, st) : launch_attention_f32(aa, max_s, st);
+        SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "attention: %s", hipGetErrorString(e));
+      }
+      GemmArgs go{};
+      go.ngroups = 1;
+      go.K = d;
+      go.lda = d;
+      go.epilogue = EPI_PARTIAL_F32;
+      go.g[0] = GemmGroup{ob, nullptr, T.nA, w.wo, nullptr, d, ws.Pres, d, pstride, 0, 0, 0};
+      {
+        ProfScope ps(KC_GEMM_O, st);
+        hipError_t e = gemm(go);
+        SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_o: %s", hipGetErrorString(e));
+      }
+      pend_split = go.split;
+      pend_slot = ws.tables + T.offSlotA;
+    }
+    if (T.nF > 0) {
+      {
+        ProfScope ps(KC_RMSNORM, st);
+        norm_kernel<AT><<<R, 256, 0, st>>>(h, d, ws.Pres, pend_split, pstride, pend_slot,
+                                           w.ffn_norm, c.eps, ws.tables + T.offSlotF, 0, xn);
+        SPIDER_LAUNCHED("rmsnorm(ffn)");
+        pend_split = 0;
+        pend_slot = nullptr;
+      }
+      GemmArgs gu{};
+      gu.ngroups = 1;
+      gu.K = d;
+      gu.lda = d;
+      gu.epilogue = EPI_SWIGLU;
+      gu.g[0] = GemmGroup{xn, nullptr, T.nF, w.wg, w.wu, c.d_ff, act, c.d_ff, 0, 0, 0, 0};
+      {
+        ProfScope ps(KC_GEMM_GATEUP, st);
+        hipError_t e = gemm(gu);
+        SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_gateup: %s", hipGetErrorString(e));
+      }
+      GemmArgs gd{};
+      gd.ngroups = 1;
+      gd.K = c.d_ff;
+      gd.lda = c.d_ff;
+      gd.epilogue = EPI_PARTIAL_F32;
+      gd.g[0] = GemmGroup{act, nullptr, T.nF, w.wd, nullptr, d, ws.Pres, d, pstride, 0, 0, 0};
+      {
+        ProfScope ps(KC_GEMM_DOWN, st);
+        hipError_t e = gemm(gd);
+        SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_down: %s", hipGetErrorString(e));
+      }
+      pend_split = gd.split;
+      pend_slot = ws.tables + T.offSlotF;
+    }
+  }
+  if (pend_split > 0) {
+    ProfScope ps(KC_RESIDUAL, st);
+    norm_kernel<AT><<<R, 256, 0, st>>>(h, d, ws.Pres, pend_split, pstride, pend_slot, nullptr, 0.f,
+                                       nullptr, 0, static_cast<AT*>(nullptr));
+    SPIDER_LAUNCHED("residual_add");
+  }
+  return SPIDER_OK;
+}
+
+}  // namespace
+}  // namespace spider
+
+using namespace spider;
+
+extern "C" size_t spider_prefill_workspace_size(const spider_decoder_cfg* cfg, int B, int rows) {
+  if (!cfg || cfg->L < 1 || cfg->d < 1 || cfg->H < 1 || cfg->d % cfg->H || B < 1 || rows < 0)
+    return 0;
+  return prefill_layout(*cfg, std::max(rows, 1), nullptr).bytes;
+}
+
+extern "C" spider_status spider_prefill(const spider_decoder_cfg* cfg,
+                                        const spider_layer_weights* layers, int B,
+                                        const int32_t* cu_seqlens, const void* x,
+                                        const uint8_t* codes, float* h_out, void* workspace,
+                                        size_t workspace_bytes, spider_stream stream) {
+  clear_error();
+  spider_status v = validate_cfg(cfg);
+  if (v != SPIDER_OK) return v;
+  SPIDER_REQUIRE(B >= 1, SPIDER_ERR_INVALID_ARG, "spider_prefill: B must be >= 1");
+  SPIDER_REQUIRE(cu_seqlens && layers, SPIDER_ERR_INVALID_ARG,
+                 "spider_prefill: cu_seqlens and layers must be non-null");
+  SPIDER_REQUIRE(cu_seqlens[0] == 0, SPIDER_ERR_SHAPE, "spider_prefill: cu_seqlens[0] must be 0");
+  for (int b = 0; b < B; ++b)
+    SPIDER_REQUIRE(cu_seqlens[b + 1] >= cu_seqlens[b], SPIDER_ERR_SHAPE,
+                   "spider_prefill: cu_seqlens must be non-decreasing");
+  const int R = cu_seqlens[B];
+  if (R == 0) return SPIDER_OK;
+  SPIDER_REQUIRE(x && h_out && codes, SPIDER_ERR_INVALID_ARG,
+                 "spider_prefill: x, h_out and codes must be non-null");
+  for (int l = 0; l < cfg->L; ++l) {
+    const spider_layer_weights& w = layers[l];
+    SPIDER_REQUIRE(w.attn_norm && w.wq && w.wk && w.wv && w.wo && w.ffn_norm && w.wg && w.wu && w.wd,
+                   SPIDER_ERR_INVALID_ARG, "spider_prefill: null weight pointer in layer %d", l);
+  }
+  for (size_t i = 0; i < (size_t)cfg->L * R; ++i)
+    SPIDER_REQUIRE(codes[i] <= 3, SPIDER_ERR_INVALID_ARG,
+                   "spider_prefill: code %u at %zu is not in [0, 3]", (unsigned)codes[i], i);
+  const PrefillWs need = prefill_layout(*cfg, R, nullptr);
+  SPIDER_REQUIRE(workspace && workspace_bytes >= need.bytes, SPIDER_ERR_WORKSPACE,
+                 "spider_prefill: workspace of %zu bytes needed, %zu given", need.bytes,
+                 workspace_bytes);
+  SPIDER_REQUIRE(((uintptr_t)workspace % 256) == 0, SPIDER_ERR_WORKSPACE,
+                 "spider_prefill: workspace must be 256-byte aligned");
+  if (cfg->dtype == SPIDER_BF16) {
+    SPIDER_REQUIRE(((uintptr_t)x % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                   "spider_prefill: x must be 16-byte aligned");
+    for (int l = 0; l < cfg->L; ++l) {
+      const spider_layer_weights& w = layers[l];
+      const void* m[7] = {w.wq, w.wk, w.wv, w.wo, w.wg, w.wu, w.wd};
+      for (int i = 0; i < 7; ++i)
+        SPIDER_REQUIRE(((uintptr_t)m[i] % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                       "spider_prefill: weight matrices must be 16-byte aligned (layer %d)", l);
+    }
+  }
+  const PrefillWs ws = prefill_layout(*cfg, R, reinterpret_cast<char*>(workspace));
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (cfg->dtype == SPIDER_BF16)
+    return run_prefill<uint16_t>(*cfg, layers, B, cu_seqlens, x, codes, h_out, ws, st);
+  return run_prefill<float>(*cfg, layers, B, cu_seqlens, x, codes, h_out, ws, st);
+}

@@ -1,0 +1,694 @@
+// MSV-Prune scoring (Sec. 4.1): anchor scores, anchor top-k (Eq. 1),
+// K-means on last-layer features (Sec. 4.1.2), anchor max-similarity and the
+// per-token multi-layer similarity score of Eq. 3 in its factored form:
+//   mean_{j in C} S_ij = sum_l u^l_i . mu^l_C + m_i + mean_{j in C} m_j,
+//   u^l_i = F^l_i / |F^l_i|,  mu^l_C = mean_{j in C} u^l_j.
+//
+// Kernels (all per tile g, enqueued in this order):
+//   score_prep     grid (ceil(n/4), G) x 256: a_i (sequential fp32 head sum,
+//                  then one IEEE division) and 1/|F^l_i| for every tapped layer.
+//   anchor_topk    grid G x 1024: LDS bitonic sort of 64-bit keys
+//                  (~order(a), i); the first n_anchor are the anchors; block
+//                  scans write the ascending anchor and non-anchor lists.
+//   anchor_maxsim  grid (ceil(n/32), G) x 256: m_i = max_p u_i . u_p.  bf16
+//                  features use v_mfma_f32_32x32x16_bf16 on the raw rows
+//                  (exact products, fp32 accumulation) scaled by the two
+//                  inverse norms; fp32 features use a wave-per-row FMA loop.
+//   kmeans         grid G x (512|256): Lloyd passes; each wave keeps every
+//                  centroid's slice of dimensions in registers, processes
+//                  rows round-robin, and the per-wave partial sums are
+//                  combined in LDS in fixed wave order (deterministic).
+//   score_final    grid G x (512|256): cluster means of unit rows per tapped
+//                  layer (same fixed-order reduction), cluster mean of m, and
+//                  the factored score of every non-anchor row.
+//
+// Lane-to-dimension map used by kmeans/score_final: lane l owns VPL
+// dimensions, in chunks of 8: dims {c*512 + 8*l + e : c < VPL/8, e < 8}.
+#include <cfloat>
+#include <cmath>
+
+#include "common.h"
+
+namespace spider {
+namespace {
+
+template <typename FT>
+struct Feat;
+template <>
+struct Feat<float> {
+  static constexpr spider_dtype dt = SPIDER_F32;
+  // 8 consecutive elements -> fp32
+  __device__ static inline void load8(const float* p, float* o) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  }
+  __device__ static inline float load1(const float* p) { return *p; }
+};
+template <>
+struct Feat<uint16_t> {
+  static constexpr spider_dtype dt = SPIDER_BF16;
+  __device__ static inline void load8(const uint16_t* p, float* o) {
+    const uint4 v = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = __uint_as_float(w[i] << 16);
+      o[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+  __device__ static inline float load1(const uint16_t* p) { return bf16_bits_to_f32(*p); }
+};
+
+struct FeatArgs {
+  const void* ptr[8];
+  int64_t stride_g, stride_row;
+  int row0;
+};
+
+template <typename FT>
+__device__ inline const FT* feat_row(const FeatArgs& fa, int l, int g, int i) {
+  return reinterpret_cast<const FT*>(fa.ptr[l]) + (int64_t)g * fa.stride_g +
+         (int64_t)(fa.row0 + i) * fa.stride_row;
+}
+
+// Load this lane's VPL dims of a row (zeros beyond d).
+template <typename FT, int VPL>
+__device__ inline void load_slice(const FT* row, int d, int lane, float* x) {
+#pragma unroll
+  for (int c = 0; c < VPL / 8; ++c) {
+    const int base = c * 512 + lane * 8;
+    if (base + 8 <= d) {
+      Feat<FT>::load8(row + base, x + 8 * c);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[8 * c + e] = (base + e < d) ? Feat<FT>::load1(row + base + e) : 0.f;
+    }
+  }
+}
+
+__device__ inline int slice_dim(int v, int lane) { return (v >> 3) * 512 + lane * 8 + (v & 7); }
+
+// ------------------------------------------------------------- score_prep
+template <typename FT>
+__global__ void __launch_bounds__(256) score_prep_kernel(
+    int n, int H, int d, int n_layers, const float* __restrict__ attn, int64_t as_g,
+    int64_t as_h, int col0, FeatArgs fa, float* __restrict__ a_out, float* __restrict__ nu) {
+  const int g = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + wave;
+  if (i >= n) return;
+  for (int l = 0; l < n_layers; ++l) {
+    const FT* row = feat_row<FT>(fa, l, g, i);
+    float ss = 0.f;
+    for (int c = lane; c < d; c += 64) {
+      const float v = Feat<FT>::load1(row + c);
+      ss = fmaf(v, v, ss);
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) nu[((int64_t)g * n_layers + l) * n + i] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
+  }
+  if (lane == 0) {
+    const float* col = attn + (int64_t)g * as_g + col0 + i;
+    float acc = 0.f;
+    for (int h = 0; h < H; ++h) acc = __fadd_rn(acc, col[(int64_t)h * as_h]);
+    a_out[(int64_t)g * n + i] = __fdiv_rn(acc, (float)H);
+  }
+}
+
+// ------------------------------------------------------------- anchor_topk
+constexpr int kMaxN = 4096;
+
+__device__ inline void block_bitonic_sort(uint64_t* keys, int N) {
+  for (int k = 2; k <= N; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int t = threadIdx.x; t < N / 2; t += blockDim.x) {
+        const int i = (t / j) * 2 * j + (t % j);
+        const int p = i + j;
+        const bool up = (i & k) == 0;
+        const uint64_t x = keys[i], y = keys[p];
+        if ((x > y) == up) {
+          keys[i] = y;
+          keys[p] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Exclusive scan of flags[0..n) (values 0/1) into pos[], returns the total.
+// Uses `scratch` (>= blockDim/64 + 1 ints of LDS).
+template <typename IT>
+__device__ inline int block_scan_flags(const IT* flags, IT* pos, int n, int* scratch) {
+  // each thread handles a contiguous chunk
+  const int T = blockDim.x;
+  const int per = (n + T - 1) / T;
+  const int beg = threadIdx.x * per;
+  const int end = min(n, beg + per);
+  int local = 0;
+  for (int i = beg; i < end; ++i) local += flags[i];
+  // inclusive scan across the block of `local`
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int v = local;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  if (lane == 63) scratch[wave] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int w = 0; w < T / 64; ++w) {
+      const int t = scratch[w];
+      scratch[w] = run;
+      run += t;
+    }
+    scratch[T / 64] = run;
+  }
+  __syncthreads();
+  int run = scratch[wave] + v - local;
+  for (int i = beg; i < end; ++i) {
+    pos[i] = (IT)run;
+    run += flags[i];
+  }
+  const int total = scratch[T / 64];
+  __syncthreads();
+  return total;
+}
+
+__global__ void __launch_bounds__(1024) anchor_topk_kernel(int n, int n_anchor,
+                                                           const float* __restrict__ a,
+                                                           int32_t* __restrict__ cluster_out,
+                                                           float* __restrict__ s_out,
+                                                           int32_t* __restrict__ anc_list,
+                                                           int32_t* __restrict__ rest_list) {
+  __shared__ uint64_t keys[kMaxN];
+  __shared__ uint16_t flag[kMaxN];
+  __shared__ uint16_t pos[kMaxN];
+  __shared__ int scratch[17];
+  const int g = blockIdx.x;
+  int N = 1;
+  while (N < n) N <<= 1;
+  for (int i = threadIdx.x; i < N; i += blockDim.x) {
+    uint64_t k = ~0ull;
+    if (i < n) k = ((uint64_t)(~float_order_key(a[(int64_t)g * n + i])) << 32) | (uint32_t)i;
+    keys[i] = k;
+  }
+  __syncthreads();
+  block_bitonic_sort(keys, N);
+  for (int p = threadIdx.x; p < n; p += blockDim.x)
+    flag[(int)(keys[p] & 0xFFFFFFFFu)] = (uint16_t)(p < n_anchor);
+  __syncthreads();
+  const int na = block_scan_flags(flag, pos, n, scratch);
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int64_t o = (int64_t)g * n;
+    if (flag[i]) {
+      anc_list[o + pos[i]] = i;
+      cluster_out[o + i] = -1;
+      s_out[o + i] = INFINITY;
+    } else {
+      rest_list[o + (i - pos[i])] = i;
+      cluster_out[o + i] = 0;
+    }
+  }
+  (void)na;
+}
+
+// ------------------------------------------------------------- anchor_maxsim
+// bf16: per block 32 data rows; the 4 waves split the anchor tiles of 32.
+__global__ void __launch_bounds__(256) anchor_maxsim_bf16_kernel(
+    int n, int d, int n_anchor, FeatArgs fa, int last, const float* __restrict__ nu_last,
+    int64_t nu_stride_g, const int32_t* __restrict__ anc_list, float* __restrict__ mvec) {
+  __shared__ float red[4][32];
+  const int g = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r0 = blockIdx.x * 32;
+  const int hi = lane >> 5, lo = lane & 31;
+  const int my_row = r0 + lo;  // data row owned by this lane (B operand / output column)
+  const bool row_ok = my_row < n;
+  const uint16_t* rowp =
+      reinterpret_cast<const uint16_t*>(feat_row<uint16_t>(fa, last, g, row_ok ? my_row : 0));
+  const float* nu_g = nu_last + (int64_t)g * nu_stride_g;
+  float best = -INFINITY;
+  const int n_at = (n_anchor + 31) / 32;
+  for (int at = wave; at < n_at; at += 4) {
+    const int p_idx = at * 32 + lo;  // anchor owned by this lane for the A operand
+    const bool anc_ok = p_idx < n_anchor;
+    const int prow = anc_ok ? anc_list[(int64_t)g * n + p_idx] : 0;
+    const uint16_t* ap = feat_row<uint16_t>(fa, last, g, prow);
+    floatx16 acc = {};
+    for (int k0 = 0; k0 < d; k0 += 64) {
+      // this lane covers k in [k0 + 32*hi, k0 + 32*hi + 32) as 4 chunks of 8;
+      // A (anchors) and B (rows) use the same k permutation.
+      bf16x8 av[4], bv[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int kk = k0 + 32 * hi + 8 * c;
+        uint4 ua = make_uint4(0, 0, 0, 0), ub = make_uint4(0, 0, 0, 0);
+        if (kk + 8 <= d) {
+          if (anc_ok) ua = *reinterpret_cast<const uint4*>(ap + kk);
+          if (row_ok) ub = *reinterpret_cast<const uint4*>(rowp + kk);
+        }
+        av[c] = __builtin_bit_cast(bf16x8, ua);
+        bv[c] = __builtin_bit_cast(bf16x8, ub);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[c], bv[c], acc, 0, 0, 0);
+    }
+    // acc[r]: anchor 8*(r/4) + 4*hi + r%4 of this tile, data row = lo
+    const float nu_r = row_ok ? nu_g[my_row] : 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int pa = at * 32 + 8 * (r >> 2) + 4 * hi + (r & 3);
+      if (pa < n_anchor) {
+        const float nu_p = nu_g[anc_list[(int64_t)g * n + pa]];
+        best = fmaxf(best, acc[r] * nu_r * nu_p);
+      }
+    }
+  }
+  best = fmaxf(best, __shfl_xor(best, 32, 64));
+  if (hi == 0) red[wave][lo] = best;
+  __syncthreads();
+  if (threadIdx.x < 32) {
+    float b = red[0][threadIdx.x];
+    for (int w = 1; w < 4; ++w) b = fmaxf(b, red[w][threadIdx.x]);
+    const int row = r0 + threadIdx.x;
+    if (row < n) mvec[(int64_t)g * n + row] = n_anchor > 0 ? b : 0.f;
+  }
+}
+
+// fp32 features: one wave per data row, loop over anchors.
+__global__ void __launch_bounds__(256) anchor_maxsim_f32_kernel(
+    int n, int d, int n_anchor, FeatArgs fa, int last, const float* __restrict__ nu_last,
+    int64_t nu_stride_g, const int32_t* __restrict__ anc_list, float* __restrict__ mvec) {
+  const int g = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + wave;
+  if (i >= n) return;
+  const float* row = feat_row<float>(fa, last, g, i);
+  const float* nu_g = nu_last + (int64_t)g * nu_stride_g;
+  float best = -INFINITY;
+  for (int q = 0; q < n_anchor; ++q) {
+    const int p = anc_list[(int64_t)g * n + q];
+    const float* pr = feat_row<float>(fa, last, g, p);
+    float dot = 0.f;
+    for (int c = lane; c < d; c += 64) dot = fmaf(row[c], pr[c], dot);
+    dot = wave_sum(dot);
+    best = fmaxf(best, dot * nu_g[i] * nu_g[p]);
+  }
+  if (lane == 0) mvec[(int64_t)g * n + i] = n_anchor > 0 ? best : 0.f;
+}
+
+// ------------------------------------------------------------- shared reduction
+// Adds the per-wave partial sums psum[K][VPL] (lane slice) into acc[K*d] in LDS
+// in fixed wave order, plus per-wave counts into cnt[K].
+template <int VPL, int KMAX>
+__device__ inline void ordered_wave_reduce(float (&psum)[KMAX][VPL], const int (&pcnt)[KMAX], int K,
+                                           int d, float* acc, int* cnt, int nwaves) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int w = 0; w < nwaves; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) {
+        if (k >= K) break;
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          const int dim = slice_dim(v, lane);
+          if (dim < d) {
+            float* p = acc + k * d + dim;
+            *p = (w == 0) ? psum[k][v] : (*p + psum[k][v]);
+          }
+        }
+        if (lane == 0) cnt[k] = (w == 0) ? pcnt[k] : cnt[k] + pcnt[k];
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------- kmeans
+template <typename FT, int VPL, int KMAX>
+__global__ void kmeans_kernel(int n, int d, int n_anchor, int K, int max_iter, FeatArgs fa,
+                              int last, const int32_t* __restrict__ rest_list,
+                              int32_t* __restrict__ cluster_out) {
+  extern __shared__ float smem[];
+  float* acc = smem;                               // [K*d]
+  int* cnt = reinterpret_cast<int*>(acc + KMAX * d);  // [KMAX]
+  int* flag = cnt + KMAX;                          // [1]
+  int* assign = flag + 1;                          // [m]
+  const int g = blockIdx.x;
+  const int m = n - n_anchor;
+  if (m <= 0) return;
+  const int nwaves = blockDim.x >> 6;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int32_t* U = rest_list + (int64_t)g * n;
+
+  float c[KMAX][VPL];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    if (k < K) {
+      const int j = (int)(((int64_t)k * m) / K);
+      load_slice<FT, VPL>(feat_row<FT>(fa, last, g, U[j]), d, lane, c[k]);
+    }
+  }
+  for (int it = 0; it < max_iter; ++it) {
+    float psum[KMAX][VPL];
+    int pcnt[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      pcnt[k] = 0;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) psum[k][v] = 0.f;
+    }
+    int changed = 0;
+    for (int j = wave; j < m; j += nwaves) {
+      float x[VPL];
+      load_slice<FT, VPL>(feat_row<FT>(fa, last, g, U[j]), d, lane, x);
+      float dist[KMAX];
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) {
+        float s = 0.f;
+        if (k < K) {
+#pragma unroll
+          for (int v = 0; v < VPL; ++v) {
+            const float t = x[v] - c[k][v];
+            s = fmaf(t, t, s);
+          }
+        }
+        dist[k] = s;
+      }
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k)
+        if (k < K) dist[k] = wave_sum(dist[k]);
+      int best = 0;
+      float bd = dist[0];
+#pragma unroll
+      for (int k = 1; k < KMAX; ++k)
+        if (k < K && dist[k] < bd) {
+          bd = dist[k];
+          best = k;
+        }
+      if (it == 0 || assign[j] != best) changed = 1;
+      __builtin_amdgcn_wave_barrier();
+      if (lane == 0) assign[j] = best;
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k)
+        if (k == best) {
+          pcnt[k] += 1;
+#pragma unroll
+          for (int v = 0; v < VPL; ++v) psum[k][v] += x[v];
+        }
+    }
+    if (threadIdx.x == 0) *flag = 0;
+    __syncthreads();
+    if (lane == 0 && changed) atomicOr(flag, 1);
+    __syncthreads();
+    const int any = *flag;
+    __syncthreads();
+    if (!any) break;
+    ordered_wave_reduce<VPL, KMAX>(psum, pcnt, K, d, acc, cnt, nwaves);
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      if (k < K && cnt[k] > 0) {
+        const float fc = (float)cnt[k];
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          const int dim = slice_dim(v, lane);
+          c[k][v] = dim < d ? __fdiv_rn(acc[k * d + dim], fc) : 0.f;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  for (int j = threadIdx.x; j < m; j += blockDim.x) cluster_out[(int64_t)g * n + U[j]] = assign[j];
+}
+
+// ------------------------------------------------------------- score_final
+template <typename FT, int VPL, int KMAX>
+__global__ void score_final_kernel(int n, int d, int n_anchor, int K, int n_layers, FeatArgs fa,
+                                   const float* __restrict__ nu, const int32_t* __restrict__ rest_list,
+                                   const int32_t* __restrict__ cluster, const float* __restrict__ mvec,
+                                   float* __restrict__ mu_ws, float* __restrict__ s_out,
+                                   float* __restrict__ m_out) {
+  extern __shared__ float smem[];
+  float* acc = smem;                                  // [K*d]
+  int* cnt = reinterpret_cast<int*>(acc + KMAX * d);  // [KMAX]
+  float* mbar = reinterpret_cast<float*>(cnt + KMAX);  // [KMAX]
+  const int g = blockIdx.x;
+  const int m = n - n_anchor;
+  const int nwaves = blockDim.x >> 6;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int32_t* U = rest_list + (int64_t)g * n;
+  const int32_t* cl = cluster + (int64_t)g * n;
+  const float* mv = mvec + (int64_t)g * n;
+  if (m_out)
+    for (int i = threadIdx.x; i < n; i += blockDim.x) m_out[(int64_t)g * n + i] = mv[i];
+  if (m <= 0) return;
+  float* mu_g = mu_ws + (int64_t)g * n_layers * KMAX * d;
+
+  // cluster mean of m (one thread, rows in ascending order)
+  if (threadIdx.x == 0) {
+    float sm[KMAX];
+    int ct[KMAX];
+    for (int k = 0; k < KMAX; ++k) {
+      sm[k] = 0.f;
+      ct[k] = 0;
+    }
+    for (int j = 0; j < m; ++j) {
+      const int i = U[j];
+      const int k = cl[i];
+      sm[k] += mv[i];
+      ct[k] += 1;
+    }
+    for (int k = 0; k < KMAX; ++k) mbar[k] = ct[k] ? __fdiv_rn(sm[k], (float)ct[k]) : 0.f;
+  }
+  // cluster means of unit rows, layer by layer
+  for (int l = 0; l < n_layers; ++l) {
+    const float* nu_l = nu + ((int64_t)g * n_layers + l) * n;
+    float psum[KMAX][VPL];
+    int pcnt[KMAX];
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      pcnt[k] = 0;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) psum[k][v] = 0.f;
+    }
+    for (int j = wave; j < m; j += nwaves) {
+      const int i = U[j];
+      const int k_i = cl[i];
+      float x[VPL];
+      load_slice<FT, VPL>(feat_row<FT>(fa, l, g, i), d, lane, x);
+      const float s = nu_l[i];
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k)
+        if (k == k_i) {
+          pcnt[k] += 1;
+#pragma unroll
+          for (int v = 0; v < VPL; ++v) psum[k][v] = fmaf(x[v], s, psum[k][v]);
+        }
+    }
+    ordered_wave_reduce<VPL, KMAX>(psum, pcnt, K, d, acc, cnt, nwaves);
+    for (int t = threadIdx.x; t < K * d; t += blockDim.x) {
+      const int k = t / d;
+      mu_g[((int64_t)l * KMAX + k) * d + (t - k * d)] = cnt[k] ? __fdiv_rn(acc[t], (float)cnt[k]) : 0.f;
+    }
+    __syncthreads();
+  }
+  __threadfence_block();
+  __syncthreads();
+  // scores of non-anchor rows
+  for (int j = wave; j < m; j += nwaves) {
+    const int i = U[j];
+    const int k_i = cl[i];
+    float s = 0.f;
+    for (int l = 0; l < n_layers; ++l) {
+      float x[VPL];
+      load_slice<FT, VPL>(feat_row<FT>(fa, l, g, i), d, lane, x);
+      const float* mu = mu_g + ((int64_t)l * KMAX + k_i) * d;
+      float dot = 0.f;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) {
+        const int dim = slice_dim(v, lane);
+        if (dim < d) dot = fmaf(x[v], mu[dim], dot);
+      }
+      dot = wave_sum(dot);
+      s += dot * nu[((int64_t)g * n_layers + l) * n + i];
+    }
+    if (lane == 0) s_out[(int64_t)g * n + i] = s + mv[i] + mbar[k_i];
+  }
+}
+
+struct ScoreWs {
+  float* nu;
+  int32_t* anc;
+  int32_t* rest;
+  float* mvec;
+  float* mu;
+};
+
+size_t score_ws_layout(int G, int n, int d, int n_layers, ScoreWs* w, char* base) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes, 256);
+    return base ? base + o : nullptr;
+  };
+  char* p_nu = take((size_t)G * n_layers * n * 4);
+  char* p_anc = take((size_t)G * n * 4);
+  char* p_rest = take((size_t)G * n * 4);
+  char* p_mvec = take((size_t)G * n * 4);
+  char* p_mu = take((size_t)G * n_layers * 8 * d * 4);
+  if (w) {
+    w->nu = reinterpret_cast<float*>(p_nu);
+    w->anc = reinterpret_cast<int32_t*>(p_anc);
+    w->rest = reinterpret_cast<int32_t*>(p_rest);
+    w->mvec = reinterpret_cast<float*>(p_mvec);
+    w->mu = reinterpret_cast<float*>(p_mu);
+  }
+  return off;
+}
+
+template <typename FT, int VPL, int KMAX>
+hipError_t launch_cluster_kernels(int G, int n, int d, int n_anchor, int K, int max_iter,
+                                  int n_layers, const FeatArgs& fa, const ScoreWs& ws,
+                                  int32_t* cluster_out, float* s_out, float* m_out, hipStream_t st) {
+  const int threads = (KMAX * VPL <= 64) ? 512 : 256;
+  const int m = n - n_anchor;
+  {
+    ProfScope ps(KC_KMEANS, st);
+    const size_t sh = (size_t)KMAX * d * 4 + KMAX * 4 + 4 + (size_t)(m > 0 ? m : 1) * 4;
+    kmeans_kernel<FT, VPL, KMAX><<<G, threads, sh, st>>>(n, d, n_anchor, K, max_iter, fa,
+                                                        n_layers - 1, ws.rest, cluster_out);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  {
+    ProfScope ps(KC_SCORE_FINAL, st);
+    const size_t sh = (size_t)KMAX * d * 4 + KMAX * 8;
+    score_final_kernel<FT, VPL, KMAX><<<G, threads, sh, st>>>(n, d, n_anchor, K, n_layers, fa,
+                                                             ws.nu, ws.rest, cluster_out, ws.mvec,
+                                                             ws.mu, s_out, m_out);
+    return hipGetLastError();
+  }
+}
+
+template <typename FT>
+hipError_t dispatch_cluster(int G, int n, int d, int n_anchor, int K, int max_iter, int n_layers,
+                            const FeatArgs& fa, const ScoreWs& ws, int32_t* cl, float* s,
+                            float* mo, hipStream_t st) {
+  if (d <= 512)
+    return launch_cluster_kernels<FT, 8, 8>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
+  if (d <= 1024) {
+    if (K <= 4)
+      return launch_cluster_kernels<FT, 16, 4>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
+    return launch_cluster_kernels<FT, 16, 8>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
+  }
+  return launch_cluster_kernels<FT, 32, 4>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
+}
+
+}  // namespace
+}  // namespace spider
+
+using namespace spider;
+
+extern "C" size_t spider_score_workspace_size(int G, int n, int d_v, int n_layers, int K) {
+  (void)K;
+  if (G <= 0 || n <= 0 || d_v <= 0 || n_layers <= 0) return 0;
+  return score_ws_layout(G, n, d_v, n_layers, nullptr, nullptr);
+}
+
+extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers,
+                                      const float* cls_attn, int64_t attn_stride_g,
+                                      int64_t attn_stride_h, int attn_col0,
+                                      const void* const* feats, spider_dtype feat_dtype,
+                                      int64_t feat_stride_g, int64_t feat_stride_row, int feat_row0,
+                                      int n_anchor, int K, int kmeans_max_iter, float* a_out,
+                                      int32_t* cluster_out, float* s_out, float* m_out,
+                                      void* workspace, size_t workspace_bytes,
+                                      spider_stream stream) {
+  clear_error();
+  SPIDER_REQUIRE(G >= 1 && n >= 1 && H >= 1 && d_v >= 1 && n_layers >= 1, SPIDER_ERR_INVALID_ARG,
+                 "spider_score: G, n, H, d_v and n_layers must be >= 1");
+  SPIDER_REQUIRE(n <= kMaxN, SPIDER_ERR_UNSUPPORTED, "spider_score: n = %d exceeds 4096", n);
+  SPIDER_REQUIRE(d_v <= 2048, SPIDER_ERR_UNSUPPORTED, "spider_score: d_v = %d exceeds 2048", d_v);
+  SPIDER_REQUIRE(n_layers <= 8, SPIDER_ERR_UNSUPPORTED, "spider_score: at most 8 tapped layers");
+  SPIDER_REQUIRE(K >= 1 && K <= 8, SPIDER_ERR_UNSUPPORTED, "spider_score: K must be in [1, 8]");
+  SPIDER_REQUIRE(!(d_v > 1024 && K > 4), SPIDER_ERR_UNSUPPORTED,
+                 "spider_score: K > 4 needs d_v <= 1024");
+  SPIDER_REQUIRE(n_anchor >= 0 && n_anchor <= n, SPIDER_ERR_SHAPE,
+                 "spider_score: n_anchor = %d outside [0, n = %d]", n_anchor, n);
+  SPIDER_REQUIRE(kmeans_max_iter >= 1, SPIDER_ERR_INVALID_ARG,
+                 "spider_score: kmeans_max_iter must be >= 1");
+  SPIDER_REQUIRE(cls_attn && feats && a_out && cluster_out && s_out, SPIDER_ERR_INVALID_ARG,
+                 "spider_score: null pointer argument");
+  SPIDER_REQUIRE(feat_dtype == SPIDER_F32 || feat_dtype == SPIDER_BF16, SPIDER_ERR_INVALID_ARG,
+                 "spider_score: bad feature dtype");
+  SPIDER_REQUIRE(attn_col0 >= 0 && feat_row0 >= 0 && attn_stride_h >= attn_col0 + n &&
+                     attn_stride_g >= (int64_t)H * attn_stride_h,
+                 SPIDER_ERR_SHAPE, "spider_score: attention strides do not cover [H, col0 + n]");
+  SPIDER_REQUIRE(feat_stride_row >= d_v && feat_stride_g >= (int64_t)(feat_row0 + n) * feat_stride_row,
+                 SPIDER_ERR_SHAPE, "spider_score: feature strides do not cover [row0 + n, d_v]");
+  SPIDER_REQUIRE(feat_stride_row % 8 == 0 && feat_stride_g % 8 == 0 && d_v % 8 == 0,
+                 SPIDER_ERR_UNSUPPORTED,
+                 "spider_score: d_v and the feature strides must be multiples of 8 elements");
+  for (int l = 0; l < n_layers; ++l) {
+    SPIDER_REQUIRE(feats[l] != nullptr, SPIDER_ERR_INVALID_ARG, "spider_score: feats[%d] is null", l);
+    SPIDER_REQUIRE(((uintptr_t)feats[l] % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                   "spider_score: feats[%d] must be 16-byte aligned", l);
+  }
+  const size_t need = score_ws_layout(G, n, d_v, n_layers, nullptr, nullptr);
+  SPIDER_REQUIRE(workspace && workspace_bytes >= need, SPIDER_ERR_WORKSPACE,
+                 "spider_score: workspace of %zu bytes needed, %zu given", need, workspace_bytes);
+  SPIDER_REQUIRE(((uintptr_t)workspace % 256) == 0, SPIDER_ERR_WORKSPACE,
+                 "spider_score: workspace must be 256-byte aligned");
+
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  ScoreWs ws;
+  score_ws_layout(G, n, d_v, n_layers, &ws, reinterpret_cast<char*>(workspace));
+  FeatArgs fa;
+  for (int l = 0; l < 8; ++l) fa.ptr[l] = l < n_layers ? feats[l] : nullptr;
+  fa.stride_g = feat_stride_g;
+  fa.stride_row = feat_stride_row;
+  fa.row0 = feat_row0;
+  const int last = n_layers - 1;
+
+  {
+    ProfScope ps(KC_SCORE_PREP, st);
+    dim3 grid(ceil_div(n, 4), G);
+    if (feat_dtype == SPIDER_BF16)
+      score_prep_kernel<uint16_t><<<grid, 256, 0, st>>>(n, H, d_v, n_layers, cls_attn, attn_stride_g,
+                                                       attn_stride_h, attn_col0, fa, a_out, ws.nu);
+    else
+      score_prep_kernel<float><<<grid, 256, 0, st>>>(n, H, d_v, n_layers, cls_attn, attn_stride_g,
+                                                    attn_stride_h, attn_col0, fa, a_out, ws.nu);
+    SPIDER_LAUNCHED("score_prep");
+  }
+  {
+    ProfScope ps(KC_ANCHOR_TOPK, st);
+    anchor_topk_kernel<<<G, 1024, 0, st>>>(n, n_anchor, a_out, cluster_out, s_out, ws.anc, ws.rest);
+    SPIDER_LAUNCHED("anchor_topk");
+  }
+  {
+    ProfScope ps(KC_MAXSIM, st);
+    const float* nu_last = ws.nu + (size_t)last * n;
+    const int64_t nu_stride = (int64_t)n_layers * n;
+    if (feat_dtype == SPIDER_BF16)
+      anchor_maxsim_bf16_kernel<<<dim3(ceil_div(n, 32), G), 256, 0, st>>>(
+          n, d_v, n_anchor, fa, last, nu_last, nu_stride, ws.anc, ws.mvec);
+    else
+      anchor_maxsim_f32_kernel<<<dim3(ceil_div(n, 4), G), 256, 0, st>>>(
+          n, d_v, n_anchor, fa, last, nu_last, nu_stride, ws.anc, ws.mvec);
+    SPIDER_LAUNCHED("anchor_maxsim");
+  }
+  hipError_t e = feat_dtype == SPIDER_BF16
+                     ? dispatch_cluster<uint16_t>(G, n, d_v, n_anchor, K, kmeans_max_iter, n_layers,
+                                                  fa, ws, cluster_out, s_out, m_out, st)
+                     : dispatch_cluster<float>(G, n, d_v, n_anchor, K, kmeans_max_iter, n_layers, fa,
+                                               ws, cluster_out, s_out, m_out, st);
+  SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "spider_score: cluster kernels failed: %s",
+                 hipGetErrorString(e));
+  return SPIDER_OK;
+}

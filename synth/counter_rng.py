@@ -31,7 +31,12 @@ def _s64(v: int) -> int:
 _GOLDEN_S, _C1_S, _C2_S = _s64(_GOLDEN), _s64(_C1), _s64(_C2)
 # sqrt(var) of the centred sum of four independent U{0..65535}: 65536/sqrt(3)
 _IH4_STD = 37837.23112659009
-_CHUNK = 1 << 24
+_CHUNK = 1 << 20          # CPU chunk (cache-sized temporaries)
+_CHUNK_GPU = 1 << 26
+
+
+def _chunk(device) -> int:
+    return _CHUNK_GPU if torch.device(device).type == "cuda" else _CHUNK
 
 
 def _lsr(z: torch.Tensor, k: int) -> torch.Tensor:
@@ -74,8 +79,9 @@ def normal_f32(shape, seed: int, tensor_id: int, std: float = 0.02,
         numel *= int(s)
     _check(seed, tensor_id, numel)
     out = torch.empty(numel, dtype=torch.float32, device=device)
-    for st in range(0, numel, _CHUNK):
-        n = min(_CHUNK, numel - st)
+    ch = _chunk(device)
+    for st in range(0, numel, ch):
+        n = min(ch, numel - st)
         out[st:st + n] = _normal_chunk(seed, tensor_id, st, n, std, device)
     return out.view(*shape)
 
@@ -95,7 +101,8 @@ def normal_bf16(shape, seed: int, tensor_id: int, std: float = 0.02,
         numel *= int(s)
     _check(seed, tensor_id, numel)
     out = torch.empty(numel, dtype=torch.bfloat16, device=device)
-    for st in range(0, numel, _CHUNK):
-        n = min(_CHUNK, numel - st)
+    ch = _chunk(device)
+    for st in range(0, numel, ch):
+        n = min(ch, numel - st)
         out[st:st + n] = f32_to_bf16_rne(_normal_chunk(seed, tensor_id, st, n, std, device))
     return out.view(*shape)

@@ -1,0 +1,200 @@
+"""C ABI checks that need no GPU: symbols, host-only entry points, argument validation.
+
+Every validation case below passes arguments that are rejected before the
+library makes any HIP call, so on a machine without a GPU the documented
+status comes back (a HIP call would instead give SPIDER_ERR_HIP).
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import asl_skip as ak
+from oracle import msv_prune as mp
+from synth import get_workload
+from synth.skip_inputs import adaptive_scores, policy_lists, slc_tables
+
+lib_mod = pytest.importorskip("paper_2609_34977_amd._lib")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+OK, INVALID, SHAPE, UNSUPPORTED, WORKSPACE, HIP = 0, 1, 2, 3, 4, 5
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(lib_mod._LIB_PATH):
+        pytest.skip("libspider.so not built")
+    return lib_mod.lib()
+
+
+def test_every_header_symbol_is_exported(L):
+    hdr = open(os.path.join(ROOT, "include", "spider.h")).read()
+    names = set(re.findall(r"\b(spider_[a-z_]+)\s*\(", hdr))
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(L, n), n
+    assert names == set(lib_mod.exported_symbols())
+    assert L.spider_version() >= 100
+
+
+@pytest.mark.parametrize("keep", [0, 1, 16, 64, 128, 192, 576, 1440, 2880])
+def test_budget_matches_oracle(L, keep):
+    assert lib_mod.budget(keep) == mp.budget(keep)
+    assert lib_mod.budget(keep, 1, 2) == mp.budget(keep, 1, 2)
+
+
+def test_budget_rejects_bad_ratio(L):
+    a, c = ctypes.c_int(), ctypes.c_int()
+    assert L.spider_budget(10, 11, 10, ctypes.byref(a), ctypes.byref(c)) == INVALID
+    assert b"r_num" in L.spider_last_error()
+    assert L.spider_budget(-1, 7, 10, ctypes.byref(a), ctypes.byref(c)) == INVALID
+
+
+@pytest.mark.parametrize("name", ["llava15_7b", "llava_next_7b", "synthetic_40"])
+def test_slc_policy_bit_exact_with_oracle(L, name):
+    n_layers = 40 if name == "synthetic_40" else 32
+    sa, sf = slc_tables(policy_lists(name, n_layers), n_layers)
+    sel, tgt = lib_mod.slc_policy(sa, sf, 1e-8)
+    na, nf = ak.slc_normalize(sa, sf, 1e-8)
+    m, osel = ak.skip_targets(na, nf)
+    assert np.array_equal(tgt, m)
+    assert np.array_equal(sel, osel)          # same doubles, bit for bit
+
+
+@pytest.mark.parametrize("wl", ["llava_next_7b", "llava15_13b"])
+def test_plan_skips_bit_exact_with_oracle(L, wl):
+    w = get_workload(wl)
+    n_layers = w.dec.L
+    sa, sf = slc_tables(policy_lists(w.skip["policy"], n_layers), n_layers)
+    na, nf = ak.slc_normalize(sa, sf)
+    m, sel = ak.skip_targets(na, nf)
+    S = adaptive_scores(w, 300)
+    for b in range(w.B):
+        codes, admit = lib_mod.plan_skips(S[b], sel, m, w.skip["w1"], w.skip["w2"],
+                                          w.skip["T_skip"], n_layers)
+        oc, oadmit, _ = ak.plan(S[b], sel, m, w.skip["w1"], w.skip["w2"], w.skip["T_skip"], n_layers)
+        assert np.array_equal(codes, oc)
+        assert np.array_equal(admit, oadmit)
+    frac = (oadmit >= 0).mean()
+    assert 0.2 < frac < 0.7
+
+
+def test_plan_skips_threshold_ties_and_window(L):
+    S = np.array([[1.0, 0.2, 0.0], [0.0, 0.9, 0.3]], np.float32)
+    codes, admit = lib_mod.plan_skips(S, np.array([0.5, 0.5, 1.0, 1.0]), np.array([0, 1, 0, 0], np.uint8),
+                                      1.0, 1.0, 1.5, 4)
+    assert codes.tolist() == [[1, 0, 0], [1, 2, 0], [1, 2, 0], [1, 2, 0]]
+    assert admit.tolist() == [0, 1, -1]
+
+
+def test_plan_skips_validation(L):
+    sel = np.zeros(4)
+    tgt = np.array([0, 1, 2, 0], np.uint8)
+    S = np.zeros((2, 3), np.float32)
+    codes = np.zeros((4, 3), np.uint8)
+    st = L.spider_plan_skips(4, 3, S.ctypes.data, 3, sel.ctypes.data, tgt.ctypes.data, 1.0, 1.0,
+                             1.0, codes.ctypes.data, 3, None)
+    assert st == INVALID and b"target" in L.spider_last_error()
+    st = L.spider_plan_skips(4, 3, S.ctypes.data, 2, sel.ctypes.data, sel.ctypes.data, 1.0, 1.0,
+                             1.0, codes.ctypes.data, 3, None)
+    assert st == SHAPE
+
+
+def _score_call(L, **kw):
+    args = dict(G=1, n=576, H=16, d_v=1024, n_layers=2, attn=0x1000, asg=16 * 577, ash=577,
+                col0=1, dt=1, fsg=577 * 1024, fsr=1024, row0=1, n_anchor=89, K=4, it=10,
+                a=0x1000, cl=0x1000, s=0x1000, m=None, ws=0x100000, wsb=1 << 30)
+    args.update(kw)
+    fp = (ctypes.c_void_p * 8)(*([0x2000] * 8))
+    if kw.get("null_feat"):
+        fp[1] = None
+    return L.spider_score(args["G"], args["n"], args["H"], args["d_v"], args["n_layers"],
+                          args["attn"], args["asg"], args["ash"], args["col0"], fp, args["dt"],
+                          args["fsg"], args["fsr"], args["row0"], args["n_anchor"], args["K"],
+                          args["it"], args["a"], args["cl"], args["s"], args["m"], args["ws"],
+                          args["wsb"], None)
+
+
+def test_score_validation_before_any_hip_call(L):
+    assert _score_call(L, G=0) == INVALID
+    assert _score_call(L, n=5000, asg=16 * 5001, ash=5001, fsg=5001 * 1024) == UNSUPPORTED
+    assert _score_call(L, K=9) == UNSUPPORTED
+    assert _score_call(L, n_anchor=577) == SHAPE
+    assert _score_call(L, it=0) == INVALID
+    assert _score_call(L, a=None) == INVALID
+    assert _score_call(L, null_feat=True) == INVALID
+    assert _score_call(L, ash=100) == SHAPE
+    assert _score_call(L, fsr=1000, fsg=577 * 1000) == SHAPE
+    assert _score_call(L, d_v=1020, fsr=1024) == UNSUPPORTED
+    assert _score_call(L, wsb=16) == WORKSPACE
+    assert b"workspace" in L.spider_last_error()
+    assert _score_call(L, ws=0x100010) == WORKSPACE  # misaligned
+    assert L.spider_score_workspace_size(1, 576, 1024, 2, 4) > 0
+    assert L.spider_score_workspace_size(0, 576, 1024, 2, 4) == 0
+
+
+def _select_call(L, **kw):
+    a = dict(G=1, n=576, cl=0x1000, s=0x1000, na=89, nc=39, K=4, qm=0, idx=0x1000, cnt=0x1000,
+             cap=132, tps=1, src=None, ssg=0, dm=0, dt=1, text=None, nt=0, x=None, cu=None)
+    a.update(kw)
+    return L.spider_select(a["G"], a["n"], a["cl"], a["s"], a["na"], a["nc"], a["K"], a["qm"],
+                           a["idx"], a["cnt"], a["cap"], a["tps"], a["src"], a["ssg"], a["dm"],
+                           a["dt"], a["text"], a["nt"], a["x"], a["cu"], None)
+
+
+def test_select_validation_before_any_hip_call(L):
+    assert _select_call(L, G=0) == INVALID
+    assert _select_call(L, cap=131) == SHAPE
+    assert _select_call(L, qm=2) == INVALID
+    assert _select_call(L, K=0) == UNSUPPORTED
+    assert _select_call(L, na=600) == SHAPE
+    assert _select_call(L, G=5, tps=2) == SHAPE
+    assert _select_call(L, cl=None) == INVALID
+    # assembly arguments
+    assert _select_call(L, src=0x2000, ssg=576 * 4096, dm=4096, x=None, cu=0x1000) == INVALID
+    assert _select_call(L, src=0x2000, ssg=100, dm=4096, x=0x3000, cu=0x1000) == SHAPE
+    assert _select_call(L, src=0x2000, ssg=576 * 4100, dm=4100, x=0x3000, cu=0x1000) == UNSUPPORTED
+    assert _select_call(L, src=0x2000, ssg=576 * 4096, dm=4096, x=0x3000, cu=0x1000, nt=5) == INVALID
+
+
+def _prefill_call(L, cfg, cu, codes, ws_bytes=1 << 40, ws=0x100000, x=0x1000, null_w=False):
+    W = (lib_mod.LayerWeights * cfg.L)()
+    for i in range(cfg.L):
+        W[i] = lib_mod.LayerWeights(*([0x1000] * 9))
+    if null_w:
+        W[cfg.L - 1].wd = None
+    cu = np.ascontiguousarray(cu, np.int32)
+    codes = np.ascontiguousarray(codes, np.uint8)
+    return L.spider_prefill(ctypes.byref(cfg), W, len(cu) - 1, cu.ctypes.data, x, codes.ctypes.data,
+                            0x1000, ws, ws_bytes, None)
+
+
+def test_prefill_validation_before_any_hip_call(L):
+    bf = lib_mod.decoder_cfg(2, 4096, 32, 11008, lib_mod.BF16)
+    codes = np.zeros((2, 10), np.uint8)
+    assert _prefill_call(L, lib_mod.decoder_cfg(2, 4096, 64, 11008, lib_mod.BF16), [0, 10], codes) == UNSUPPORTED
+    assert _prefill_call(L, lib_mod.decoder_cfg(2, 4096, 30, 11008, lib_mod.BF16), [0, 10], codes) == SHAPE
+    assert _prefill_call(L, lib_mod.decoder_cfg(0, 4096, 32, 11008, lib_mod.BF16), [0, 10], codes) == INVALID
+    assert _prefill_call(L, lib_mod.decoder_cfg(2, 4096, 32, 11000, lib_mod.BF16), [0, 10], codes) == UNSUPPORTED
+    assert _prefill_call(L, lib_mod.decoder_cfg(2, 96, 32, 100, lib_mod.F32), [0, 10], codes) == SHAPE
+    assert _prefill_call(L, bf, [1, 10], codes) == SHAPE
+    assert _prefill_call(L, bf, [0, 6, 5], np.zeros((2, 5), np.uint8)) == SHAPE
+    bad = codes.copy()
+    bad[1, 3] = 4
+    assert _prefill_call(L, bf, [0, 10], bad) == INVALID
+    assert _prefill_call(L, bf, [0, 10], codes, null_w=True) == INVALID
+    assert _prefill_call(L, bf, [0, 10], codes, ws_bytes=100) == WORKSPACE
+    assert _prefill_call(L, bf, [0, 10], codes, x=0x1001) == UNSUPPORTED
+    # an empty batch is a no-op
+    assert _prefill_call(L, bf, [0, 0], np.zeros((2, 0), np.uint8)) == OK
+    assert lib_mod.prefill_workspace_size(bf, 1, 192) > 0
+
+
+def test_profiler_host_side(L):
+    lib_mod.profile_enable(True)
+    d = lib_mod.profile_read()
+    assert "gemm_gateup" in d and all(v == (0, 0.0) for v in d.values())
+    lib_mod.profile_enable(False)
+    assert L.spider_profile_read(99, ctypes.byref(ctypes.c_int64()), ctypes.byref(ctypes.c_double())) == INVALID

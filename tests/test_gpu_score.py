@@ -1,0 +1,89 @@
+"""GPU scoring (spider_score) against the oracle on the same seeded inputs.
+
+Bars: head-mean scores and the anchor set bit-exact; K-means assignments
+identical (the oracle also reports how far every decision is from a tie, and
+the inputs are required to keep that margin well above float32 rounding, so
+equality is the expected outcome rather than luck); scores s and anchor
+max-similarities m within 1e-5 relative of the float64 oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+from synth import get_workload
+from synth.vision import vision_inputs
+from gpu_common import need_gpu, oracle_tiles, log
+
+CASES = {
+    # name: (workload, keep, tie_stress, K, r_num, r_den)
+    "tiny": ("tiny", 16, False, 4, 7, 10),
+    "tiny_keep_all": ("tiny", 49, False, 4, 7, 10),
+    "tiny_no_anchor": ("tiny", 16, False, 4, 0, 10),
+    "tiny_K1": ("tiny", 16, False, 1, 7, 10),
+    "llava15_k64": ("llava15_7b", 64, False, 4, 7, 10),
+    "llava15_k128": ("llava15_7b", 128, False, 4, 7, 10),
+    "llava15_k192": ("llava15_7b", 192, False, 4, 7, 10),
+    "llava15_ties": ("llava15_7b", 128, True, 4, 7, 10),
+    "llava15_K8": ("llava15_7b", 128, False, 8, 7, 10),
+    "next_5tiles": ("llava_next_7b", 128, False, 4, 7, 10),
+    "all_anchors": ("llava15_7b", 576, False, 4, 10, 10),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", list(CASES))
+def test_score_parity(case):
+    L = need_gpu()
+    wl, keep, ties, K, rn, rd = CASES[case]
+    w = get_workload(wl, keep=keep)
+    log(f"[score] case={case} G={w.score.G} n={w.score.n} keep={keep} K={K}")
+    attn, feats = vision_inputs(w.score, w.seed, tie_stress=ties)
+    n_anchor = (keep * rn) // rd
+    out = L.score(attn.cuda(), [f.cuda() for f in feats], n_anchor, K, w.score.kmeans_iter)
+    torch.cuda.synchronize()
+    a = out["a"].cpu().numpy()
+    cl = out["cluster"].cpu().numpy()
+    s = out["s"].cpu().numpy()
+    m = out["m"].cpu().numpy()
+    ref = oracle_tiles(attn, feats, keep, rn, rd, K, w.score.kmeans_iter)
+    for g, o in enumerate(ref):
+        assert np.array_equal(a[g], o["a"]), f"tile {g}: anchor scores differ"
+        assert set(np.nonzero(cl[g] < 0)[0]) == set(o["anchors"]), f"tile {g}: anchors differ"
+        if len(o["margin"]):
+            assert o["margin"].min() > 1e-4, "input too close to a K-means tie for an exact check"
+        assert np.array_equal(cl[g], o["cluster"]), f"tile {g}: clusters differ"
+        na = o["cluster"] >= 0
+        assert np.all(np.isinf(s[g][~na]))
+        err = np.abs(s[g][na] - o["s"][na]) / np.maximum(1.0, np.abs(o["s"][na]))
+        assert err.size == 0 or err.max() <= 1e-5, f"tile {g}: s error {err.max()}"
+        merr = np.abs(m[g] - o["mvec"]) / np.maximum(1.0, np.abs(o["mvec"]))
+        assert merr.max() <= 1e-5, f"tile {g}: m error {merr.max()}"
+
+
+@pytest.mark.gpu
+def test_score_deterministic():
+    L = need_gpu()
+    w = get_workload("llava_next_7b", keep=128)
+    attn, feats = vision_inputs(w.score, 1)
+    fa = [f.cuda() for f in feats]
+    r1 = L.score(attn.cuda(), fa, 89)
+    r2 = L.score(attn.cuda(), fa, 89)
+    torch.cuda.synchronize()
+    for k in ("a", "cluster", "s", "m"):
+        assert torch.equal(r1[k], r2[k]), k
+
+
+@pytest.mark.gpu
+def test_score_large_tile_batch_matches_per_tile():
+    """64 tiles in one call give the same bits as the same tiles scored separately."""
+    L = need_gpu()
+    w = get_workload("llava15_7b", keep=128)
+    from dataclasses import replace
+    w64 = replace(w, score=replace(w.score, G=64))
+    attn, feats = vision_inputs(w64.score, 3)
+    log("[score] G=64 batch")
+    allr = L.score(attn.cuda(), [f.cuda() for f in feats], 89)
+    for g in (0, 17, 63):
+        one = L.score(attn[g:g + 1].contiguous().cuda(), [f[g:g + 1].contiguous().cuda() for f in feats], 89)
+        for k in ("a", "cluster", "s", "m"):
+            assert torch.equal(allr[k][g:g + 1], one[k]), (g, k)
