@@ -195,6 +195,8 @@ spider_status spider_plan_skips(int L, int n_vis, const float* s_sa, int s_sa_st
  *   accumulate in fp32 (MFMA); O and down outputs are added to h in fp32;
  *   softmax in fp32.  Requires dh == 128, d % 64 == 0, d_ff % 64 == 0.
  * dtype SPIDER_F32: everything fp32 (any dh <= 256 with dh even).
+ * Both: d % 4 == 0, d <= 8192; x (bf16), weights, norms and h_out 16-byte
+ * aligned.
  * Inputs: cfg; layers = HOST array [L] of per-layer device weight pointers
  *   (matrices in nn.Linear layout [out, in], norms fp32 [d]); cu_seqlens =
  *   HOST int32 [B+1] (cu[0] = 0, non-decreasing); x = device [rows, d] in
@@ -239,9 +241,12 @@ spider_status spider_prefill(const spider_decoder_cfg* cfg, const spider_layer_w
  * returns, for kernel class `cls` (0 .. spider_profile_classes()-1), the
  * number of launches and the summed kernel time in milliseconds since the
  * last reset.  spider_profile_enable(0) stops recording; (1) starts it and
- * resets the counters.
+ * resets the counters.  spider_profile_mask() restricts recording to the
+ * classes whose bit is set (bit cls; all classes by default), so a timed
+ * run can carry events around one kernel class only.
  * ------------------------------------------------------------------------ */
 spider_status spider_profile_enable(int enable);
+spider_status spider_profile_mask(uint32_t mask);
 int spider_profile_classes(void);
 const char* spider_profile_class_name(int cls);
 spider_status spider_profile_read(int cls, int64_t* launches, double* total_ms);

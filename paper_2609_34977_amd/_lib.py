@@ -55,6 +55,7 @@ _SIGS = {
     "spider_prefill": ([ctypes.POINTER(DecoderCfg), ctypes.POINTER(LayerWeights), _I, _VP, _VP,
                         _VP, _VP, _VP, _SZ, _VP], _I),
     "spider_profile_enable": ([_I], _I),
+    "spider_profile_mask": ([ctypes.c_uint32], _I),
     "spider_profile_classes": ([], _I),
     "spider_profile_class_name": ([_I], ctypes.c_char_p),
     "spider_profile_read": ([_I, ctypes.POINTER(_I64), ctypes.POINTER(_D)], _I),
@@ -241,6 +242,19 @@ def prefill(cfg: DecoderCfg, weights, cu_seqlens, x: torch.Tensor, codes,
 # ----------------------------------------------------------------- profiler
 def profile_enable(on: bool = True):
     _check(lib().spider_profile_enable(1 if on else 0))
+
+
+def profile_mask(classes=None):
+    """Record only the named kernel classes (None = all)."""
+    L = lib()
+    if classes is None:
+        m = 0xFFFFFFFF
+    else:
+        names = [L.spider_profile_class_name(c).decode() for c in range(L.spider_profile_classes())]
+        m = 0
+        for c in classes:
+            m |= 1 << names.index(c)
+    _check(L.spider_profile_mask(m))
 
 
 def profile_read() -> dict:

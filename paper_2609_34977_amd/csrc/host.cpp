@@ -31,6 +31,7 @@ struct ProfRecord {
 };
 struct Profiler {
   bool enabled = false;
+  uint32_t mask = 0xFFFFFFFFu;
   std::vector<ProfRecord> records;
   std::vector<hipEvent_t> pool;
   int64_t launches[KC_COUNT] = {};
@@ -74,7 +75,7 @@ const char* kClassNames[KC_COUNT] = {
 }  // namespace
 
 void prof_begin(int cls, hipStream_t s) {
-  if (!g_prof.enabled) return;
+  if (!g_prof.enabled || !((g_prof.mask >> cls) & 1u)) return;
   std::lock_guard<std::mutex> lk(g_prof_mu);
   ProfRecord r{cls, take_event(), nullptr};
   if (r.start) hipEventRecord(r.start, s);
@@ -108,7 +109,7 @@ void prof_begin(int cls, hipStream_t s) {
 }
 
 void prof_end(int cls, hipStream_t s) {
-  if (!g_prof.enabled) return;
+  if (!g_prof.enabled || !((g_prof.mask >> cls) & 1u)) return;
   std::lock_guard<std::mutex> lk(g_prof_mu);
   if ((int)g_prof.open.size() < KC_COUNT) return;
   int i = g_prof.open[cls];
@@ -228,6 +229,14 @@ spider_status spider_profile_enable(int enable) {
   } else {
     g_prof.enabled = false;
   }
+  return SPIDER_OK;
+}
+
+spider_status spider_profile_mask(uint32_t mask) {
+  clear_error();
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  drain_records();
+  g_prof.mask = mask;
   return SPIDER_OK;
 }
 

@@ -62,9 +62,11 @@ __global__ void __launch_bounds__(256) rope_table_kernel(float2* __restrict__ ta
   tab[t] = make_float2((float)cos(ang), (float)sin(ang));
 }
 
-// One block per row: apply pending residual partials (h[r] += sum_s P[s][pslot[r]])
-// then, if the row is selected, out[nslot[r]] = round(h * rsqrt(mean(h^2) + eps) * w).
-template <typename AT>
+// One block per row: apply pending residual partials (h[r] += sum_s P[s][pslot[r]],
+// summed in split order) then, if the row is selected,
+// out[nslot[r]] = round(h * rsqrt(mean(h^2) + eps) * w).  Each thread owns up to
+// 8 float4 of the row (d <= 8192, d % 4 == 0) and issues all of its loads at once.
+template <typename AT, int MAXV>
 __global__ void __launch_bounds__(256) norm_kernel(float* __restrict__ h, int d,
                                                    const float* __restrict__ P, int psplit,
                                                    int64_t pstride, const int32_t* __restrict__ pslot,
@@ -73,29 +75,80 @@ __global__ void __launch_bounds__(256) norm_kernel(float* __restrict__ h, int d,
                                                    AT* __restrict__ out) {
   __shared__ float red[4];
   const int r = blockIdx.x;
-  float* hr = h + (int64_t)r * d;
   const int ps = (P && pslot) ? pslot[r] : -1;
   const int ns = all_rows ? r : (nslot ? nslot[r] : -1);
   if (ps < 0 && ns < 0) return;
-  float ss = 0.f;
-  for (int c = threadIdx.x; c < d; c += 256) {
-    float v = hr[c];
-    if (ps >= 0) {
-      float add = 0.f;
-      for (int s = 0; s < psplit; ++s) add += P[s * pstride + (int64_t)ps * d + c];
-      v += add;
-      hr[c] = v;
+  const int d4 = d >> 2;
+  float4* hr = reinterpret_cast<float4*>(h + (int64_t)r * d);
+  float4 v[MAXV];
+#pragma unroll
+  for (int k = 0; k < MAXV; ++k) {
+    const int c = threadIdx.x + k * 256;
+    v[k] = c < d4 ? hr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  if (ps >= 0) {
+    const float4* pr = reinterpret_cast<const float4*>(P + (int64_t)ps * d);
+    const int64_t ps4 = pstride >> 2;
+    // four splits' loads in flight at a time, summed in split order
+    for (int s0 = 0; s0 < psplit; s0 += 4) {
+      float4 add[4][MAXV];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int k = 0; k < MAXV; ++k) {
+          const int c = threadIdx.x + k * 256;
+          add[q][k] = (c < d4 && s0 + q < psplit) ? pr[(s0 + q) * ps4 + c] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int k = 0; k < MAXV; ++k) {
+          v[k].x += add[q][k].x;
+          v[k].y += add[q][k].y;
+          v[k].z += add[q][k].z;
+          v[k].w += add[q][k].w;
+        }
     }
-    ss = fmaf(v, v, ss);
+#pragma unroll
+    for (int k = 0; k < MAXV; ++k) {
+      const int c = threadIdx.x + k * 256;
+      if (c < d4) hr[c] = v[k];
+    }
   }
   if (ns < 0) return;
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < MAXV; ++k)
+    ss = fmaf(v[k].x, v[k].x, fmaf(v[k].y, v[k].y, fmaf(v[k].z, v[k].z, fmaf(v[k].w, v[k].w, ss))));
   ss = wave_sum(ss);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float inv = 1.0f / sqrtf(tot / (float)d + eps);
   AT* o = out + (int64_t)ns * d;
-  for (int c = threadIdx.x; c < d; c += 256) Act<AT>::store(o + c, hr[c] * inv * w[c]);
+  const float4* w4 = reinterpret_cast<const float4*>(w);
+#pragma unroll
+  for (int k = 0; k < MAXV; ++k) {
+    const int c = threadIdx.x + k * 256;
+    if (c < d4) {
+      const float4 ww = w4[c];
+      Act<AT>::store(o + 4 * c + 0, v[k].x * inv * ww.x);
+      Act<AT>::store(o + 4 * c + 1, v[k].y * inv * ww.y);
+      Act<AT>::store(o + 4 * c + 2, v[k].z * inv * ww.z);
+      Act<AT>::store(o + 4 * c + 3, v[k].w * inv * ww.w);
+    }
+  }
+}
+
+// d <= 4096 uses 4 float4 per thread, larger rows 8.
+template <typename AT>
+void launch_norm(int R, float* h, int d, const float* P, int psplit, int64_t pstride,
+                 const int32_t* pslot, const float* w, float eps, const int32_t* nslot,
+                 int all_rows, AT* out, hipStream_t st) {
+  if (d <= 4096)
+    norm_kernel<AT, 4><<<R, 256, 0, st>>>(h, d, P, psplit, pstride, pslot, w, eps, nslot, all_rows, out);
+  else
+    norm_kernel<AT, 8><<<R, 256, 0, st>>>(h, d, P, psplit, pstride, pslot, w, eps, nslot, all_rows, out);
 }
 
 // Blocks [0, nq): Q rows, [nq, nq+R): K rows, [nq+R, nq+2R): V rows.
@@ -167,7 +220,7 @@ struct Staging {
 };
 thread_local Staging g_stage;
 
-int split_max_for_rows(int R) { return std::max(1, std::min(4, 2048 / std::max(1, R))); }
+int split_max_for_rows(int R) { return std::max(1, std::min(8, 4096 / std::max(1, R))); }
 
 struct PrefillWs {
   int32_t* tables;
@@ -215,6 +268,8 @@ spider_status validate_cfg(const spider_decoder_cfg* cfg) {
   SPIDER_REQUIRE(dh % 2 == 0, SPIDER_ERR_SHAPE, "spider_prefill: dh must be even");
   SPIDER_REQUIRE(cfg->dtype == SPIDER_F32 || cfg->dtype == SPIDER_BF16, SPIDER_ERR_INVALID_ARG,
                  "spider_prefill: bad dtype");
+  SPIDER_REQUIRE(cfg->d % 4 == 0 && cfg->d <= 8192, SPIDER_ERR_UNSUPPORTED,
+                 "spider_prefill: d must be a multiple of 4 and at most 8192");
   SPIDER_REQUIRE(std::isfinite(cfg->eps) && cfg->eps >= 0.f && std::isfinite(cfg->theta) &&
                      cfg->theta > 0.f,
                  SPIDER_ERR_INVALID_ARG, "spider_prefill: eps must be >= 0 and theta > 0");
@@ -331,8 +386,11 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
   AT* vb = reinterpret_cast<AT*>(ws.v);
   AT* ob = reinterpret_cast<AT*>(ws.o);
   AT* act = reinterpret_cast<AT*>(ws.act);
-  auto gemm = [&](GemmArgs& ga) {
-    return bf16 ? launch_gemm_bf16(ga, split_max, st) : launch_gemm_f32(ga, split_max, st);
+  // split-K caps: the QKV partials are re-read by the finalize kernel and the
+  // O/down partials by the next norm, so splitting is kept modest
+  auto gemm = [&](GemmArgs& ga, int cap) {
+    const int sm = std::min(split_max, cap);
+    return bf16 ? launch_gemm_bf16(ga, sm, st) : launch_gemm_f32(ga, sm, st);
   };
 
   for (int l = 0; l < c.L; ++l) {
@@ -341,8 +399,8 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
     if (T.nA > 0) {
       {
         ProfScope ps(KC_RMSNORM, st);
-        norm_kernel<AT><<<R, 256, 0, st>>>(h, d, ws.Pres, pend_split, pstride, pend_slot,
-                                           w.attn_norm, c.eps, nullptr, 1, xn);
+        launch_norm<AT>(R, h, d, ws.Pres, pend_split, pstride, pend_slot, w.attn_norm, c.eps,
+                        nullptr, 1, xn, st);
         SPIDER_LAUNCHED("rmsnorm(attn)");
         pend_split = 0;
         pend_slot = nullptr;
@@ -357,7 +415,7 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
       ga.g[2] = GemmGroup{xn, nullptr, R, w.wv, nullptr, d, ws.Pv, d, pstride, 0, 0, 0};
       {
         ProfScope ps(KC_GEMM_QKV, st);
-        hipError_t e = gemm(ga);
+        hipError_t e = gemm(ga, 2);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_qkv: %s", hipGetErrorString(e));
       }
       {
@@ -382,7 +440,7 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
       go.g[0] = GemmGroup{ob, nullptr, T.nA, w.wo, nullptr, d, ws.Pres, d, pstride, 0, 0, 0};
       {
         ProfScope ps(KC_GEMM_O, st);
-        hipError_t e = gemm(go);
+        hipError_t e = gemm(go, 8);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_o: %s", hipGetErrorString(e));
       }
       pend_split = go.split;
@@ -391,8 +449,8 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
     if (T.nF > 0) {
       {
         ProfScope ps(KC_RMSNORM, st);
-        norm_kernel<AT><<<R, 256, 0, st>>>(h, d, ws.Pres, pend_split, pstride, pend_slot,
-                                           w.ffn_norm, c.eps, ws.tables + T.offSlotF, 0, xn);
+        launch_norm<AT>(R, h, d, ws.Pres, pend_split, pstride, pend_slot, w.ffn_norm, c.eps,
+                        ws.tables + T.offSlotF, 0, xn, st);
         SPIDER_LAUNCHED("rmsnorm(ffn)");
         pend_split = 0;
         pend_slot = nullptr;
@@ -405,7 +463,7 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
       gu.g[0] = GemmGroup{xn, nullptr, T.nF, w.wg, w.wu, c.d_ff, act, c.d_ff, 0, 0, 0, 0};
       {
         ProfScope ps(KC_GEMM_GATEUP, st);
-        hipError_t e = gemm(gu);
+        hipError_t e = gemm(gu, 1);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_gateup: %s", hipGetErrorString(e));
       }
       GemmArgs gd{};
@@ -416,7 +474,7 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
       gd.g[0] = GemmGroup{act, nullptr, T.nF, w.wd, nullptr, d, ws.Pres, d, pstride, 0, 0, 0};
       {
         ProfScope ps(KC_GEMM_DOWN, st);
-        hipError_t e = gemm(gd);
+        hipError_t e = gemm(gd, 8);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_down: %s", hipGetErrorString(e));
       }
       pend_split = gd.split;
@@ -425,8 +483,8 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
   }
   if (pend_split > 0) {
     ProfScope ps(KC_RESIDUAL, st);
-    norm_kernel<AT><<<R, 256, 0, st>>>(h, d, ws.Pres, pend_split, pstride, pend_slot, nullptr, 0.f,
-                                       nullptr, 0, static_cast<AT*>(nullptr));
+    launch_norm<AT>(R, h, d, ws.Pres, pend_split, pstride, pend_slot, nullptr, 0.f, nullptr, 0,
+                    static_cast<AT*>(nullptr), st);
     SPIDER_LAUNCHED("residual_add");
   }
   return SPIDER_OK;
@@ -476,6 +534,12 @@ extern "C" spider_status spider_prefill(const spider_decoder_cfg* cfg,
                  workspace_bytes);
   SPIDER_REQUIRE(((uintptr_t)workspace % 256) == 0, SPIDER_ERR_WORKSPACE,
                  "spider_prefill: workspace must be 256-byte aligned");
+  SPIDER_REQUIRE(((uintptr_t)h_out % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                 "spider_prefill: h_out must be 16-byte aligned");
+  for (int l = 0; l < cfg->L; ++l)
+    SPIDER_REQUIRE(((uintptr_t)layers[l].attn_norm % 16) == 0 &&
+                       ((uintptr_t)layers[l].ffn_norm % 16) == 0,
+                   SPIDER_ERR_UNSUPPORTED, "spider_prefill: norm weights must be 16-byte aligned");
   if (cfg->dtype == SPIDER_BF16) {
     SPIDER_REQUIRE(((uintptr_t)x % 16) == 0, SPIDER_ERR_UNSUPPORTED,
                    "spider_prefill: x must be 16-byte aligned");

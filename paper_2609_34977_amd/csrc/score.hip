@@ -24,6 +24,7 @@
 //
 // Lane-to-dimension map used by kmeans/score_final: lane l owns VPL
 // dimensions, in chunks of 8: dims {c*512 + 8*l + e : c < VPL/8, e < 8}.
+#include <algorithm>
 #include <cfloat>
 #include <cmath>
 
@@ -184,12 +185,14 @@ __global__ void __launch_bounds__(1024) anchor_topk_kernel(int n, int n_anchor,
                                                            int32_t* __restrict__ cluster_out,
                                                            float* __restrict__ s_out,
                                                            int32_t* __restrict__ anc_list,
-                                                           int32_t* __restrict__ rest_list) {
+                                                           int32_t* __restrict__ rest_list,
+                                                           int32_t* __restrict__ conv) {
   __shared__ uint64_t keys[kMaxN];
   __shared__ uint16_t flag[kMaxN];
   __shared__ uint16_t pos[kMaxN];
   __shared__ int scratch[17];
   const int g = blockIdx.x;
+  if (threadIdx.x == 0) conv[g] = 0;
   int N = 1;
   while (N < n) N <<= 1;
   for (int i = threadIdx.x; i < N; i += blockDim.x) {
@@ -302,223 +305,258 @@ __global__ void __launch_bounds__(256) anchor_maxsim_f32_kernel(
   if (lane == 0) mvec[(int64_t)g * n + i] = n_anchor > 0 ? best : 0.f;
 }
 
-// ------------------------------------------------------------- shared reduction
-// Adds the per-wave partial sums psum[K][VPL] (lane slice) into acc[K*d] in LDS
-// in fixed wave order, plus per-wave counts into cnt[K].
-template <int VPL, int KMAX>
-__device__ inline void ordered_wave_reduce(float (&psum)[KMAX][VPL], const int (&pcnt)[KMAX], int K,
-                                           int d, float* acc, int* cnt, int nwaves) {
+// ------------------------------------------------------------- clustering
+// Multi-workgroup Lloyd iterations.  Each tile's m non-anchor rows are split
+// into NB contiguous row ranges, one 256-thread block per range.  One Lloyd
+// pass = kmeans_assign (assign rows to the nearest centroid, per-block
+// per-cluster partial sums) + kmeans_update (fixed-order sum of the NB
+// partials, new centroids in place; empty clusters keep theirs).  The host
+// enqueues max_iter passes; once a pass changes no assignment, update sets a
+// per-tile flag and the remaining launches return at once.  Centroids live
+// in global memory and are staged in LDS; every reduction runs in a fixed
+// order, so results are bitwise reproducible.
+
+// Per-cluster partial sums over this block's rows [j0, j1) of layer `l`
+// (optionally scaled by w[i]): out[k*d + c] for k < K.  The block makes one
+// pass per cluster over its rows (they stay in L1/L2), one wave per row; the 4
+// wave partials are combined in a fixed order through LDS, 512 dimensions at
+// a time (red: 4 * 512 floats).
+template <typename FT, int VPL>
+__device__ inline void block_cluster_sums(const FeatArgs& fa, int l, int g, int d, int K,
+                                          const int32_t* U, int j0, int j1, const int32_t* lab,
+                                          const float* w, float* red, float* out) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int w = 0; w < nwaves; ++w) {
-    if (wave == w) {
+  for (int k = 0; k < K; ++k) {
+    float acc[VPL];
 #pragma unroll
-      for (int k = 0; k < KMAX; ++k) {
-        if (k >= K) break;
-#pragma unroll
-        for (int v = 0; v < VPL; ++v) {
-          const int dim = slice_dim(v, lane);
-          if (dim < d) {
-            float* p = acc + k * d + dim;
-            *p = (w == 0) ? psum[k][v] : (*p + psum[k][v]);
-          }
-        }
-        if (lane == 0) cnt[k] = (w == 0) ? pcnt[k] : cnt[k] + pcnt[k];
-      }
-    }
-    __syncthreads();
-  }
-}
-
-// ------------------------------------------------------------- kmeans
-template <typename FT, int VPL, int KMAX>
-__global__ void kmeans_kernel(int n, int d, int n_anchor, int K, int max_iter, FeatArgs fa,
-                              int last, const int32_t* __restrict__ rest_list,
-                              int32_t* __restrict__ cluster_out) {
-  extern __shared__ float smem[];
-  float* acc = smem;                               // [K*d]
-  int* cnt = reinterpret_cast<int*>(acc + KMAX * d);  // [KMAX]
-  int* flag = cnt + KMAX;                          // [1]
-  int* assign = flag + 1;                          // [m]
-  const int g = blockIdx.x;
-  const int m = n - n_anchor;
-  if (m <= 0) return;
-  const int nwaves = blockDim.x >> 6;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int32_t* U = rest_list + (int64_t)g * n;
-
-  float c[KMAX][VPL];
-#pragma unroll
-  for (int k = 0; k < KMAX; ++k) {
-    if (k < K) {
-      const int j = (int)(((int64_t)k * m) / K);
-      load_slice<FT, VPL>(feat_row<FT>(fa, last, g, U[j]), d, lane, c[k]);
-    }
-  }
-  for (int it = 0; it < max_iter; ++it) {
-    float psum[KMAX][VPL];
-    int pcnt[KMAX];
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) {
-      pcnt[k] = 0;
-#pragma unroll
-      for (int v = 0; v < VPL; ++v) psum[k][v] = 0.f;
-    }
-    int changed = 0;
-    for (int j = wave; j < m; j += nwaves) {
-      float x[VPL];
-      load_slice<FT, VPL>(feat_row<FT>(fa, last, g, U[j]), d, lane, x);
-      float dist[KMAX];
-#pragma unroll
-      for (int k = 0; k < KMAX; ++k) {
-        float s = 0.f;
-        if (k < K) {
-#pragma unroll
-          for (int v = 0; v < VPL; ++v) {
-            const float t = x[v] - c[k][v];
-            s = fmaf(t, t, s);
-          }
-        }
-        dist[k] = s;
-      }
-#pragma unroll
-      for (int k = 0; k < KMAX; ++k)
-        if (k < K) dist[k] = wave_sum(dist[k]);
-      int best = 0;
-      float bd = dist[0];
-#pragma unroll
-      for (int k = 1; k < KMAX; ++k)
-        if (k < K && dist[k] < bd) {
-          bd = dist[k];
-          best = k;
-        }
-      if (it == 0 || assign[j] != best) changed = 1;
-      __builtin_amdgcn_wave_barrier();
-      if (lane == 0) assign[j] = best;
-#pragma unroll
-      for (int k = 0; k < KMAX; ++k)
-        if (k == best) {
-          pcnt[k] += 1;
-#pragma unroll
-          for (int v = 0; v < VPL; ++v) psum[k][v] += x[v];
-        }
-    }
-    if (threadIdx.x == 0) *flag = 0;
-    __syncthreads();
-    if (lane == 0 && changed) atomicOr(flag, 1);
-    __syncthreads();
-    const int any = *flag;
-    __syncthreads();
-    if (!any) break;
-    ordered_wave_reduce<VPL, KMAX>(psum, pcnt, K, d, acc, cnt, nwaves);
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) {
-      if (k < K && cnt[k] > 0) {
-        const float fc = (float)cnt[k];
-#pragma unroll
-        for (int v = 0; v < VPL; ++v) {
-          const int dim = slice_dim(v, lane);
-          c[k][v] = dim < d ? __fdiv_rn(acc[k * d + dim], fc) : 0.f;
-        }
-      }
-    }
-    __syncthreads();
-  }
-  for (int j = threadIdx.x; j < m; j += blockDim.x) cluster_out[(int64_t)g * n + U[j]] = assign[j];
-}
-
-// ------------------------------------------------------------- score_final
-template <typename FT, int VPL, int KMAX>
-__global__ void score_final_kernel(int n, int d, int n_anchor, int K, int n_layers, FeatArgs fa,
-                                   const float* __restrict__ nu, const int32_t* __restrict__ rest_list,
-                                   const int32_t* __restrict__ cluster, const float* __restrict__ mvec,
-                                   float* __restrict__ mu_ws, float* __restrict__ s_out,
-                                   float* __restrict__ m_out) {
-  extern __shared__ float smem[];
-  float* acc = smem;                                  // [K*d]
-  int* cnt = reinterpret_cast<int*>(acc + KMAX * d);  // [KMAX]
-  float* mbar = reinterpret_cast<float*>(cnt + KMAX);  // [KMAX]
-  const int g = blockIdx.x;
-  const int m = n - n_anchor;
-  const int nwaves = blockDim.x >> 6;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int32_t* U = rest_list + (int64_t)g * n;
-  const int32_t* cl = cluster + (int64_t)g * n;
-  const float* mv = mvec + (int64_t)g * n;
-  if (m_out)
-    for (int i = threadIdx.x; i < n; i += blockDim.x) m_out[(int64_t)g * n + i] = mv[i];
-  if (m <= 0) return;
-  float* mu_g = mu_ws + (int64_t)g * n_layers * KMAX * d;
-
-  // cluster mean of m (one thread, rows in ascending order)
-  if (threadIdx.x == 0) {
-    float sm[KMAX];
-    int ct[KMAX];
-    for (int k = 0; k < KMAX; ++k) {
-      sm[k] = 0.f;
-      ct[k] = 0;
-    }
-    for (int j = 0; j < m; ++j) {
+    for (int v = 0; v < VPL; ++v) acc[v] = 0.f;
+    for (int j = j0 + wave; j < j1; j += 4) {
+      if (lab[j - j0] != k) continue;
       const int i = U[j];
-      const int k = cl[i];
-      sm[k] += mv[i];
-      ct[k] += 1;
-    }
-    for (int k = 0; k < KMAX; ++k) mbar[k] = ct[k] ? __fdiv_rn(sm[k], (float)ct[k]) : 0.f;
-  }
-  // cluster means of unit rows, layer by layer
-  for (int l = 0; l < n_layers; ++l) {
-    const float* nu_l = nu + ((int64_t)g * n_layers + l) * n;
-    float psum[KMAX][VPL];
-    int pcnt[KMAX];
-#pragma unroll
-    for (int k = 0; k < KMAX; ++k) {
-      pcnt[k] = 0;
-#pragma unroll
-      for (int v = 0; v < VPL; ++v) psum[k][v] = 0.f;
-    }
-    for (int j = wave; j < m; j += nwaves) {
-      const int i = U[j];
-      const int k_i = cl[i];
       float x[VPL];
       load_slice<FT, VPL>(feat_row<FT>(fa, l, g, i), d, lane, x);
-      const float s = nu_l[i];
+      const float sc = w ? w[i] : 1.0f;
 #pragma unroll
-      for (int k = 0; k < KMAX; ++k)
-        if (k == k_i) {
-          pcnt[k] += 1;
-#pragma unroll
-          for (int v = 0; v < VPL; ++v) psum[k][v] = fmaf(x[v], s, psum[k][v]);
-        }
+      for (int v = 0; v < VPL; ++v) acc[v] = fmaf(x[v], sc, acc[v]);
     }
-    ordered_wave_reduce<VPL, KMAX>(psum, pcnt, K, d, acc, cnt, nwaves);
+#pragma unroll
+    for (int q = 0; q < VPL / 8; ++q) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) red[wave * 512 + lane * 8 + e] = acc[8 * q + e];
+      __syncthreads();
+      for (int c = threadIdx.x; c < 512; c += blockDim.x) {
+        const int dim = q * 512 + c;
+        if (dim < d) out[k * d + dim] = ((red[c] + red[512 + c]) + red[1024 + c]) + red[1536 + c];
+      }
+      __syncthreads();
+    }
+  }
+}
+
+constexpr int kMaxRowsPerBlock = 128;
+
+struct ClusterWs {
+  float* cent;      // [G][K][d]
+  float* psum;      // [G][NB][K][d]    (kmeans) / [G][NB][L][K][d] (means)
+  int32_t* pcnt;    // [G][NB][K]
+  float* pm;        // [G][NB][K]       partial sums of m
+  int32_t* pchg;    // [G][NB]
+  int32_t* conv;    // [G]
+  int32_t* assign;  // [G][n]  assignment of non-anchor row j (index into U)
+  float* mu;        // [G][L][K][d]
+  float* mbar;      // [G][K]
+  int NB, RB;       // blocks per tile, rows per block
+};
+
+template <typename FT, int VPL>
+__global__ void __launch_bounds__(256) kmeans_assign_kernel(int n, int d, int n_anchor, int K,
+                                                            int first, FeatArgs fa, int last,
+                                                            const int32_t* __restrict__ rest_list,
+                                                            ClusterWs cw, int32_t* __restrict__ cluster_out) {
+  extern __shared__ float smem[];
+  float* cs = smem;                 // [K*d] centroids
+  float* red = cs + K * d;          // [4*512]
+  __shared__ int lab[kMaxRowsPerBlock];
+  __shared__ int chg;
+  const int g = blockIdx.y, b = blockIdx.x;
+  const int m = n - n_anchor;
+  const int j0 = b * cw.RB, j1 = min(m, j0 + cw.RB);
+  if (j0 >= j1 || cw.conv[g]) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int32_t* U = rest_list + (int64_t)g * n;
+  float* cent = cw.cent + (int64_t)g * K * d;
+  if (first) {
+    // centroids at rows floor(k*m/K) of the non-anchor list
     for (int t = threadIdx.x; t < K * d; t += blockDim.x) {
-      const int k = t / d;
-      mu_g[((int64_t)l * KMAX + k) * d + (t - k * d)] = cnt[k] ? __fdiv_rn(acc[t], (float)cnt[k]) : 0.f;
+      const int k = t / d, c = t - k * d;
+      const FT* row = feat_row<FT>(fa, last, g, U[(int)(((int64_t)k * m) / K)]);
+      const float v = Feat<FT>::load1(row + c);
+      cs[t] = v;
+      if (b == 0) cent[t] = v;
     }
-    __syncthreads();
+  } else {
+    for (int t = threadIdx.x; t < K * d; t += blockDim.x) cs[t] = cent[t];
   }
-  __threadfence_block();
+  if (threadIdx.x == 0) chg = first;
   __syncthreads();
-  // scores of non-anchor rows
-  for (int j = wave; j < m; j += nwaves) {
-    const int i = U[j];
-    const int k_i = cl[i];
-    float s = 0.f;
-    for (int l = 0; l < n_layers; ++l) {
-      float x[VPL];
-      load_slice<FT, VPL>(feat_row<FT>(fa, l, g, i), d, lane, x);
-      const float* mu = mu_g + ((int64_t)l * KMAX + k_i) * d;
-      float dot = 0.f;
+  int32_t* asg = cw.assign + (int64_t)g * n;
+  for (int j = j0 + wave; j < j1; j += 4) {
+    float x[VPL];
+    load_slice<FT, VPL>(feat_row<FT>(fa, last, g, U[j]), d, lane, x);
+    int best = 0;
+    float bd = 0.f;
+    for (int k = 0; k < K; ++k) {
+      float s = 0.f;
 #pragma unroll
       for (int v = 0; v < VPL; ++v) {
         const int dim = slice_dim(v, lane);
-        if (dim < d) dot = fmaf(x[v], mu[dim], dot);
+        const float t = dim < d ? x[v] - cs[k * d + dim] : 0.f;
+        s = fmaf(t, t, s);
       }
-      dot = wave_sum(dot);
-      s += dot * nu[((int64_t)g * n_layers + l) * n + i];
+      s = wave_sum(s);
+      if (k == 0 || s < bd) {
+        bd = s;
+        best = k;
+      }
     }
-    if (lane == 0) s_out[(int64_t)g * n + i] = s + mv[i] + mbar[k_i];
+    if (lane == 0) {
+      if (!first && asg[j] != best) chg = 1;
+      asg[j] = best;
+      lab[j - j0] = best;
+      cluster_out[(int64_t)g * n + U[j]] = best;
+    }
   }
+  __syncthreads();
+  const int64_t slot = (int64_t)g * cw.NB + b;
+  block_cluster_sums<FT, VPL>(fa, last, g, d, K, U, j0, j1, lab, nullptr, red, cw.psum + slot * K * d);
+  if (threadIdx.x < K) {
+    int c = 0;
+    for (int j = j0; j < j1; ++j) c += lab[j - j0] == (int)threadIdx.x;
+    cw.pcnt[slot * K + threadIdx.x] = c;
+  }
+  if (threadIdx.x == 0) cw.pchg[slot] = chg;
+}
+
+// grid (ceil(K*d/256), G): new centroids = fixed-order sums of the partials.
+__global__ void __launch_bounds__(256) kmeans_update_kernel(int d, int K, ClusterWs cw, int nb_used) {
+  const int g = blockIdx.y;
+  if (cw.conv[g]) return;
+  int any = 0;
+  for (int b = 0; b < nb_used; ++b) any |= cw.pchg[(int64_t)g * cw.NB + b];
+  if (!any) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) cw.conv[g] = 1;
+    return;
+  }
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= K * d) return;
+  const int k = t / d;
+  float s = 0.f;
+  int c = 0;
+  for (int b = 0; b < nb_used; ++b) {
+    const int64_t slot = (int64_t)g * cw.NB + b;
+    s += cw.psum[slot * K * d + t];
+    c += cw.pcnt[slot * K + k];
+  }
+  if (c > 0) cw.cent[(int64_t)g * K * d + t] = __fdiv_rn(s, (float)c);
+}
+
+// Partial per-cluster sums of unit rows (every tapped layer) and of m.
+template <typename FT, int VPL>
+__global__ void __launch_bounds__(256) cluster_sum_kernel(int n, int d, int n_anchor, int K,
+                                                          int n_layers, FeatArgs fa,
+                                                          const float* __restrict__ nu,
+                                                          const int32_t* __restrict__ rest_list,
+                                                          const float* __restrict__ mvec, ClusterWs cw) {
+  __shared__ float red[4 * 512];
+  __shared__ int lab[kMaxRowsPerBlock];
+  const int g = blockIdx.y, b = blockIdx.x;
+  const int m = n - n_anchor;
+  const int j0 = b * cw.RB, j1 = min(m, j0 + cw.RB);
+  if (j0 >= j1) return;
+  const int32_t* U = rest_list + (int64_t)g * n;
+  const int32_t* asg = cw.assign + (int64_t)g * n;
+  for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) lab[j - j0] = asg[j];
+  __syncthreads();
+  const int64_t slot = (int64_t)g * cw.NB + b;
+  for (int l = 0; l < n_layers; ++l)
+    block_cluster_sums<FT, VPL>(fa, l, g, d, K, U, j0, j1, lab, nu + ((int64_t)g * n_layers + l) * n,
+                                red, cw.psum + (slot * n_layers + l) * K * d);
+  if (threadIdx.x < K) {
+    int c = 0;
+    float sm = 0.f;
+    for (int j = j0; j < j1; ++j)
+      if (lab[j - j0] == (int)threadIdx.x) {
+        ++c;
+        sm += mvec[(int64_t)g * n + U[j]];
+      }
+    cw.pcnt[slot * K + threadIdx.x] = c;
+    cw.pm[slot * K + threadIdx.x] = sm;
+  }
+}
+
+// grid (ceil(L*K*d/256), G): mu = fixed-order sums / counts; mbar likewise.
+__global__ void __launch_bounds__(256) cluster_mean_kernel(int d, int K, int n_layers, ClusterWs cw,
+                                                           int nb_used) {
+  const int g = blockIdx.y;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  const int per = K * d;
+  if (t < n_layers * per) {
+    const int l = t / per, r = t - l * per, k = r / d;
+    float s = 0.f;
+    int c = 0;
+    for (int b = 0; b < nb_used; ++b) {
+      const int64_t slot = (int64_t)g * cw.NB + b;
+      s += cw.psum[(slot * n_layers + l) * per + r];
+      c += cw.pcnt[slot * K + k];
+    }
+    cw.mu[((int64_t)g * n_layers + l) * per + r] = c ? __fdiv_rn(s, (float)c) : 0.f;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < K) {
+    const int k = threadIdx.x;
+    float s = 0.f;
+    int c = 0;
+    for (int b = 0; b < nb_used; ++b) {
+      const int64_t slot = (int64_t)g * cw.NB + b;
+      s += cw.pm[slot * K + k];
+      c += cw.pcnt[slot * K + k];
+    }
+    cw.mbar[(int64_t)g * K + k] = c ? __fdiv_rn(s, (float)c) : 0.f;
+  }
+}
+
+// One wave per non-anchor row: s = sum_l nu_l * (F^l_i . mu^l_c) + m_i + mbar_c.
+template <typename FT, int VPL>
+__global__ void __launch_bounds__(256) score_rows_kernel(int n, int d, int n_anchor, int K,
+                                                         int n_layers, FeatArgs fa,
+                                                         const float* __restrict__ nu,
+                                                         const int32_t* __restrict__ rest_list,
+                                                         const float* __restrict__ mvec, ClusterWs cw,
+                                                         float* __restrict__ s_out,
+                                                         float* __restrict__ m_out) {
+  const int g = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m = n - n_anchor;
+  if (m_out && blockIdx.x == 0)
+    for (int i = threadIdx.x; i < n; i += blockDim.x) m_out[(int64_t)g * n + i] = mvec[(int64_t)g * n + i];
+  const int j = blockIdx.x * 4 + wave;
+  if (j >= m) return;
+  const int i = rest_list[(int64_t)g * n + j];
+  const int k = cw.assign[(int64_t)g * n + j];
+  float s = 0.f;
+  for (int l = 0; l < n_layers; ++l) {
+    float x[VPL];
+    load_slice<FT, VPL>(feat_row<FT>(fa, l, g, i), d, lane, x);
+    const float* mu = cw.mu + (((int64_t)g * n_layers + l) * K + k) * d;
+    float dot = 0.f;
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      const int dim = slice_dim(v, lane);
+      if (dim < d) dot = fmaf(x[v], mu[dim], dot);
+    }
+    dot = wave_sum(dot);
+    s += dot * nu[((int64_t)g * n_layers + l) * n + i];
+  }
+  if (lane == 0) s_out[(int64_t)g * n + i] = s + mvec[(int64_t)g * n + i] + cw.mbar[(int64_t)g * K + k];
 }
 
 struct ScoreWs {
@@ -526,51 +564,99 @@ struct ScoreWs {
   int32_t* anc;
   int32_t* rest;
   float* mvec;
-  float* mu;
+  ClusterWs cw;
 };
 
-size_t score_ws_layout(int G, int n, int d, int n_layers, ScoreWs* w, char* base) {
+// Blocks per tile: about 32 rows each (at most 16 per tile, never more than
+// kMaxRowsPerBlock rows per block).  It depends on n only, so a tile gets the
+// same partial-sum order, hence the same bits, whatever the batch size G.
+int blocks_per_tile(int G, int n) {
+  (void)G;
+  const int need = (n + kMaxRowsPerBlock - 1) / kMaxRowsPerBlock;
+  const int want = std::min(16, (n + 31) / 32);
+  return std::max(need, std::max(1, want));
+}
+
+size_t score_ws_layout(int G, int n, int d, int n_layers, int K, ScoreWs* w, char* base) {
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
     off = align_up(off + bytes, 256);
     return base ? base + o : nullptr;
   };
+  const int NB = blocks_per_tile(G, n);
+  const int L1 = std::max(1, n_layers);
   char* p_nu = take((size_t)G * n_layers * n * 4);
   char* p_anc = take((size_t)G * n * 4);
   char* p_rest = take((size_t)G * n * 4);
   char* p_mvec = take((size_t)G * n * 4);
-  char* p_mu = take((size_t)G * n_layers * 8 * d * 4);
+  char* p_cent = take((size_t)G * K * d * 4);
+  char* p_psum = take((size_t)G * NB * L1 * K * d * 4);
+  char* p_pcnt = take((size_t)G * NB * K * 4);
+  char* p_pm = take((size_t)G * NB * K * 4);
+  char* p_pchg = take((size_t)G * NB * 4);
+  char* p_conv = take((size_t)G * 4);
+  char* p_asg = take((size_t)G * n * 4);
+  char* p_mu = take((size_t)G * L1 * K * d * 4);
+  char* p_mbar = take((size_t)G * K * 4);
   if (w) {
     w->nu = reinterpret_cast<float*>(p_nu);
     w->anc = reinterpret_cast<int32_t*>(p_anc);
     w->rest = reinterpret_cast<int32_t*>(p_rest);
     w->mvec = reinterpret_cast<float*>(p_mvec);
-    w->mu = reinterpret_cast<float*>(p_mu);
+    w->cw.cent = reinterpret_cast<float*>(p_cent);
+    w->cw.psum = reinterpret_cast<float*>(p_psum);
+    w->cw.pcnt = reinterpret_cast<int32_t*>(p_pcnt);
+    w->cw.pm = reinterpret_cast<float*>(p_pm);
+    w->cw.pchg = reinterpret_cast<int32_t*>(p_pchg);
+    w->cw.conv = reinterpret_cast<int32_t*>(p_conv);
+    w->cw.assign = reinterpret_cast<int32_t*>(p_asg);
+    w->cw.mu = reinterpret_cast<float*>(p_mu);
+    w->cw.mbar = reinterpret_cast<float*>(p_mbar);
+    w->cw.NB = NB;
   }
   return off;
 }
 
-template <typename FT, int VPL, int KMAX>
+template <typename FT, int VPL>
 hipError_t launch_cluster_kernels(int G, int n, int d, int n_anchor, int K, int max_iter,
-                                  int n_layers, const FeatArgs& fa, const ScoreWs& ws,
+                                  int n_layers, const FeatArgs& fa, ScoreWs ws,
                                   int32_t* cluster_out, float* s_out, float* m_out, hipStream_t st) {
-  const int threads = (KMAX * VPL <= 64) ? 512 : 256;
   const int m = n - n_anchor;
-  {
+  const int NB = ws.cw.NB;
+  ws.cw.RB = m > 0 ? (m + NB - 1) / NB : 1;
+  const int nb_used = m > 0 ? (m + ws.cw.RB - 1) / ws.cw.RB : 0;
+  // NB >= ceil(n / kMaxRowsPerBlock) guarantees these; checked before any launch
+  if (ws.cw.RB > kMaxRowsPerBlock || nb_used > NB) return hipErrorInvalidValue;
+  if (m > 0) {
     ProfScope ps(KC_KMEANS, st);
-    const size_t sh = (size_t)KMAX * d * 4 + KMAX * 4 + 4 + (size_t)(m > 0 ? m : 1) * 4;
-    kmeans_kernel<FT, VPL, KMAX><<<G, threads, sh, st>>>(n, d, n_anchor, K, max_iter, fa,
-                                                        n_layers - 1, ws.rest, cluster_out);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    const size_t sh = ((size_t)K * d + 4 * 512) * 4;
+    for (int it = 0; it < max_iter; ++it) {
+      kmeans_assign_kernel<FT, VPL><<<dim3(nb_used, G), 256, sh, st>>>(
+          n, d, n_anchor, K, it == 0, fa, n_layers - 1, ws.rest, ws.cw, cluster_out);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      if (it + 1 < max_iter) {
+        kmeans_update_kernel<<<dim3(ceil_div(K * d, 256), G), 256, 0, st>>>(d, K, ws.cw, nb_used);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+      }
+    }
   }
   {
     ProfScope ps(KC_SCORE_FINAL, st);
-    const size_t sh = (size_t)KMAX * d * 4 + KMAX * 8;
-    score_final_kernel<FT, VPL, KMAX><<<G, threads, sh, st>>>(n, d, n_anchor, K, n_layers, fa,
-                                                             ws.nu, ws.rest, cluster_out, ws.mvec,
-                                                             ws.mu, s_out, m_out);
+    if (m > 0) {
+      cluster_sum_kernel<FT, VPL><<<dim3(nb_used, G), 256, 0, st>>>(
+          n, d, n_anchor, K, n_layers, fa, ws.nu, ws.rest, ws.mvec, ws.cw);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      cluster_mean_kernel<<<dim3(ceil_div(n_layers * K * d, 256), G), 256, 0, st>>>(d, K, n_layers,
+                                                                                  ws.cw, nb_used);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    score_rows_kernel<FT, VPL><<<dim3(std::max(1, ceil_div(m, 4)), G), 256, 0, st>>>(
+        n, d, n_anchor, K, n_layers, fa, ws.nu, ws.rest, ws.mvec, ws.cw, s_out, m_out);
     return hipGetLastError();
   }
 }
@@ -580,13 +666,10 @@ hipError_t dispatch_cluster(int G, int n, int d, int n_anchor, int K, int max_it
                             const FeatArgs& fa, const ScoreWs& ws, int32_t* cl, float* s,
                             float* mo, hipStream_t st) {
   if (d <= 512)
-    return launch_cluster_kernels<FT, 8, 8>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
-  if (d <= 1024) {
-    if (K <= 4)
-      return launch_cluster_kernels<FT, 16, 4>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
-    return launch_cluster_kernels<FT, 16, 8>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
-  }
-  return launch_cluster_kernels<FT, 32, 4>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
+    return launch_cluster_kernels<FT, 8>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
+  if (d <= 1024)
+    return launch_cluster_kernels<FT, 16>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
+  return launch_cluster_kernels<FT, 32>(G, n, d, n_anchor, K, max_iter, n_layers, fa, ws, cl, s, mo, st);
 }
 
 }  // namespace
@@ -595,9 +678,8 @@ hipError_t dispatch_cluster(int G, int n, int d, int n_anchor, int K, int max_it
 using namespace spider;
 
 extern "C" size_t spider_score_workspace_size(int G, int n, int d_v, int n_layers, int K) {
-  (void)K;
-  if (G <= 0 || n <= 0 || d_v <= 0 || n_layers <= 0) return 0;
-  return score_ws_layout(G, n, d_v, n_layers, nullptr, nullptr);
+  if (G <= 0 || n <= 0 || d_v <= 0 || n_layers <= 0 || K <= 0) return 0;
+  return score_ws_layout(G, n, d_v, n_layers, K, nullptr, nullptr);
 }
 
 extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers,
@@ -639,7 +721,7 @@ extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers
     SPIDER_REQUIRE(((uintptr_t)feats[l] % 16) == 0, SPIDER_ERR_UNSUPPORTED,
                    "spider_score: feats[%d] must be 16-byte aligned", l);
   }
-  const size_t need = score_ws_layout(G, n, d_v, n_layers, nullptr, nullptr);
+  const size_t need = score_ws_layout(G, n, d_v, n_layers, K, nullptr, nullptr);
   SPIDER_REQUIRE(workspace && workspace_bytes >= need, SPIDER_ERR_WORKSPACE,
                  "spider_score: workspace of %zu bytes needed, %zu given", need, workspace_bytes);
   SPIDER_REQUIRE(((uintptr_t)workspace % 256) == 0, SPIDER_ERR_WORKSPACE,
@@ -647,7 +729,7 @@ extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers
 
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   ScoreWs ws;
-  score_ws_layout(G, n, d_v, n_layers, &ws, reinterpret_cast<char*>(workspace));
+  score_ws_layout(G, n, d_v, n_layers, K, &ws, reinterpret_cast<char*>(workspace));
   FeatArgs fa;
   for (int l = 0; l < 8; ++l) fa.ptr[l] = l < n_layers ? feats[l] : nullptr;
   fa.stride_g = feat_stride_g;
@@ -668,7 +750,8 @@ extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers
   }
   {
     ProfScope ps(KC_ANCHOR_TOPK, st);
-    anchor_topk_kernel<<<G, 1024, 0, st>>>(n, n_anchor, a_out, cluster_out, s_out, ws.anc, ws.rest);
+    anchor_topk_kernel<<<G, 1024, 0, st>>>(n, n_anchor, a_out, cluster_out, s_out, ws.anc, ws.rest,
+                                            ws.cw.conv);
     SPIDER_LAUNCHED("anchor_topk");
   }
   {
