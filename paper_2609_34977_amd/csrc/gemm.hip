@@ -1,23 +1,21 @@
 // Decoder GEMMs: out = A[rows] x W^T with W in nn.Linear layout [N, K].
 //
-// bf16 path (gemm_bf16_kernel): built for the weight-streaming regime of a
-// pruned prefill (a few hundred rows against multi-MB weight matrices), and
-// for large row counts.  256 threads = 4 waves; block tile BM x BN x 32 with
-// v_mfma_f32_16x16x32_bf16 (fp32 accumulation); a wave owns a
-// (BM/WGM) x (BN/WGN) sub-tile.  For up to 256 rows one block covers every
-// row (BM = rows rounded up to 64), so each weight element is read from HBM
-// exactly once; the activations (a few MB) stay in L2.  The k-loop keeps a
-// ring of PF register stages of 16-byte global loads in flight (PF tiles
-// ahead), double-buffers LDS (row pitch 40 bf16: the 16 rows x 16 bytes of a
-// fragment read hit distinct banks) and needs one barrier per k-tile.  A rows
-// may be gathered through a row list.  Grouped launch: up to three problems
-// sharing K (Q over the query rows, K and V over all rows) in one grid.
-// Logical tiles are ordered (group, n-tile, k-split, m-tile) and the hardware
-// block id is remapped so consecutive logical tiles run on the same XCD
-// (blocks are dispatched round-robin over the 8 XCDs) and share its L2.
-// Epilogues: fp32 split-K partials (summed by the consumer kernel in fixed
-// order: deterministic without atomics), or the fused SwiGLU
-// silu(A Wg^T) * (A Wu^T) rounded to bf16 (dual weights, no split).
+// Up to 256 rows (the pruned-prefill regime: a few hundred rows against
+// multi-MB weight matrices) gemm_stream_kernel below streams every weight
+// element from HBM exactly once, straight into MFMA registers.  More rows use
+// gemm_bf16_kernel: 256 threads = 4 waves, block tile BM x BN x 32 with
+// v_mfma_f32_16x16x32_bf16 (fp32 accumulation), a wave owning a
+// (BM/WGM) x (BN/WGN) sub-tile; a ring of PF register stages of 16-byte
+// global loads in flight, double-buffered LDS (row pitch 40 bf16: the
+// 16 rows x 16 bytes of a fragment read hit distinct banks), one barrier per
+// k-tile.  Both kernels may gather A rows through a row list and take a
+// grouped launch: up to three problems sharing K (Q over the query rows, K and
+// V over all rows) in one grid.  Logical tiles are ordered (group, n-tile,
+// k-split, m-tile) and the hardware block id is remapped so consecutive
+// logical tiles run on the same XCD (blocks are dispatched round-robin over
+// the 8 XCDs) and share its L2.  Epilogues: fp32 split-K partials (summed by
+// the consumer kernel in fixed order: deterministic without atomics), or the
+// fused SwiGLU silu(A Wg^T) * (A Wu^T) rounded to bf16 (dual weights, no split).
 //
 // fp32 path (gemm_f32_kernel): 16x16 FMA tiles through LDS with the same
 // group/gather/split/epilogue semantics (used by fp32 workloads).
@@ -256,32 +254,46 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(GemmArgs a) {
 }
 
 // ------------------------------------------------------------------ weight streaming
-// gemm_ws_kernel: for M <= 32*MT rows (the pruned-prefill regime).  4 waves per
-// block; wave w owns NWT consecutive 32-column tiles (dual: NWT/2 tiles of
-// each weight matrix over the same columns).  Each lane streams one weight
-// row (n = lane % 32 of a tile) straight into MFMA B registers: per 64-wide
-// k-block it loads 64 contiguous bytes (k = 32*(lane/32) .. +32) and feeds
-// them to four v_mfma_f32_32x32x16_bf16 steps, so weights never touch LDS.
-// The activations (all M rows) are shared through a double-buffered LDS tile
-// of 64 k; their k order inside a block is the same permutation as the
-// weights' (a consistent permutation of k leaves the dot products unchanged).
-// Software pipeline with one barrier per k-block: at iteration kb the block
-// multiplies k-block kb, issues the global loads of k-block kb+LEAD for both
-// operands together (A into a register ring, W into the MFMA register ring),
-// and writes k-block kb+1's activations (loaded LEAD-1 iterations earlier)
-// to LDS.  Loads of one k-block are issued in the order they are consumed,
-// so the in-order vector-memory counter never makes a wait for near data
-// also wait for far data.
-template <int MT, int NWT, int LEAD, bool DUAL, bool NT = false>
-__global__ void __launch_bounds__(256) gemm_ws_kernel(GemmArgs a) {
-  constexpr int KB = 64, PITCH = KB + 8;
+// gemm_stream_kernel: up to 32*MT (<= 256) rows, the pruned-prefill regime.
+// 4 waves per block, one per SIMD.  Each wave streams 32 weight rows straight
+// into MFMA B registers: lane (n = lane % 32, half = lane / 32) loads 64
+// contiguous bytes per 64-wide k-block (k = 32*half .. +32) and feeds them to
+// four v_mfma_f32_32x32x16_bf16 steps, so weights never touch LDS.  Non-dual:
+// the block covers 128 output columns.  Dual (SwiGLU): waves 0-1 stream gate
+// rows and waves 2-3 up rows of the same 64 output columns; the up sums are
+// handed over through LDS and the epilogue writes bf16 silu(g) * u.
+//
+// Activations (all rows of the tile) go global -> LDS with global_load_lds
+// (no register round trip) into a ring of LEAD+1 stages of BM x 64.  Every
+// row is 128 B = eight 16-B chunks; chunk c of row r is stored at slot
+// c ^ (r & 7), so both the DMA writes (1 KB per instruction, 8 rows) and the
+// MFMA fragment reads (32 rows, one chunk) are free of bank conflicts.  MFMA
+// step q of a k-block takes chunk 4*half + q on both operands (a consistent
+// permutation of k leaves every dot product unchanged).
+//
+// Pipeline: at iteration kb the block multiplies k-block kb, then issues the
+// weight loads and activation DMA of k-block kb+LEAD, waits until k-block
+// kb+1 has landed and passes one barrier.  Every iteration issues the same
+// loads (the tail re-reads the last k-block into a slot never consumed), so
+// the wait is an exact count of outstanding loads; ring slots are
+// compile-time (k-block kb lives in slot kb % (LEAD+1)).  Rows past M read
+// row M-1 (their outputs are never stored).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int MT, int LEAD, bool DUAL>
+__global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
+  constexpr int KB = 64;
   constexpr int BM = 32 * MT;
-  constexpr int NCOLW = DUAL ? 32 * NWT / 2 : 32 * NWT;  // output columns per wave
-  constexpr int BN = 4 * NCOLW;
-  constexpr int A_CH = BM * (KB / 8) / 256;
-  static_assert(A_CH * 256 == BM * (KB / 8), "A tile split");
-  static_assert(!DUAL || NWT % 2 == 0, "dual needs pairs of tiles");
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * PITCH];
+  constexpr int BN = DUAL ? 64 : 128;  // output columns per block
+  constexpr int STAGES = LEAD + 1;
+  constexpr int STAGE_BYTES = BM * 128;
+  constexpr int PER_IT = 4 + MT;  // loads per wave per k-block: 4 weight, MT activation
+  static_assert(!DUAL || 2 * MT * 16 * 64 * 4 <= STAGES * STAGE_BYTES, "dual hand-over fits");
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[STAGES * STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hi = lane >> 5, lo = lane & 31;
@@ -291,122 +303,122 @@ __global__ void __launch_bounds__(256) gemm_ws_kernel(GemmArgs a) {
   const int kbeg = tc.s * a.k_per_split;
   const int kend = min(a.K, kbeg + a.k_per_split);
   const int nkb = kend > kbeg ? (kend - kbeg) / KB : 0;
-  const int col0 = tc.n0 + wave * NCOLW;  // first output column of this wave
+  const int col = tc.n0 + 32 * (DUAL ? (wave & 1) : wave) + lo;  // this lane's output column
+  const uint16_t* W = reinterpret_cast<const uint16_t*>(DUAL && wave >= 2 ? G.W2 : G.W);
+  const uint16_t* pw = W + (int64_t)col * a.K + kbeg + 32 * hi;
 
-  // weight row streamed by this lane for each of its tiles
-  const uint16_t* pw[NWT];
+  // activation DMA: instruction j of this wave fills tile rows 8g..8g+7,
+  // g = wave*MT + j; lane l takes row 8g + l/8 and chunk (l%8) ^ (l/8)
+  const uint16_t* pa[MT];
 #pragma unroll
-  for (int t = 0; t < NWT; ++t) {
-    const bool second = DUAL && t >= NWT / 2;
-    const int col = col0 + 32 * (DUAL ? (t % (NWT / 2)) : t) + lo;
-    const uint16_t* W = reinterpret_cast<const uint16_t*>(second ? G.W2 : G.W);
-    pw[t] = W + (int64_t)col * a.K + kbeg + 32 * hi;
-  }
-  const uint16_t* pa[A_CH];
-  int ca[A_CH];
-#pragma unroll
-  for (int c = 0; c < A_CH; ++c) {
-    const int lin = c * 256 + tid;
-    const int row = lin >> 3, col = (lin & 7) * 8;
-    ca[c] = row * PITCH + col;
-    pa[c] = nullptr;
-    if (tc.m0 + row < M) {
-      const int gm = tc.m0 + row;
-      const int src = G.rows ? G.rows[gm] : gm;
-      pa[c] = reinterpret_cast<const uint16_t*>(G.A) + (int64_t)src * a.lda + kbeg + col;
-    }
+  for (int j = 0; j < MT; ++j) {
+    const int g = wave * MT + j;
+    const int r = min(tc.m0 + 8 * g + (lane >> 3), M - 1);
+    const int src = G.rows ? G.rows[r] : r;
+    const int c = (lane & 7) ^ (lane >> 3);
+    pa[j] = reinterpret_cast<const uint16_t*>(G.A) + (int64_t)src * a.lda + kbeg + 8 * c;
   }
 
-  floatx16 acc[MT][NWT];
+  floatx16 acc[MT];
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int t = 0; t < NWT; ++t) acc[i][t] = floatx16{};
+  for (int i = 0; i < MT; ++i) acc[i] = floatx16{};
+  u32x4 wr[STAGES][4];
 
-  u32x4 wr[LEAD][NWT][4];
-  u32x4 ar[LEAD][A_CH];
-  auto issue = [&](int kb, u32x4 (&xa)[A_CH], u32x4 (&xw)[NWT][4]) {
+  auto issue = [&](int kb, auto S) {
+    constexpr int st = decltype(S)::value;
 #pragma unroll
-    for (int c = 0; c < A_CH; ++c)
-      xa[c] = pa[c] ? *reinterpret_cast<const u32x4*>(pa[c] + kb * KB) : u32x4{0, 0, 0, 0};
+    for (int q = 0; q < 4; ++q) wr[st][q] = *reinterpret_cast<const u32x4*>(pw + kb * KB + 8 * q);
 #pragma unroll
-    for (int t = 0; t < NWT; ++t)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const u32x4* src = reinterpret_cast<const u32x4*>(pw[t] + kb * KB + 8 * q);
-        // weights are read once: stream them past L2 so the activations stay resident
-        xw[t][q] = NT ? __builtin_nontemporal_load(src) : *src;
-      }
+    for (int j = 0; j < MT; ++j)
+      __builtin_amdgcn_global_load_lds(
+          reinterpret_cast<const void*>(pa[j] + kb * KB),
+          (__attribute__((address_space(3))) void*)(ring + st * STAGE_BYTES + (wave * MT + j) * 1024), 16,
+          0, 0);
   };
-  auto store_a = [&](int buf, const u32x4 (&xa)[A_CH]) {
-#pragma unroll
-    for (int c = 0; c < A_CH; ++c) *reinterpret_cast<u32x4*>(&sA[buf][ca[c]]) = xa[c];
-  };
-  // One k-block = 4 MFMA steps.  A fragments of step q+1 are read from LDS
-  // while the MFMAs of step q issue (one wave per SIMD: nothing else would
-  // hide the LDS latency).
-  auto compute = [&](int buf, const u32x4 (&w)[NWT][4]) {
-    const uint16_t* A = sA[buf];
+  auto compute = [&](auto S) {
+    constexpr int st = decltype(S)::value;
+    const uint8_t* tile = ring + st * STAGE_BYTES;
     bf16x8 af[2][MT];
     auto frags = [&](int q, bf16x8 (&dst)[MT]) {
 #pragma unroll
       for (int i = 0; i < MT; ++i)
         dst[i] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(&A[(32 * i + lo) * PITCH + 32 * hi + 8 * q]));
+            bf16x8, *reinterpret_cast<const u32x4*>(tile + (32 * i + lo) * 128 + 16 * ((4 * hi + q) ^ (lo & 7))));
     };
     frags(0, af[0]);
     static_for<0, 4>([&](auto Q) {
       constexpr int q = Q.value;
       if constexpr (q + 1 < 4) frags(q + 1, af[(q + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int t = 0; t < NWT; ++t)
-          acc[i][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              af[q & 1][i], __builtin_bit_cast(bf16x8, w[t][q]), acc[i][t], 0, 0, 0);
+        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][i], __builtin_bit_cast(bf16x8, wr[st][q]),
+                                                         acc[i], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     });
   };
 
-  // prologue: k-blocks 0..LEAD-1 in flight (k-block j in ring slot j % LEAD),
-  // k-block 0's activations in LDS buffer 0
-  static_for<0, LEAD>([&](auto P) {
-    if (P.value < nkb) issue(P.value, ar[P.value], wr[P.value]);
-  });
-  if (nkb > 0) store_a(0, ar[0]);
-  __syncthreads();
-  for (int k0 = 0; k0 < nkb; k0 += LEAD) {
-    static_for<0, LEAD>([&](auto J) {
-      constexpr int slot = J.value;
-      constexpr int nxt = (J.value + 1) % LEAD;
-      const int kb = k0 + J.value;
-      if (kb < nkb) {
-        compute(kb & 1, wr[slot]);
-        if (kb + LEAD < nkb) issue(kb + LEAD, ar[slot], wr[slot]);
-        if (kb + 1 < nkb) store_a((kb + 1) & 1, ar[nxt]);
-        __syncthreads();
-      }
+  if (nkb > 0) {
+    static_for<0, LEAD>([&](auto P) { issue(min((int)P.value, nkb - 1), P); });
+    wait_vmcnt<(LEAD - 1) * PER_IT>();
+    __builtin_amdgcn_s_barrier();
+    // EXACT: all loads issued here are consumed later, so the count holds; in
+    // the remainder the compiler may drop unused weight loads, so wait for all
+    auto body = [&](int kb, auto J, auto EXACT) {
+      constexpr int j = decltype(J)::value;
+      compute(J);
+      issue(min(kb + LEAD, nkb - 1), std::integral_constant<int, (j + LEAD) % STAGES>{});
+      if constexpr (decltype(EXACT)::value) wait_vmcnt<(LEAD - 1) * PER_IT>();
+      else wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+    };
+    int k0 = 0;
+    for (; k0 + STAGES <= nkb; k0 += STAGES)
+      static_for<0, STAGES>([&](auto J) { body(k0 + J.value, J, std::true_type{}); });
+    const int rem = nkb - k0;
+    static_for<0, STAGES>([&](auto J) {
+      if (J.value < rem) body(k0 + J.value, J, std::false_type{});
     });
+    wait_vmcnt<0>();
   }
 
-  // epilogue: D[m][n], n = lane%32 (this lane's weight row), m = 8*(r/4) + 4*hi + r%4
-  constexpr int NOUT = DUAL ? NWT / 2 : NWT;
+  // D layout of 32x32 MFMA: n = lane % 32, m = 8*(r/4) + 4*(lane/32) + r%4
+  if constexpr (DUAL) {
+    __syncthreads();  // ring free: up waves hand their sums to the gate waves
+    float* xfer = reinterpret_cast<float*>(ring);
+    if (wave >= 2) {
 #pragma unroll
-  for (int t = 0; t < NOUT; ++t) {
-    const int ncol = col0 + 32 * t + lo;
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          *reinterpret_cast<floatx4*>(xfer + (((wave - 2) * MT + i) * 64 + lane) * 16 + 4 * v) =
+              floatx4{acc[i][4 * v], acc[i][4 * v + 1], acc[i][4 * v + 2], acc[i][4 * v + 3]};
+    }
+    __syncthreads();
+    if (wave < 2) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const floatx4 u = *reinterpret_cast<const floatx4*>(xfer + ((wave * MT + i) * 64 + lane) * 16 + 4 * v);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * v + e;
+            const int m = tc.m0 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
+            if (m < M)
+              reinterpret_cast<uint16_t*>(G.out)[(int64_t)m * G.ldo + col] =
+                  f32_to_bf16_bits(silu(acc[i][r]) * u[e]);
+          }
+        }
+    }
+  } else {
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = tc.m0 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
-        if (m < M) {
-          if constexpr (DUAL) {
-            const float v = silu(acc[i][t][r]) * acc[i][t + NWT / 2][r];
-            reinterpret_cast<uint16_t*>(G.out)[(int64_t)m * G.ldo + ncol] = f32_to_bf16_bits(v);
-          } else {
-            reinterpret_cast<float*>(G.out)[tc.s * G.sstride + (int64_t)m * G.ldo + ncol] =
-                acc[i][t][r];
-          }
-        }
+        if (m < M)
+          reinterpret_cast<float*>(G.out)[tc.s * G.sstride + (int64_t)m * G.ldo + col] = acc[i][r];
       }
   }
 }
@@ -457,31 +469,32 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
 
 struct TileCfg {
   int BM, BN;
-  bool ws;  // weight-streaming kernel
+  bool stream;  // weight-streaming kernel
 };
 
-// Tile shape.  Up to 256 rows one M-tile covers every row so each weight
-// element is read from HBM once.  Non-dual skinny GEMMs use the
-// weight-streaming kernel (4 waves x 32 columns, BM = rows rounded up to 64,
-// at most 192); the dual SwiGLU GEMM and everything with more rows use the
-// LDS-staged kernel.
+// Tile shape.  Up to 256 rows the weight-streaming kernel covers every row in
+// one tile (BM = rows rounded up to 64), so each weight element is read from
+// HBM once; more rows use the LDS-staged kernel.
 TileCfg pick_bf16_tile(int maxM, bool dual) {
-  if (maxM <= 192 && !dual) {
-    const int bm = std::max(64, (maxM + 63) / 64 * 64);
-    return TileCfg{bm, 128, true};
-  }
   if (maxM <= 256) {
     const int bm = std::max(64, (maxM + 63) / 64 * 64);
-    return dual ? TileCfg{bm, 32, false} : TileCfg{bm, 64, false};
+    return TileCfg{bm, dual ? 64 : 128, true};
   }
   return dual ? TileCfg{128, 64, false} : TileCfg{128, 128, false};
 }
 
 constexpr int kTargetBlocks = 256;
 
-int choose_split(int tiles, int K, int split_max, int kgran) {
+// LDS-staged kernel: split until the grid covers the chip.  Streaming kernel
+// (one block per CU): the largest split whose grid still fits in one wave of
+// blocks; a second partial wave costs more than it hides.
+int choose_split(int tiles, int K, int split_max, int kgran, bool stream) {
   int split = 1;
-  while (split < split_max && tiles * split < kTargetBlocks && K / (kgran * split * 2) >= 4) split *= 2;
+  if (stream) {
+    while (split < split_max && tiles * split * 2 <= kTargetBlocks && K / (kgran * split * 2) >= 4) split *= 2;
+  } else {
+    while (split < split_max && tiles * split < kTargetBlocks && K / (kgran * split * 2) >= 4) split *= 2;
+  }
   return split;
 }
 
@@ -508,9 +521,10 @@ void launch_cfg(const GemmArgs& a, hipStream_t st) {
   gemm_bf16_kernel<BM, BN, WGM, WGN, 4, DUAL><<<a.total_tiles, 256, 0, st>>>(a);
 }
 
-template <int MT>
-void launch_ws(const GemmArgs& a, hipStream_t st) {
-  gemm_ws_kernel<MT, 1, 3, false><<<a.total_tiles, 256, 0, st>>>(a);
+template <int MT, bool DUAL>
+void launch_stream(const GemmArgs& a, hipStream_t st) {
+  constexpr int LEAD = MT <= 2 ? 3 : 2;
+  gemm_stream_kernel<MT, LEAD, DUAL><<<a.total_tiles, 256, 0, st>>>(a);
 }
 
 }  // namespace
@@ -518,7 +532,7 @@ void launch_ws(const GemmArgs& a, hipStream_t st) {
 int gemm_split_for(int M, int N, int K, bool dual, bool bf16, int split_max) {
   if (dual || !bf16) return 1;
   TileCfg tc = pick_bf16_tile(M, false);
-  return choose_split(ceil_div(M, tc.BM) * (N / tc.BN), K, split_max, tc.ws ? 64 : 32);
+  return choose_split(ceil_div(M, tc.BM) * (N / tc.BN), K, split_max, tc.stream ? 64 : 32, tc.stream);
 }
 
 hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
@@ -527,21 +541,25 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
   const bool dual = a.epilogue == EPI_SWIGLU;
   TileCfg tc = pick_bf16_tile(maxM, dual);
   for (int i = 0; i < a.ngroups; ++i)
-    if (a.g[i].N % tc.BN) {
-      if (tc.ws) tc = TileCfg{std::max(64, (maxM + 63) / 64 * 64), 64, false};
-      if (a.g[i].N % tc.BN) return hipErrorInvalidValue;
+    if (a.g[i].N % tc.BN || (tc.stream && a.K % 64)) {
+      tc = maxM <= 256 ? TileCfg{std::max(64, (maxM + 63) / 64 * 64), dual ? 32 : 64, false}
+                       : TileCfg{128, dual ? 64 : 128, false};
+      break;
     }
-  const int kgran = tc.ws ? 64 : 32;
+  for (int i = 0; i < a.ngroups; ++i)
+    if (a.g[i].N % tc.BN) return hipErrorInvalidValue;
+  const int kgran = tc.stream ? 64 : 32;
   if (a.K % kgran) return hipErrorInvalidValue;
-  a.split = dual ? 1 : choose_split(tiles_for(a, tc.BM, tc.BN), a.K, split_max, kgran);
+  a.split = dual ? 1 : choose_split(tiles_for(a, tc.BM, tc.BN), a.K, split_max, kgran, tc.stream);
   a.k_per_split = ceil_div(ceil_div(a.K, kgran), a.split) * kgran;
   fill_tiles(a, tc.BM, tc.BN);
   if (a.total_tiles == 0) return hipSuccess;
-  if (tc.ws) {
+  if (tc.stream) {
     switch (tc.BM) {
-      case 64: launch_ws<2>(a, st); break;
-      case 128: launch_ws<4>(a, st); break;
-      default: launch_ws<6>(a, st); break;
+      case 64: dual ? launch_stream<2, true>(a, st) : launch_stream<2, false>(a, st); break;
+      case 128: dual ? launch_stream<4, true>(a, st) : launch_stream<4, false>(a, st); break;
+      case 192: dual ? launch_stream<6, true>(a, st) : launch_stream<6, false>(a, st); break;
+      default: dual ? launch_stream<8, true>(a, st) : launch_stream<8, false>(a, st); break;
     }
   } else if (dual) {
     switch (tc.BM * 1000 + tc.BN) {

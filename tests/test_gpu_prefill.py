@@ -68,6 +68,8 @@ PARITY = {
     "7b_dense": ("llava15_7b", 2, [0, 192], 64, 0.0, 0.0, False),
     "7b_two_samples_ragged": ("llava15_7b", 2, [0, 131, 324], 64, 0.3, 0.3, True),
     "7b_704_rows_layer_mask": ("llava_next_7b", 2, [0, 704], 64, 0.5, 0.5, False),
+    "7b_256_rows": ("llava15_7b", 1, [0, 256], 64, 0.3, 0.3, True),
+    "7b_97_rows_dense": ("llava15_7b", 1, [0, 97], 64, 0.0, 0.0, False),
     "13b_two_samples": ("llava15_13b", 1, [0, 256, 512], 128, 0.4, 0.2, True),
 }
 
