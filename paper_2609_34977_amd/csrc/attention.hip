@@ -3,16 +3,19 @@
 // the query's sample up to the query's own position (VSkip-Attn rows still
 // serve as keys and values, Sec. 3.2).
 //
-// bf16, dh = 128 (attention_bf16_kernel): one wave per (block of 32 queries,
-// head).  S^T = K Q^T is computed 32 keys at a time with
+// bf16, dh = 128 (attention_bf16_kernel): one block of 4 waves per (block of
+// 32 queries, head).  The key range of the 32 queries is cut into 32-key
+// blocks aligned to multiples of 32, dealt round-robin to the 4 waves; each
+// wave keeps its own online softmax and the four partial results are merged
+// through LDS in fixed wave order at the end.  S^T = K Q^T is computed with
 // v_mfma_f32_32x32x16_bf16 so that each lane owns one query (lane % 32) and
-// 16 of the 32 keys (the other 16 are in lane ^ 32); the online softmax is
-// per lane (fp32, exp2 with the 1/sqrt(dh)*log2(e) scale folded in) plus one
+// 16 of the 32 keys (the other 16 are in lane ^ 32); the softmax runs per lane
+// in fp32 (exp2 with the 1/sqrt(dh)*log2(e) scale folded in) plus one
 // cross-half exchange; O^T += V^T P^T with P taken straight from the S^T
 // registers (the key order inside an MFMA k-block is any permutation as long
-// as both operands use it).  V tiles are transposed through LDS so every lane
-// reads its 8 keys of a dh column as two 8-byte words.  Masking: key row j is
-// visible to query row q iff start(q) <= j <= q.
+// as both operands use it) and V^T fragments read from the transposed V
+// written by the QKV finalize (8 bytes = 4 keys per load, no LDS staging).
+// Masking: key row j is visible to query row q iff start(q) <= j <= q.
 //
 // fp32 (attention_f32_kernel): one wave per (query, head), scores in LDS,
 // wave reductions; any even dh <= 256.
@@ -23,17 +26,18 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-__global__ void __launch_bounds__(64) attention_bf16_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
   constexpr int DH = 128;
-  constexpr int VP = 32 + 4;  // key pitch of the transposed V tile (bf16)
-  __shared__ __attribute__((aligned(16))) uint16_t sV[DH * VP];
-  const int lane = threadIdx.x, hi = lane >> 5, lo = lane & 31;
+  constexpr int NW = 4;
+  __shared__ float xm[NW - 1][32], xl[NW - 1][32];
+  __shared__ __attribute__((aligned(16))) float xo[NW - 1][64 * 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hi = lane >> 5, lo = lane & 31;
   const int h = blockIdx.y;
   const int qa = blockIdx.x * 32 + lo;
   const bool qok = qa < a.nq;
   const uint16_t* Q = reinterpret_cast<const uint16_t*>(a.q);
   const uint16_t* Kp = reinterpret_cast<const uint16_t*>(a.k);
-  const uint16_t* Vp = reinterpret_cast<const uint16_t*>(a.v);
+  const uint16_t* VT = reinterpret_cast<const uint16_t*>(a.v);
   const int qrow = qok ? a.q_rows[qa] : -1;
   const int qstart = qok ? a.row_start[qrow] : 0x7FFFFFFF;
 
@@ -41,51 +45,51 @@ __global__ void __launch_bounds__(64) attention_bf16_kernel(AttnArgs a) {
   bf16x8 qf[DH / 16];
 #pragma unroll
   for (int t = 0; t < DH / 16; ++t) {
-    uint4 u = make_uint4(0, 0, 0, 0);
-    if (qok) u = *reinterpret_cast<const uint4*>(Q + (int64_t)qa * a.d + h * DH + 16 * t + 8 * hi);
+    u32x4 u = {0, 0, 0, 0};
+    if (qok) u = *reinterpret_cast<const u32x4*>(Q + (int64_t)qa * a.d + h * DH + 16 * t + 8 * hi);
     qf[t] = __builtin_bit_cast(bf16x8, u);
   }
-  // key range of the block
+  // key range of the 32 queries (every block holds at least one query)
   int lo_row = qstart, hi_row = qrow;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
     lo_row = min(lo_row, __shfl_xor(lo_row, o, 64));
     hi_row = max(hi_row, __shfl_xor(hi_row, o, 64));
   }
+  const int jb0 = lo_row & ~31;
+  const int nblk = (hi_row - jb0) / 32 + 1;
   const float sc = a.scale * kLog2e;
   float m_run = -INFINITY, l_run = 0.f;
   floatx16 o[DH / 32];
 #pragma unroll
   for (int c = 0; c < DH / 32; ++c) o[c] = floatx16{};
 
-  for (int j0 = lo_row; j0 <= hi_row; j0 += 32) {
-    // ---- S^T = K Q^T for keys j0 .. j0+31
+  for (int bi = wave; bi < nblk; bi += NW) {
+    const int j0 = jb0 + 32 * bi;
+    // ---- loads of this key block: K rows j0 + lane%32, V^T keys j0 .. j0+31
     const int kr = j0 + lo;
-    const bool kok = kr <= hi_row && kr < a.rows;
-    floatx16 s = {};
+    const bool kok = kr <= hi_row;
+    u32x4 kf[DH / 16];
 #pragma unroll
     for (int t = 0; t < DH / 16; ++t) {
-      uint4 u = make_uint4(0, 0, 0, 0);
-      if (kok) u = *reinterpret_cast<const uint4*>(Kp + (int64_t)kr * a.d + h * DH + 16 * t + 8 * hi);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, u), qf[t], s, 0, 0, 0);
+      kf[t] = u32x4{0, 0, 0, 0};
+      if (kok) kf[t] = *reinterpret_cast<const u32x4*>(Kp + (int64_t)kr * a.d + h * DH + 16 * t + 8 * hi);
     }
-    // ---- stage V^T tile in LDS: sV[dh][key]
-    __syncthreads();
+    // V^T fragment (c, u): dh column 32c + lane%32, keys 16u + 4hi + [0,4) and 16u + 8 + 4hi + [0,4)
+    uint2 vf[DH / 32][2][2];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int lin = c * 64 + lane;  // 512 chunks of 8 dh
-      const int key = lin >> 4, ch = lin & 15;
-      const int vr = j0 + key;
-      uint4 u = make_uint4(0, 0, 0, 0);
-      if (vr <= hi_row && vr < a.rows)
-        u = *reinterpret_cast<const uint4*>(Vp + (int64_t)vr * a.d + h * DH + ch * 8);
-      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+    for (int c = 0; c < DH / 32; ++c)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        sV[(ch * 8 + 2 * e) * VP + key] = (uint16_t)(w[e] & 0xFFFFu);
-        sV[(ch * 8 + 2 * e + 1) * VP + key] = (uint16_t)(w[e] >> 16);
+      for (int u = 0; u < 2; ++u) {
+        const uint16_t* base = VT + (int64_t)(h * DH + 32 * c + lo) * a.ldvt + j0 + 16 * u + 4 * hi;
+        vf[c][u][0] = *reinterpret_cast<const uint2*>(base);
+        vf[c][u][1] = *reinterpret_cast<const uint2*>(base + 8);
       }
-    }
+    // ---- S^T = K Q^T
+    floatx16 s = {};
+#pragma unroll
+    for (int t = 0; t < DH / 16; ++t)
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[t]), qf[t], s, 0, 0, 0);
     // ---- online softmax (this lane: query lo, keys 8*(r/4) + 4*hi + r%4)
     float mx = -INFINITY;
 #pragma unroll
@@ -127,24 +131,59 @@ __global__ void __launch_bounds__(64) attention_bf16_kernel(AttnArgs a) {
       for (int e = 0; e < 4; ++e)
         w[e] = (uint32_t)f32_to_bf16_bits(p[8 * u + 2 * e]) |
                ((uint32_t)f32_to_bf16_bits(p[8 * u + 2 * e + 1]) << 16);
-      pf[u] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+      pf[u] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
     }
-    __syncthreads();
 #pragma unroll
-    for (int c = 0; c < DH / 32; ++c) {
-      const int dcol = c * 32 + lo;
+    for (int c = 0; c < DH / 32; ++c)
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        // keys 16u + 4hi + [0,4) and 16u + 8 + 4hi + [0,4), matching p[8u .. 8u+7]
-        const uint2 v0 = *reinterpret_cast<const uint2*>(&sV[dcol * VP + 16 * u + 4 * hi]);
-        const uint2 v1 = *reinterpret_cast<const uint2*>(&sV[dcol * VP + 16 * u + 8 + 4 * hi]);
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, make_uint4(v0.x, v0.y, v1.x, v1.y));
-        o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[u], o[c], 0, 0, 0);
+        const bf16x8 v8 = __builtin_bit_cast(
+            bf16x8, u32x4{vf[c][u][0].x, vf[c][u][0].y, vf[c][u][1].x, vf[c][u][1].y});
+        o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v8, pf[u], o[c], 0, 0, 0);
       }
-    }
   }
-  if (!qok) return;
-  const float inv = l_run > 0.f ? 1.0f / l_run : 0.f;
+
+  // ---- merge the waves' partial softmax states (fixed order 0..3)
+  if (wave > 0) {
+    if (hi == 0) {
+      xm[wave - 1][lo] = m_run;
+      xl[wave - 1][lo] = l_run;
+    }
+    float* dst = xo[wave - 1] + lane * 64;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        *reinterpret_cast<floatx4*>(dst + 16 * c + 4 * v) =
+            floatx4{o[c][4 * v], o[c][4 * v + 1], o[c][4 * v + 2], o[c][4 * v + 3]};
+  }
+  __syncthreads();
+  if (wave != 0 || !qok) return;
+  float M = m_run;
+#pragma unroll
+  for (int w = 0; w < NW - 1; ++w) M = fmaxf(M, xm[w][lo]);
+  const float f0 = m_run == -INFINITY ? 0.f : exp2f(m_run - M);
+  float L = f0 * l_run;
+#pragma unroll
+  for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[c][r] *= f0;
+#pragma unroll
+  for (int w = 0; w < NW - 1; ++w) {
+    const float mw = xm[w][lo];
+    const float fw = mw == -INFINITY ? 0.f : exp2f(mw - M);
+    L += fw * xl[w][lo];
+    const float* srcp = xo[w] + lane * 64;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const floatx4 x = *reinterpret_cast<const floatx4*>(srcp + 16 * c + 4 * v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[c][4 * v + e] += fw * x[e];
+      }
+  }
+  const float inv = L > 0.f ? 1.0f / L : 0.f;
   uint16_t* O = reinterpret_cast<uint16_t*>(a.o) + (int64_t)qa * a.d + h * DH;
 #pragma unroll
   for (int c = 0; c < DH / 32; ++c)
@@ -219,8 +258,9 @@ __global__ void __launch_bounds__(64) attention_f32_kernel(AttnArgs a) {
 
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t st) {
   if (a.nq == 0) return hipSuccess;
+  if (a.dh != 128 || a.ldvt < ((a.rows + 31) / 32) * 32 || a.ldvt % 32) return hipErrorInvalidValue;
   dim3 grid(ceil_div(a.nq, 32), a.H);
-  attention_bf16_kernel<<<grid, 64, 0, st>>>(a);
+  attention_bf16_kernel<<<grid, 256, 0, st>>>(a);
   return hipGetLastError();
 }
 

@@ -49,7 +49,8 @@ struct AttnArgs {
   const void* q;           // [nq, d] (row a = query a)
   const int32_t* q_rows;   // [nq] packed row of query a
   const void* k;           // [rows, d]
-  const void* v;           // [rows, d]
+  const void* v;           // bf16: V^T [d][ldvt] (rows >= `rows` zero); fp32: [rows, d]
+  int64_t ldvt;            // row stride of V^T (a multiple of 32); 0 for row-major V
   const int32_t* row_start;  // [rows] first row of the sample that owns the row
   void* o;                 // [nq, d]
   int nq, rows, H, dh, d;

@@ -151,15 +151,47 @@ void launch_norm(int R, float* h, int d, const float* P, int psplit, int64_t pst
     norm_kernel<AT, 8><<<R, 256, 0, st>>>(h, d, P, psplit, pstride, pslot, w, eps, nslot, all_rows, out);
 }
 
-// Blocks [0, nq): Q rows, [nq, nq+R): K rows, [nq+R, nq+2R): V rows.
-// Sums split partials, applies rotate-half RoPE to Q and K, stores act dtype.
+// Blocks [0, nq): Q rows, [nq, nq+R): K rows; then V.  Sums split partials,
+// applies rotate-half RoPE to Q and K, stores act dtype.  V: with ldvt == 0
+// one block per row, row-major [R, d]; with ldvt > 0 (bf16) V is stored
+// transposed, V^T [d][ldvt] with ldvt = R rounded up to 32 and rows R..ldvt-1
+// zero, one block per 32-row x 64-column tile (transposed through LDS).
 template <typename AT>
 __global__ void __launch_bounds__(256) qkv_finalize_kernel(
     const float* __restrict__ Pq, const float* __restrict__ Pk, const float* __restrict__ Pv,
     int split, int64_t pstride, int nq, int R, int d, int dh, const int32_t* __restrict__ q_rows,
     const int32_t* __restrict__ pos, const float2* __restrict__ rope, AT* __restrict__ Q,
-    AT* __restrict__ K, AT* __restrict__ V) {
+    AT* __restrict__ K, AT* __restrict__ V, int64_t ldvt) {
   int b = blockIdx.x;
+  if (ldvt > 0 && b >= nq + R) {
+    // one 32 x 64 tile of V, written transposed
+    __shared__ __attribute__((aligned(16))) uint16_t tT[64 * 40];  // [column][row], pitch 40
+    const int vb = b - nq - R, ntc = d / 64;
+    const int rt = vb / ntc, ct = vb - rt * ntc;
+    const int t = threadIdx.x;
+    {
+      const int r = t >> 3, c8 = (t & 7) * 8;
+      const int row = rt * 32 + r, col = ct * 64 + c8;
+      float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if (row < R) {
+        for (int s = 0; s < split; ++s) {
+          const float4* src = reinterpret_cast<const float4*>(Pv + s * pstride + (int64_t)row * d + col);
+          const float4 v0 = src[0], v1 = src[1];
+          x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
+          x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) tT[(c8 + e) * 40 + r] = f32_to_bf16_bits(x[e]);
+    }
+    __syncthreads();
+    {
+      const int cidx = t >> 2, k8 = (t & 3) * 8;
+      const u32x4 w = *reinterpret_cast<const u32x4*>(&tT[cidx * 40 + k8]);
+      *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(V) + (int64_t)(ct * 64 + cidx) * ldvt + rt * 32 + k8) = w;
+    }
+    return;
+  }
   const float* P;
   AT* out;
   int prow, p = -1;
@@ -230,6 +262,9 @@ struct PrefillWs {
   size_t bytes;
 };
 
+// Rows of the transposed V buffer: R rounded up to the 32-key blocks of attention.
+int vt_rows(int R) { return (R + 31) / 32 * 32; }
+
 size_t table_ints_bound(int L, int R) { return (size_t)R * 2 + (size_t)L * 4 * R + 64; }
 
 PrefillWs prefill_layout(const spider_decoder_cfg& c, int R, char* base) {
@@ -248,7 +283,7 @@ PrefillWs prefill_layout(const spider_decoder_cfg& c, int R, char* base) {
   w.xn = take((size_t)R * c.d * es);
   w.q = take((size_t)R * c.d * es);
   w.k = take((size_t)R * c.d * es);
-  w.v = take((size_t)R * c.d * es);
+  w.v = take((size_t)vt_rows(R) * c.d * es);  // bf16: V^T [d][vt_rows(R)]
   w.o = take((size_t)R * c.d * es);
   w.act = take((size_t)R * c.d_ff * es);
   w.Pq = reinterpret_cast<float*>(take((size_t)sm * R * c.d * 4));
@@ -420,15 +455,17 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
       }
       {
         ProfScope ps(KC_QKV_FINALIZE, st);
-        qkv_finalize_kernel<AT><<<T.nA + 2 * R, 256, 0, st>>>(ws.Pq, ws.Pk, ws.Pv, ga.split, pstride,
-                                                              T.nA, R, d, dh, ws.tables + T.offA,
-                                                              dpos, ws.rope, qb, kb, vb);
+        const int64_t ldvt = bf16 ? vt_rows(R) : 0;
+        const int vblocks = bf16 ? (vt_rows(R) / 32) * (d / 64) : R;
+        qkv_finalize_kernel<AT><<<T.nA + R + vblocks, 256, 0, st>>>(
+            ws.Pq, ws.Pk, ws.Pv, ga.split, pstride, T.nA, R, d, dh, ws.tables + T.offA, dpos, ws.rope, qb,
+            kb, vb, ldvt);
         SPIDER_LAUNCHED("qkv_finalize");
       }
       {
         ProfScope ps(KC_ATTENTION, st);
-        AttnArgs aa{qb, ws.tables + T.offA, kb, vb, dstart, ob, T.nA, R, c.H, dh, d,
-                    (float)(1.0 / std::sqrt((double)dh))};
+        AttnArgs aa{qb, ws.tables + T.offA, kb, vb, bf16 ? (int64_t)vt_rows(R) : 0, dstart, ob, T.nA, R,
+                    c.H, dh, d, (float)(1.0 / std::sqrt((double)dh))};
         hipError_t e = bf16 ? launch_attention_bf16(aa, st) : launch_attention_f32(aa, max_s, st);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "attention: %s", hipGetErrorString(e));
       }
