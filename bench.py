@@ -45,6 +45,10 @@ def parse():
     p.add_argument("--skip-p", type=float, default=None)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-layers", type=int, default=8)
+    p.add_argument("--copy-probe-mib", type=int, default=0,
+                   help="run one plain device copy of this size after warm-up (counter calibration)")
+    p.add_argument("--score-sweep", action="store_true",
+                   help="instead of the step: time scoring over 20/64/256/512 tiles (one JSON line each)")
     return p.parse_args()
 
 
@@ -145,6 +149,49 @@ def cpu_baseline(w, n_layers: int, W_dev=None):
                        f"time scaled by {w.dec.L}/{n_layers}; {rows} rows")}
 
 
+def score_sweep(w, dev, args):
+    """Scoring (spider_score) over many tiles: time per call, and the compulsory
+    HBM bytes (CLS attention + every tapped layer's features, read once, plus
+    the outputs) over that time.  Tiles are the workload's synthetic tiles
+    repeated up to G (20 distinct tiles are generated)."""
+    import dataclasses
+    from synth.vision import vision_inputs
+    from paper_2609_34977_amd import _lib
+
+    sc = w.score
+    base = dataclasses.replace(sc, G=20)
+    attn0, feats0 = vision_inputs(base, w.seed)
+    attn0, feats0 = attn0.to(dev), [f.to(dev) for f in feats0]
+    n_anchor, _ = _lib.budget(sc.keep, sc.r_num, sc.r_den)
+    for G in (20, 64, 256, 512):
+        reps = (G + 19) // 20
+        attn = attn0.repeat(reps, 1, 1)[:G].contiguous()
+        feats = [f.repeat(reps, 1, 1)[:G].contiguous() for f in feats0]
+        for _ in range(2):
+            _lib.score(attn, feats, min(n_anchor, sc.n), sc.K, sc.kmeans_iter)
+        torch.cuda.synchronize()
+        _lib.profile_mask(None)
+        _lib.profile_enable(True)
+        iters = 5
+        t0 = time.perf_counter()
+        for _ in range(iters):
+            _lib.score(attn, feats, min(n_anchor, sc.n), sc.K, sc.kmeans_iter)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        prof = _lib.profile_read()
+        _lib.profile_enable(False)
+        ms = (t1 - t0) * 1e3 / iters
+        H, n, dv = attn.shape[1], sc.n, feats[0].shape[2]
+        byts = G * (H * (n + 1) * 4 + len(feats) * n * dv * feats[0].element_size() + 16 * n)
+        kms = {k: round(v[1] / iters, 4) for k, v in prof.items() if v[0]}
+        ach = byts / (ms * 1e-3) / 1e9
+        print(json.dumps({"mode": "score_sweep", "tiles": G, "ms_per_call": ms,
+                          "compulsory_bytes": byts, "achieved_GBs": ach, "frac_of_hbm_peak": ach / HBM_PEAK_GBS,
+                          "kernel_ms_per_call": kms}), flush=True)
+        del attn, feats
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -158,6 +205,9 @@ def main():
     w = get_workload(args.workload, keep=args.keep, L=args.layers, skip_p=args.skip_p)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.score_sweep:
+        score_sweep(w, dev, args)
+        return
     t_setup = time.perf_counter()
     attn, feats, src, text, W, pol = build_inputs(w, dev)
     sc, dec = w.score, w.dec
@@ -174,6 +224,12 @@ def main():
         out = pipe.step(attn, feats, src, text, pol)
     torch.cuda.synchronize()
     print("# warmup done", file=sys.stderr, flush=True)
+    if args.copy_probe_mib > 0:
+        a = torch.empty(args.copy_probe_mib << 20, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
 
     # per-class breakdown (events around every launch) from a separate pass
     n_full = max(2, min(args.steps, 5))
@@ -223,9 +279,11 @@ def main():
             roof = {"bound": "mfma", "achieved": ach, "peak": pk, "unit": "TFLOP/s", "frac": ach / pk}
     else:
         roof = {"bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": None}
+    from paper_2609_34977_amd.profiling import recorded_traffic
     roof.update({"kernel": dom, "launches_per_step": prof[dom][0] // args.steps,
                  "avg_launch_us": prof[dom][1] * 1e3 / max(prof[dom][0], 1),
-                 "traffic": None})
+                 "traffic": recorded_traffic(os.path.join(ROOT, "profiles", f"{dom}_traffic.json"), dom)
+                 if dom in ("gemm_gateup",) else None})
     prefill_flops = sum(v[1] for v in alg.values())
     res = {
         "metric": METRIC,
