@@ -255,29 +255,34 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(GemmArgs a) {
 
 // ------------------------------------------------------------------ weight streaming
 // gemm_stream_kernel: up to 32*MT (<= 256) rows, the pruned-prefill regime.
-// 4 waves per block, one per SIMD.  Each wave streams 32 weight rows straight
-// into MFMA B registers: lane (n = lane % 32, half = lane / 32) loads 64
-// contiguous bytes per 64-wide k-block (k = 32*half .. +32) and feeds them to
-// four v_mfma_f32_32x32x16_bf16 steps, so weights never touch LDS.  Non-dual:
-// the block covers 128 output columns.  Dual (SwiGLU): waves 0-1 stream gate
-// rows and waves 2-3 up rows of the same 64 output columns; the up sums are
-// handed over through LDS and the epilogue writes bf16 silu(g) * u.
+// 4 waves per block, one per SIMD, each owning 32 weight rows: non-dual, the
+// block covers 128 output columns; dual (SwiGLU), waves 0-1 take gate rows and
+// waves 2-3 up rows of the same 64 output columns, the up sums are handed over
+// through LDS and the epilogue writes bf16 silu(g) * u.
 //
-// Activations (all rows of the tile) go global -> LDS with global_load_lds
-// (no register round trip) into a ring of LEAD+1 stages of BM x 64.  Every
-// row is 128 B = eight 16-B chunks; chunk c of row r is stored at slot
-// c ^ (r & 7), so both the DMA writes (1 KB per instruction, 8 rows) and the
-// MFMA fragment reads (32 rows, one chunk) are free of bank conflicts.  MFMA
-// step q of a k-block takes chunk 4*half + q on both operands (a consistent
-// permutation of k leaves every dot product unchanged).
+// Both operands go global -> LDS with global_load_lds (no register round
+// trip) into a ring of LEAD+1 stages; a stage holds BM activation rows and the
+// block's 128 weight rows, 64 k each.  Every row is 128 B = eight 16-B chunks;
+// chunk c of row r sits in slot c ^ (r & 7), so the DMA writes (1 KB per
+// instruction, 8 rows of 8 lanes: a whole cache line per 8 lanes) and the MFMA
+// fragment reads (32 rows, one chunk) are both free of bank conflicts.  Each
+// k-block is four v_mfma_f32_32x32x16_bf16 steps; step q takes chunk
+// 4*(lane/32) + q on both operands (a consistent permutation of k leaves every
+// dot product unchanged).
 //
-// Pipeline: at iteration kb the block multiplies k-block kb, then issues the
-// weight loads and activation DMA of k-block kb+LEAD, waits until k-block
-// kb+1 has landed and passes one barrier.  Every iteration issues the same
-// loads (the tail re-reads the last k-block into a slot never consumed), so
-// the wait is an exact count of outstanding loads; ring slots are
-// compile-time (k-block kb lives in slot kb % (LEAD+1)).  Rows past M read
-// row M-1 (their outputs are never stored).
+// Pipeline: at iteration kb the block multiplies k-block kb, issues the DMA of
+// k-block kb+LEAD, waits until k-block kb+1 has landed and passes one barrier.
+// Every iteration issues the same loads (the tail re-reads the last k-block
+// into a slot never consumed), so the wait is an exact count of outstanding
+// loads; ring slots are compile-time (k-block kb lives in slot kb % (LEAD+1)).
+// Rows past M read row M-1 (their outputs are never stored).
+//
+// Why this shape: at a few hundred rows the activation tile is 1.5x the
+// weight bytes of a block per k-block, and both streams compete for the
+// per-CU limit on outstanding L1 requests; whole-line weight requests (8
+// lanes per 128-B line) need a quarter of the L1 accesses of lane-per-row
+// register loads, and one block per column tile with the full row range reads
+// every weight once.
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -290,8 +295,9 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   constexpr int BM = 32 * MT;
   constexpr int BN = DUAL ? 64 : 128;  // output columns per block
   constexpr int STAGES = LEAD + 1;
-  constexpr int STAGE_BYTES = BM * 128;
-  constexpr int PER_IT = 4 + MT;  // loads per wave per k-block: 4 weight, MT activation
+  constexpr int A_BYTES = BM * 128;
+  constexpr int STAGE_BYTES = A_BYTES + 128 * 128;  // activations, then the 128 weight rows
+  constexpr int PER_IT = 4 + MT;  // DMA instructions per wave per k-block: 4 weight, MT activation
   static_assert(!DUAL || 2 * MT * 16 * 64 * 4 <= STAGES * STAGE_BYTES, "dual hand-over fits");
   __shared__ __attribute__((aligned(1024))) uint8_t ring[STAGES * STAGE_BYTES];
 
@@ -303,9 +309,15 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   const int kbeg = tc.s * a.k_per_split;
   const int kend = min(a.K, kbeg + a.k_per_split);
   const int nkb = kend > kbeg ? (kend - kbeg) / KB : 0;
-  const int col = tc.n0 + 32 * (DUAL ? (wave & 1) : wave) + lo;  // this lane's output column
+  const int wrow0 = tc.n0 + 32 * (DUAL ? (wave & 1) : wave);  // first weight row of this wave
+  const int col = wrow0 + lo;                                    // this lane's output column
   const uint16_t* W = reinterpret_cast<const uint16_t*>(DUAL && wave >= 2 ? G.W2 : G.W);
-  const uint16_t* pw = W + (int64_t)col * a.K + kbeg + 32 * hi;
+  // weight DMA: instruction q fills the wave's rows 8q..8q+7; lane l takes row
+  // 8q + l/8 and chunk (l%8) ^ (l/8)
+  const uint16_t* pw[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    pw[q] = W + (int64_t)(wrow0 + 8 * q + (lane >> 3)) * a.K + kbeg + 8 * ((lane & 7) ^ (lane >> 3));
 
   // activation DMA: instruction j of this wave fills tile rows 8g..8g+7,
   // g = wave*MT + j; lane l takes row 8g + l/8 and chunk (l%8) ^ (l/8)
@@ -322,12 +334,15 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   floatx16 acc[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) acc[i] = floatx16{};
-  u32x4 wr[STAGES][4];
 
   auto issue = [&](int kb, auto S) {
     constexpr int st = decltype(S)::value;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) wr[st][q] = *reinterpret_cast<const u32x4*>(pw + kb * KB + 8 * q);
+    for (int q = 0; q < 4; ++q)
+      __builtin_amdgcn_global_load_lds(
+          reinterpret_cast<const void*>(pw[q] + kb * KB),
+          (__attribute__((address_space(3))) void*)(ring + st * STAGE_BYTES + A_BYTES + (wave * 4 + q) * 1024),
+          16, 0, 0);
 #pragma unroll
     for (int j = 0; j < MT; ++j)
       __builtin_amdgcn_global_load_lds(
@@ -338,6 +353,11 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   auto compute = [&](auto S) {
     constexpr int st = decltype(S)::value;
     const uint8_t* tile = ring + st * STAGE_BYTES;
+    const uint8_t* wt = tile + A_BYTES + (32 * wave + lo) * 128;
+    bf16x8 wf[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      wf[q] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wt + 16 * ((4 * hi + q) ^ (lo & 7))));
     bf16x8 af[2][MT];
     auto frags = [&](int q, bf16x8 (&dst)[MT]) {
 #pragma unroll
@@ -352,8 +372,7 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < MT; ++i)
-        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][i], __builtin_bit_cast(bf16x8, wr[st][q]),
-                                                         acc[i], 0, 0, 0);
+        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][i], wf[q], acc[i], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     });
   };
