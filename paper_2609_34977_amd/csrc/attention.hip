@@ -13,7 +13,8 @@
 // in fp32 (exp2 with the 1/sqrt(dh)*log2(e) scale folded in) plus one
 // cross-half exchange; O^T += V^T P^T with P taken straight from the S^T
 // registers (the key order inside an MFMA k-block is any permutation as long
-// as both operands use it) and V^T fragments read from the transposed V
+// as both operands use it), split into bf16 hi + lo parts so the product sees
+// P to ~16 bits, and V^T fragments read from the transposed V
 // written by the QKV finalize (8 bytes = 4 keys per load, no LDS staging).
 // Masking: key row j is visible to query row q iff start(q) <= j <= q.
 //
@@ -110,8 +111,7 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
       alpha = exp2f(m_run - m_new);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        // P enters the MFMA in bf16; normalise with the same rounded weights
-        p[r] = bf16_bits_to_f32(f32_to_bf16_bits(exp2f(s[r] - m_new)));
+        p[r] = exp2f(s[r] - m_new);
         sum += p[r];
       }
     }
@@ -122,16 +122,23 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
     for (int c = 0; c < DH / 32; ++c)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[c][r] *= alpha;
-    // ---- O^T += V^T P^T, two k-blocks of 16 keys
-    bf16x8 pf[2];
+    // ---- O^T += V^T P^T, two k-blocks of 16 keys.  The fp32 weights enter the
+    // bf16 MFMA as hi + lo parts (hi = bf16(p), lo = bf16(p - hi)), so P keeps
+    // ~16 significant bits and the softmax stays fp32 up to that split.
+    bf16x8 pf[2][2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      uint32_t w[4];
+      uint32_t wh[4], wl[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        w[e] = (uint32_t)f32_to_bf16_bits(p[8 * u + 2 * e]) |
-               ((uint32_t)f32_to_bf16_bits(p[8 * u + 2 * e + 1]) << 16);
-      pf[u] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+      for (int e = 0; e < 4; ++e) {
+        const float a0 = p[8 * u + 2 * e], a1 = p[8 * u + 2 * e + 1];
+        const uint16_t h0 = f32_to_bf16_bits(a0), h1 = f32_to_bf16_bits(a1);
+        wh[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        wl[e] = (uint32_t)f32_to_bf16_bits(a0 - bf16_bits_to_f32(h0)) |
+                ((uint32_t)f32_to_bf16_bits(a1 - bf16_bits_to_f32(h1)) << 16);
+      }
+      pf[u][0] = __builtin_bit_cast(bf16x8, u32x4{wh[0], wh[1], wh[2], wh[3]});
+      pf[u][1] = __builtin_bit_cast(bf16x8, u32x4{wl[0], wl[1], wl[2], wl[3]});
     }
 #pragma unroll
     for (int c = 0; c < DH / 32; ++c)
@@ -139,7 +146,8 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
       for (int u = 0; u < 2; ++u) {
         const bf16x8 v8 = __builtin_bit_cast(
             bf16x8, u32x4{vf[c][u][0].x, vf[c][u][0].y, vf[c][u][1].x, vf[c][u][1].y});
-        o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v8, pf[u], o[c], 0, 0, 0);
+        o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v8, pf[u][0], o[c], 0, 0, 0);
+        o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v8, pf[u][1], o[c], 0, 0, 0);
       }
   }
 
