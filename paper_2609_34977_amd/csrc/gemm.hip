@@ -35,15 +35,6 @@ __device__ inline int xcd_remap(int b, int total) {
   return xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
 }
 
-// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).
-template <int B, int E, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-  if constexpr (B < E) {
-    f(std::integral_constant<int, B>{});
-    static_for<B + 1, E>(f);
-  }
-}
-
 template <typename T>
 __device__ __forceinline__ T sel3(int gi, T x0, T x1, T x2) {
   return gi == 0 ? x0 : (gi == 1 ? x1 : x2);

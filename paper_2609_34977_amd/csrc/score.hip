@@ -103,9 +103,11 @@ __global__ void __launch_bounds__(256) score_prep_kernel(
   for (int l = 0; l < n_layers; ++l) {
     const FT* row = feat_row<FT>(fa, l, g, i);
     float ss = 0.f;
-    for (int c = lane; c < d; c += 64) {
-      const float v = Feat<FT>::load1(row + c);
-      ss = fmaf(v, v, ss);
+    for (int c = lane * 8; c < d; c += 512) {  // d is a multiple of 8
+      float x[8];
+      Feat<FT>::load8(row + c, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
     }
     ss = wave_sum(ss);
     if (lane == 0) nu[((int64_t)g * n_layers + l) * n + i] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
@@ -353,6 +355,51 @@ __device__ inline void block_cluster_sums(const FeatArgs& fa, int l, int g, int 
   }
 }
 
+// Fixed-order combine of the 4 waves' per-cluster sums acc[k] (k < K) into
+// out[k*d + c], 512 dimensions at a time through LDS (red: 4 * 512 floats).
+template <int KM, int VPL>
+__device__ __forceinline__ void block_combine_cluster_sums(const float (&acc)[KM][VPL], int K, int d, float* red,
+                                                           float* out) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int k = 0; k < KM; ++k) {
+    if (k >= K) break;
+#pragma unroll
+    for (int q = 0; q < VPL / 8; ++q) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) red[wave * 512 + lane * 8 + e] = acc[k][8 * q + e];
+      __syncthreads();
+      for (int c = threadIdx.x; c < 512; c += blockDim.x) {
+        const int dim = q * 512 + c;
+        if (dim < d) out[k * d + dim] = ((red[c] + red[512 + c]) + red[1024 + c]) + red[1536 + c];
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Adds row x (scaled by sc) to the accumulator of its cluster.  fmaf(x, 1, a)
+// rounds like a + x, and each cluster receives its rows in increasing row
+// order, the order block_cluster_sums uses: both paths give the same bits.
+// (Written as per-element selects: a branch per cluster gets merged by the
+// compiler into one dynamically indexed update, which lives in scratch.)
+template <int KM, int VPL>
+__device__ __forceinline__ void add_to_cluster(float (&acc)[KM][VPL], int k_row, const float* x, float sc) {
+#pragma unroll
+  for (int k = 0; k < KM; ++k) {
+    const bool mine = k_row == k;
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      const float t = fmaf(x[v], sc, acc[k][v]);
+      acc[k][v] = mine ? t : acc[k][v];
+    }
+  }
+}
+
+// Cluster counts up to this size keep one accumulator per cluster in
+// registers and read every row once per pass.
+constexpr int kFusedClusters = 4;
+
 constexpr int kMaxRowsPerBlock = 128;
 
 struct ClusterWs {
@@ -400,6 +447,12 @@ __global__ void __launch_bounds__(256) kmeans_assign_kernel(int n, int d, int n_
   if (threadIdx.x == 0) chg = first;
   __syncthreads();
   int32_t* asg = cw.assign + (int64_t)g * n;
+  const bool fused = K <= kFusedClusters;
+  float acc[kFusedClusters][VPL];
+#pragma unroll
+  for (int k = 0; k < kFusedClusters; ++k)
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) acc[k][v] = 0.f;
   for (int j = j0 + wave; j < j1; j += 4) {
     float x[VPL];
     load_slice<FT, VPL>(feat_row<FT>(fa, last, g, U[j]), d, lane, x);
@@ -419,6 +472,7 @@ __global__ void __launch_bounds__(256) kmeans_assign_kernel(int n, int d, int n_
         best = k;
       }
     }
+    if (fused) add_to_cluster<kFusedClusters, VPL>(acc, best, x, 1.0f);
     if (lane == 0) {
       if (!first && asg[j] != best) chg = 1;
       asg[j] = best;
@@ -428,7 +482,10 @@ __global__ void __launch_bounds__(256) kmeans_assign_kernel(int n, int d, int n_
   }
   __syncthreads();
   const int64_t slot = (int64_t)g * cw.NB + b;
-  block_cluster_sums<FT, VPL>(fa, last, g, d, K, U, j0, j1, lab, nullptr, red, cw.psum + slot * K * d);
+  if (fused)
+    block_combine_cluster_sums<kFusedClusters, VPL>(acc, K, d, red, cw.psum + slot * K * d);
+  else
+    block_cluster_sums<FT, VPL>(fa, last, g, d, K, U, j0, j1, lab, nullptr, red, cw.psum + slot * K * d);
   if (threadIdx.x < K) {
     int c = 0;
     for (int j = j0; j < j1; ++j) c += lab[j - j0] == (int)threadIdx.x;
@@ -478,9 +535,28 @@ __global__ void __launch_bounds__(256) cluster_sum_kernel(int n, int d, int n_an
   for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) lab[j - j0] = asg[j];
   __syncthreads();
   const int64_t slot = (int64_t)g * cw.NB + b;
-  for (int l = 0; l < n_layers; ++l)
-    block_cluster_sums<FT, VPL>(fa, l, g, d, K, U, j0, j1, lab, nu + ((int64_t)g * n_layers + l) * n,
-                                red, cw.psum + (slot * n_layers + l) * K * d);
+  for (int l = 0; l < n_layers; ++l) {
+    const float* nul = nu + ((int64_t)g * n_layers + l) * n;
+    float* out = cw.psum + (slot * n_layers + l) * K * d;
+    if (K <= kFusedClusters) {
+      // one read of every row: each goes to its cluster's accumulator
+      const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+      float acc[kFusedClusters][VPL];
+#pragma unroll
+      for (int k = 0; k < kFusedClusters; ++k)
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) acc[k][v] = 0.f;
+      for (int j = j0 + wave; j < j1; j += 4) {
+        const int i = U[j];
+        float x[VPL];
+        load_slice<FT, VPL>(feat_row<FT>(fa, l, g, i), d, lane, x);
+        add_to_cluster<kFusedClusters, VPL>(acc, lab[j - j0], x, nul[i]);
+      }
+      block_combine_cluster_sums<kFusedClusters, VPL>(acc, K, d, red, out);
+    } else {
+      block_cluster_sums<FT, VPL>(fa, l, g, d, K, U, j0, j1, lab, nul, red, out);
+    }
+  }
   if (threadIdx.x < K) {
     int c = 0;
     float sm = 0.f;
