@@ -89,18 +89,20 @@ __global__ void __launch_bounds__(256) norm_kernel(float* __restrict__ h, int d,
   if (ps >= 0) {
     const float4* pr = reinterpret_cast<const float4*>(P + (int64_t)ps * d);
     const int64_t ps4 = pstride >> 2;
-    // four splits' loads in flight at a time, summed in split order
-    for (int s0 = 0; s0 < psplit; s0 += 4) {
-      float4 add[4][MAXV];
+    // SB splits' loads in flight at a time (all of them up to 8 splits when
+    // rows are at most 4096 wide), summed in split order
+    constexpr int SB = MAXV <= 4 ? 8 : 4;
+    for (int s0 = 0; s0 < psplit; s0 += SB) {
+      float4 add[SB][MAXV];
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < SB; ++q)
 #pragma unroll
         for (int k = 0; k < MAXV; ++k) {
           const int c = threadIdx.x + k * 256;
           add[q][k] = (c < d4 && s0 + q < psplit) ? pr[(s0 + q) * ps4 + c] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < SB; ++q)
 #pragma unroll
         for (int k = 0; k < MAXV; ++k) {
           v[k].x += add[q][k].x;
@@ -213,6 +215,61 @@ __global__ void __launch_bounds__(256) qkv_finalize_kernel(
   const int half = dh / 2;
   const float* src = P + (int64_t)prow * d;
   AT* dst = out + (int64_t)prow * d;
+  if (half % 4 == 0 && split <= 2 && d <= 8192) {
+    // each thread: up to 4 groups of 4 consecutive rotate-half pairs (float4
+    // loads), every load issued before any use
+    constexpr int NG = 4;
+    const int ngroups = d / 8;  // pairs / 4
+    float4 x0[NG][2], x1[NG][2];
+    float4 cs[NG][2];
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+      const int gi = threadIdx.x + 256 * q;
+      if (gi < ngroups) {
+        const int pair = 4 * gi, head = pair / half, i = pair - head * half;
+        const int c0 = head * dh + i, c1 = c0 + half;
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          x0[q][s2] = s2 < split ? *reinterpret_cast<const float4*>(src + s2 * pstride + c0) : make_float4(0.f, 0.f, 0.f, 0.f);
+          x1[q][s2] = s2 < split ? *reinterpret_cast<const float4*>(src + s2 * pstride + c1) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        if (p >= 0) {
+          const float4* rp = reinterpret_cast<const float4*>(rope + (int64_t)p * half + i);
+          cs[q][0] = rp[0];
+          cs[q][1] = rp[1];
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+      const int gi = threadIdx.x + 256 * q;
+      if (gi >= ngroups) continue;
+      const int pair = 4 * gi, head = pair / half, i = pair - head * half;
+      const int c0 = head * dh + i, c1 = c0 + half;
+      // split-order sums (split 0 first), as the scalar loop below
+      float a[4] = {x0[q][0].x + x0[q][1].x, x0[q][0].y + x0[q][1].y, x0[q][0].z + x0[q][1].z,
+                    x0[q][0].w + x0[q][1].w};
+      float b[4] = {x1[q][0].x + x1[q][1].x, x1[q][0].y + x1[q][1].y, x1[q][0].z + x1[q][1].z,
+                    x1[q][0].w + x1[q][1].w};
+      if (p >= 0) {
+        const float cx[4] = {cs[q][0].x, cs[q][0].z, cs[q][1].x, cs[q][1].z};
+        const float sy[4] = {cs[q][0].y, cs[q][0].w, cs[q][1].y, cs[q][1].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float y0 = a[e] * cx[e] - b[e] * sy[e];
+          const float y1 = b[e] * cx[e] + a[e] * sy[e];
+          a[e] = y0;
+          b[e] = y1;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        Act<AT>::store(dst + c0 + e, a[e]);
+        Act<AT>::store(dst + c1 + e, b[e]);
+      }
+    }
+    return;
+  }
   for (int t = threadIdx.x; t < d / 2; t += 256) {
     const int head = t / half, i = t - head * half;
     const int c0 = head * dh + i, c1 = c0 + half;
