@@ -49,7 +49,28 @@ def parse():
                    help="run one plain device copy of this size after warm-up (counter calibration)")
     p.add_argument("--score-sweep", action="store_true",
                    help="instead of the step: time scoring over 20/64/256/512 tiles (one JSON line each)")
+    p.add_argument("--online", action="store_true",
+                   help="decoder mask from the online skip controller on the device (logit lens over a "
+                        "32000-token unembedding, w1=3, w2=1, T_skip=20) instead of the workload's mask")
+    p.add_argument("--vocab", type=int, default=32000)
     return p.parse_args()
+
+
+def online_policy(w, dev, V):
+    """Online controller policy: the paper's operating point (w1/w2 = 3, T_skip = 20) with the
+    workload's replaced-layer list (or a drawn one), and an unembedding of V rows."""
+    from synth.online_inputs import unembed
+    from synth.skip_inputs import REPLACED_LAYERS, policy_lists, slc_tables, synthetic_policy
+    from paper_2609_34977_amd import _lib
+    from paper_2609_34977_amd.pipeline import SkipPolicy
+
+    L = w.dec.L
+    name = w.skip.get("policy", w.name)
+    lists = policy_lists(name, L, w.seed) if name in REPLACED_LAYERS else synthetic_policy(L, 7, w.seed)
+    sa, sf = slc_tables(lists, L)
+    sel, tgt = _lib.slc_policy(sa, sf)
+    return SkipPolicy(kind="online", slc_sel=sel, target=tgt, w1=3.0, w2=1.0, T_skip=20.0,
+                      w_unembed=unembed(w.dec, V, w.seed, dev))
 
 
 def build_inputs(w, dev):
@@ -76,11 +97,21 @@ def build_inputs(w, dev):
     return attn, feats, src, text, W, pol
 
 
-def algorithmic(w, cu, codes):
-    """Per kernel class: (bytes, flops) summed over one step, from the per-layer row counts."""
+def algorithmic(w, cu, codes, admit=None, V=0):
+    """Per kernel class: (bytes, flops) summed over one step, from the per-layer row counts.
+    With the online controller (admit given) the logit-lens GEMM of every window layer reads
+    the unembedding [V, d] and the candidate rows once and writes fp32 logits."""
     d, f, L, dh = w.dec.d, w.dec.d_ff, w.dec.L, w.dec.dh
     rows = int(cu[-1])
-    out = {k: [0.0, 0.0] for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "attention")}
+    out = {k: [0.0, 0.0] for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down", "attention",
+                                   "gemm_lens")}
+    if admit is not None:
+        vis = np.concatenate([np.arange(cu[b], cu[b + 1] - w.n_text) for b in range(len(cu) - 1)])
+        for l in range(L // 2):
+            nc = int(np.sum((admit[vis] < 0) | (admit[vis] >= l)))
+            if nc:
+                out["gemm_lens"][0] += V * d * 2 + nc * d * 2 + nc * V * 4
+                out["gemm_lens"][1] += 2.0 * V * d * nc
     pos = np.concatenate([np.arange(cu[b + 1] - cu[b]) for b in range(len(cu) - 1)])
     for l in range(L):
         A = codes[l] & 1 == 0
@@ -210,6 +241,8 @@ def main():
         return
     t_setup = time.perf_counter()
     attn, feats, src, text, W, pol = build_inputs(w, dev)
+    if args.online:
+        pol = online_policy(w, dev, args.vocab)
     sc, dec = w.score, w.dec
     cfg = _lib.decoder_cfg(dec.L, dec.d, dec.H, dec.d_ff,
                            _lib.BF16 if dec.dtype == "bf16" else _lib.F32, dec.eps, dec.theta)
@@ -260,7 +293,8 @@ def main():
     cu, codes = out["cu"], out["codes"]
     rows = int(cu[-1])
     B = w.B
-    alg = algorithmic(w, cu, codes)
+    admit = out.get("admit")
+    alg = algorithmic(w, cu, codes, admit, args.vocab)
     kernel_ms = {k: v[1] / n_full for k, v in full.items() if v[0]}
     launches = {k: v[0] // n_full for k, v in full.items() if v[0]}
     per_step_ms = prof[dom][1] / args.steps
@@ -293,21 +327,27 @@ def main():
         "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": dec.dtype, "data": "synthetic",
-        "config": {"workload": f"{w.name}_keep{sc.keep}", "batch": B, "tiles": sc.G,
+        "config": {"workload": f"{w.name}_keep{sc.keep}" + ("_online" if args.online else ""),
+                   "batch": B, "tiles": sc.G,
                    "visual_tokens_per_tile": sc.n, "keep_per_tile": sc.keep,
                    "text_tokens": w.n_text, "decoder_rows": rows, "decoder_layers": dec.L,
                    "d_model": dec.d, "heads": dec.H, "d_ff": dec.d_ff,
-                   "skip": w.skip.get("kind"), "skip_p": w.skip.get("p"),
+                   "skip": "online" if args.online else w.skip.get("kind"),
+                   "skip_p": None if args.online else w.skip.get("p"),
                    "skipped_sublayer_slots": float((codes[:, :rows] != 0).mean()),
                    "parallelism": "single GPU"},
         "ms_per_sample": ms / B,
         "effective_tokens_per_s": B * (sc.n * w.tiles_per_sample + w.n_text) / (ms * 1e-3),
         "prefill_tflop_per_step": prefill_flops / 1e12,
+        "online": None if admit is None else {
+            "vocab": args.vocab, "w1": pol.w1, "w2": pol.w2, "T_skip": pol.T_skip,
+            "admitted_visual_rows": int(np.sum(admit >= 0)),
+            "visual_rows": int(sum(cu[b + 1] - cu[b] - w.n_text for b in range(B)))},
         "roofline": roof,
         "kernel_ms_per_step": {k: round(v, 4) for k, v in kernel_ms.items()},
         "launches_per_step": launches,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.online:
         print("# cpu baseline", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, min(args.cpu_layers, dec.L), W)
     print(json.dumps(res), flush=True)

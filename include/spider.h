@@ -21,8 +21,8 @@
  *     floating-point atomics).
  *   - Calls on distinct workspaces are independent; the library keeps no
  *     per-call state except the thread-local error message, the optional
- *     profiler and a per-thread pinned staging buffer used by
- *     spider_prefill to upload its row tables.
+ *     profiler and the per-thread pinned staging buffers used by the
+ *     prefill calls to upload row tables and read back admission flags.
  */
 #ifndef SPIDER_H
 #define SPIDER_H
@@ -233,6 +233,49 @@ spider_status spider_prefill(const spider_decoder_cfg* cfg, const spider_layer_w
                              int B, const int32_t* cu_seqlens, const void* x,
                              const uint8_t* codes, float* h_out,
                              void* workspace, size_t workspace_bytes, spider_stream stream);
+
+/* ------------------------------------------------------------------------
+ * spider_prefill_online - spider_prefill driven by the online skip
+ * controller of ASL-Skip (Sec. 4.2.1, Eq. 4; Eq. 6 and Algorithm 1) instead
+ * of a precomputed mask.  Sample b's last n_text rows are text, the rows
+ * before them visual.  At every layer l < floor(L/2) (the decision window)
+ * and for every visual row i not yet in skip mode, on the hidden state h
+ * entering layer l:
+ *   E_ii  = H(softmax(W_unembed h_i')) / ln V, the logit lens with no final
+ *           norm; h_i' = bf16(h_i) in the bf16 path (the GEMM operand), h_i
+ *           in fp32; H = natural-log Shannon entropy;
+ *   F_itc = (1 + cos(h_i, q_b)) / 2, q_b = mean of sample b's text rows of h
+ *           (cosine with a zero vector is 0);
+ *   S_sa  = max(0, 1 - (E_ii + F_itc))                               (Eq. 4)
+ *   acc_i += w1 * S_sa + w2 * slc_sel[l]  (double; acc starts at 0)
+ *   acc_i >= T_skip: row i enters skip mode at layer l and bypasses
+ *           sub-layer target[l] (0 attention, 1 FFN) in layers l .. L-1.
+ * Layer l then runs (same semantics and precision as spider_prefill) with
+ * the updated mask.  Text rows never skip.
+ * Inputs as spider_prefill, plus: n_text >= 1 (every sample has at least
+ *   n_text rows); w_unembed device [V, d] in cfg->dtype (16-byte aligned;
+ *   bf16 needs V % 64 == 0); slc_sel HOST [L] doubles and target HOST [L]
+ *   bytes as written by spider_slc_policy (entries l < floor(L/2) are read).
+ * Outputs: codes_out HOST uint8 [L, rows], the mask the controller built
+ *   (same encoding as spider_prefill's codes); admit_out HOST int32 [rows] or
+ *   NULL: admission layer, -1 if never; s_sa_out device fp32
+ *   [floor(L/2), rows] or NULL: S_sa of each row at each window layer where it
+ *   was scored, 0 elsewhere; h_out as spider_prefill.
+ * Synchronisation: the admission flags are read back to the host once per
+ *   window layer (the call waits for the stream there), so the call returns
+ *   after the window has executed; the layers after it run asynchronously.
+ * Workspace: spider_prefill_online_workspace_size(cfg, B, rows, V) bytes.
+ * ------------------------------------------------------------------------ */
+size_t spider_prefill_online_workspace_size(const spider_decoder_cfg* cfg, int B, int rows, int V);
+
+spider_status spider_prefill_online(const spider_decoder_cfg* cfg,
+                                    const spider_layer_weights* layers, int B,
+                                    const int32_t* cu_seqlens, const void* x, int n_text,
+                                    const void* w_unembed, int V, const double* slc_sel,
+                                    const uint8_t* target, double w1, double w2, double T_skip,
+                                    uint8_t* codes_out, int32_t* admit_out, float* s_sa_out,
+                                    float* h_out, void* workspace, size_t workspace_bytes,
+                                    spider_stream stream);
 
 /* ------------------------------------------------------------------------
  * Kernel-class profiler (process-global, not thread-safe; for benchmarks).

@@ -54,6 +54,10 @@ _SIGS = {
     "spider_prefill_workspace_size": ([ctypes.POINTER(DecoderCfg), _I, _I], _SZ),
     "spider_prefill": ([ctypes.POINTER(DecoderCfg), ctypes.POINTER(LayerWeights), _I, _VP, _VP,
                         _VP, _VP, _VP, _SZ, _VP], _I),
+    "spider_prefill_online_workspace_size": ([ctypes.POINTER(DecoderCfg), _I, _I, _I], _SZ),
+    "spider_prefill_online": ([ctypes.POINTER(DecoderCfg), ctypes.POINTER(LayerWeights), _I, _VP, _VP,
+                               _I, _VP, _I, _VP, _VP, _D, _D, _D, _VP, _VP, _VP, _VP, _VP, _SZ, _VP],
+                              _I),
     "spider_profile_enable": ([_I], _I),
     "spider_profile_mask": ([ctypes.c_uint32], _I),
     "spider_profile_classes": ([], _I),
@@ -237,6 +241,43 @@ def prefill(cfg: DecoderCfg, weights, cu_seqlens, x: torch.Tensor, codes,
                                 c.ctypes.data if c.size else None, _ptr(out), _aligned(workspace),
                                 wsz, _stream(dev)))
     return out
+
+
+def prefill_online_workspace_size(cfg: DecoderCfg, B: int, rows: int, V: int) -> int:
+    return lib().spider_prefill_online_workspace_size(ctypes.byref(cfg), B, rows, V)
+
+
+def prefill_online(cfg: DecoderCfg, weights, cu_seqlens, x: torch.Tensor, n_text: int,
+                   w_unembed: torch.Tensor, slc_sel, target, w1: float, w2: float, T_skip: float,
+                   s_sa: bool = True, out: Optional[torch.Tensor] = None,
+                   workspace: Optional[torch.Tensor] = None, weight_table=None):
+    """Prefill driven by the online skip controller.
+
+    Returns (h [rows, d] fp32, codes [L, rows] uint8, admit [rows] int32,
+    S_sa [L//2, rows] fp32 or None)."""
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    B = len(cu) - 1
+    rows = int(cu[-1])
+    dev = x.device
+    V = int(w_unembed.shape[0])
+    if out is None:
+        out = torch.empty(rows, cfg.d, dtype=torch.float32, device=dev)
+    W = cfg.L // 2
+    s_out = torch.empty(W, rows, dtype=torch.float32, device=dev) if (s_sa and W > 0) else None
+    sel = np.ascontiguousarray(slc_sel, dtype=np.float64)
+    tgt = np.ascontiguousarray(target, dtype=np.uint8)
+    codes = np.zeros((cfg.L, rows), np.uint8)
+    admit = np.full(rows, -1, np.int32)
+    wsz = prefill_online_workspace_size(cfg, B, rows, V)
+    if workspace is None or workspace.numel() < wsz + 256:
+        workspace = _ws(wsz, dev)
+    wt = weight_table if weight_table is not None else layer_weights(weights)
+    _check(lib().spider_prefill_online(ctypes.byref(cfg), wt, B, cu.ctypes.data, _ptr(x), n_text,
+                                       _ptr(w_unembed), V, sel.ctypes.data, tgt.ctypes.data, w1, w2,
+                                       T_skip, codes.ctypes.data if codes.size else None,
+                                       admit.ctypes.data if admit.size else None, _ptr(s_out),
+                                       _ptr(out), _aligned(workspace), wsz, _stream(dev)))
+    return out, codes, admit, s_out
 
 
 # ----------------------------------------------------------------- profiler

@@ -20,7 +20,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libspider.so")
-SOURCES = ["host.cpp", "score.hip", "select.hip", "gemm.hip", "attention.hip", "prefill.hip"]
+SOURCES = ["host.cpp", "score.hip", "select.hip", "gemm.hip", "attention.hip", "prefill.hip",
+           "controller.hip"]
 ARCH = "gfx950"
 
 

@@ -62,6 +62,9 @@ enum KernelClass {
   KC_GEMM_GATEUP,
   KC_GEMM_DOWN,
   KC_RESIDUAL,
+  KC_LENS_PREP,
+  KC_GEMM_LENS,
+  KC_LENS_ADMIT,
   KC_COUNT
 };
 

@@ -59,4 +59,28 @@ struct AttnArgs {
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t st);
 hipError_t launch_attention_f32(const AttnArgs& a, int max_seq, hipStream_t st);
 
+// Online skip controller (Sec. 4.2.1, Eq. 4, Eq. 6).  Candidates are visual
+// rows not yet in skip mode: cand[c] = packed row, cand_sample[c] = its sample.
+// tmean[b] = mean hidden state of sample b's last n_text rows.
+hipError_t launch_text_mean(const float* h, int d, const int32_t* cu, int B, int n_text, float* tmean,
+                            hipStream_t st);
+// hc[c] = h[cand[c]] in the activation dtype, F[c] = (1 + cos(h[cand[c]], tmean[b])) / 2.
+hipError_t launch_lens_prep(bool bf16, const float* h, int d, const int32_t* cand,
+                            const int32_t* cand_sample, int nc, const float* tmean, void* hc, double* F,
+                            hipStream_t st);
+struct LensAdmitArgs {
+  double log_v;      // ln V
+  double w1;         // weight of S_sa
+  double w2_sel;     // w2 * SLC_sel(l), formed on the host in double
+  double t_skip;     // admission threshold
+  double* acc;       // [rows] accumulated skip score (indexed by packed row)
+  int32_t* flag;     // [nc] 1 = admitted at this layer
+  float* s_out;      // [rows] S_sa of this layer, or null
+};
+// Per candidate c (logits row c of [nc, V]): E_ii, S_sa, acc update, flag.
+hipError_t launch_lens_admit(const float* logits, int V, const int32_t* cand, int nc, const double* F,
+                             const LensAdmitArgs& p, hipStream_t st);
+// Zero `bytes` (a multiple of 4) of device memory with a kernel.
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
+
 }  // namespace spider

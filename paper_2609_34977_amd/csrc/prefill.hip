@@ -298,9 +298,9 @@ struct LayerTables {
 };
 
 // Pinned host buffer for the row tables of one thread's prefill calls.  It is
-// reused across calls once the previous upload has completed (event), and is
-// deliberately not released at thread exit (the HIP runtime may already be
-// shut down then); the OS reclaims it with the process.
+// reused once the previous upload has completed (event), and is deliberately
+// not released at thread exit (the HIP runtime may already be shut down
+// then); the OS reclaims it with the process.
 struct Staging {
   void* host = nullptr;
   size_t cap = 0;
@@ -308,6 +308,91 @@ struct Staging {
   bool pending = false;
 };
 thread_local Staging g_stage;
+
+// Pinned host buffer for the admission flags read back by the online controller.
+struct Readback {
+  void* host = nullptr;
+  size_t cap = 0;
+};
+thread_local Readback g_back;
+
+#define SPIDER_TRY(expr)                 \
+  do {                                   \
+    spider_status s_ = (expr);           \
+    if (s_ != SPIDER_OK) return s_;      \
+  } while (0)
+
+// Copies n ints from host memory to dst (device) on st through the pinned
+// staging buffer; returns once the copy is enqueued.
+spider_status upload_ints(const int32_t* src, size_t n, int32_t* dst, hipStream_t st) {
+  const size_t bytes = n * sizeof(int32_t);
+  if (bytes == 0) return SPIDER_OK;
+  if (g_stage.pending) {
+    SPIDER_HIP(hipEventSynchronize(g_stage.ev));
+    g_stage.pending = false;
+  }
+  if (g_stage.cap < bytes) {
+    if (g_stage.host) SPIDER_HIP(hipHostFree(g_stage.host));
+    g_stage.host = nullptr;
+    g_stage.cap = 0;
+    SPIDER_HIP(hipHostMalloc(&g_stage.host, bytes));
+    g_stage.cap = bytes;
+  }
+  if (!g_stage.ev) SPIDER_HIP(hipEventCreateWithFlags(&g_stage.ev, hipEventDisableTiming));
+  std::memcpy(g_stage.host, src, bytes);
+  SPIDER_HIP(hipMemcpyAsync(dst, g_stage.host, bytes, hipMemcpyHostToDevice, st));
+  SPIDER_HIP(hipEventRecord(g_stage.ev, st));
+  g_stage.pending = true;
+  return SPIDER_OK;
+}
+
+// Row lists of layers appended to `tab`: for each sub-layer the rows whose
+// code lacks its bypass bit, then the row -> slot map (-1 for bypassing rows).
+// Layers with identical sets share one list.  Offsets are relative to the
+// device table base; tab[0] sits at offset `base`.
+struct TableBuilder {
+  std::vector<int32_t>& tab;
+  int base;
+  std::map<std::string, std::pair<int, int>> seen[2];
+
+  LayerTables add(const uint8_t* col, int R) {
+    LayerTables t;
+    for (int which = 0; which < 2; ++which) {
+      const uint8_t bit = which == 0 ? 1 : 2;
+      std::string key(R, '\0');
+      int cnt = 0;
+      for (int r = 0; r < R; ++r) {
+        const bool active = !(col[r] & bit);
+        key[r] = active ? 1 : 0;
+        cnt += active;
+      }
+      auto it = seen[which].find(key);
+      std::pair<int, int> offs;
+      if (it != seen[which].end()) {
+        offs = it->second;
+      } else {
+        const int off_list = base + (int)tab.size();
+        for (int r = 0; r < R; ++r)
+          if (key[r]) tab.push_back(r);
+        const int off_slot = base + (int)tab.size();
+        int s = 0;
+        for (int r = 0; r < R; ++r) tab.push_back(key[r] ? s++ : -1);
+        offs = {off_list, off_slot};
+        seen[which][key] = offs;
+      }
+      if (which == 0) {
+        t.nA = cnt;
+        t.offA = offs.first;
+        t.offSlotA = offs.second;
+      } else {
+        t.nF = cnt;
+        t.offF = offs.first;
+        t.offSlotF = offs.second;
+      }
+    }
+    return t;
+  }
+};
 
 int split_max_for_rows(int R) { return std::max(1, std::min(8, 4096 / std::max(1, R))); }
 
@@ -324,30 +409,88 @@ int vt_rows(int R) { return (R + 31) / 32 * 32; }
 
 size_t table_ints_bound(int L, int R) { return (size_t)R * 2 + (size_t)L * 4 * R + 64; }
 
-PrefillWs prefill_layout(const spider_decoder_cfg& c, int R, char* base) {
-  PrefillWs w{};
+struct Carver {
+  char* base;
   size_t off = 0;
-  auto take = [&](size_t bytes) {
-    size_t o = off;
+  void* take(size_t bytes) {
+    const size_t o = off;
     off = align_up(off + bytes, 256);
     return base ? base + o : nullptr;
-  };
+  }
+};
+
+PrefillWs prefill_layout(const spider_decoder_cfg& c, int R, Carver& cv) {
+  PrefillWs w{};
   const size_t es = c.dtype == SPIDER_BF16 ? 2 : 4;
   const int dh = c.d / c.H;
   const int sm = split_max_for_rows(R);
-  w.tables = reinterpret_cast<int32_t*>(take(table_ints_bound(c.L, R) * 4));
-  w.rope = reinterpret_cast<float2*>(take((size_t)R * (dh / 2) * sizeof(float2)));
-  w.xn = take((size_t)R * c.d * es);
-  w.q = take((size_t)R * c.d * es);
-  w.k = take((size_t)R * c.d * es);
-  w.v = take((size_t)vt_rows(R) * c.d * es);  // bf16: V^T [d][vt_rows(R)]
-  w.o = take((size_t)R * c.d * es);
-  w.act = take((size_t)R * c.d_ff * es);
-  w.Pq = reinterpret_cast<float*>(take((size_t)sm * R * c.d * 4));
-  w.Pk = reinterpret_cast<float*>(take((size_t)sm * R * c.d * 4));
-  w.Pv = reinterpret_cast<float*>(take((size_t)sm * R * c.d * 4));
-  w.Pres = reinterpret_cast<float*>(take((size_t)sm * R * c.d * 4));
-  w.bytes = off;
+  w.tables = reinterpret_cast<int32_t*>(cv.take(table_ints_bound(c.L, R) * 4));
+  w.rope = reinterpret_cast<float2*>(cv.take((size_t)R * (dh / 2) * sizeof(float2)));
+  w.xn = cv.take((size_t)R * c.d * es);
+  w.q = cv.take((size_t)R * c.d * es);
+  w.k = cv.take((size_t)R * c.d * es);
+  w.v = cv.take((size_t)vt_rows(R) * c.d * es);  // bf16: V^T [d][vt_rows(R)]
+  w.o = cv.take((size_t)R * c.d * es);
+  w.act = cv.take((size_t)R * c.d_ff * es);
+  w.Pq = reinterpret_cast<float*>(cv.take((size_t)sm * R * c.d * 4));
+  w.Pk = reinterpret_cast<float*>(cv.take((size_t)sm * R * c.d * 4));
+  w.Pv = reinterpret_cast<float*>(cv.take((size_t)sm * R * c.d * 4));
+  w.Pres = reinterpret_cast<float*>(cv.take((size_t)sm * R * c.d * 4));
+  w.bytes = cv.off;
+  return w;
+}
+
+PrefillWs prefill_layout(const spider_decoder_cfg& c, int R, char* base) {
+  Carver cv{base};
+  return prefill_layout(c, R, cv);
+}
+
+// Integer tables of the online prefill (offsets in ints from the table base):
+// positions, sample starts, cu_seqlens, two regions for the row lists of the
+// current layer (alternating, so the slot map of the previous layer's pending
+// residual stays intact until it is consumed), then the candidate list and
+// the sample of each candidate.
+struct OnlineTabs {
+  int pos, start, cu, reg[2], cand, total;
+};
+
+OnlineTabs online_tabs(int R, int B) {
+  OnlineTabs t;
+  t.pos = 0;
+  t.start = R;
+  t.cu = 2 * R;
+  t.reg[0] = (2 * R + B + 1 + 63) / 64 * 64;
+  t.reg[1] = t.reg[0] + 4 * R;
+  t.cand = t.reg[1] + 4 * R;
+  t.total = t.cand + 2 * R;
+  return t;
+}
+
+struct OnlineWs {
+  PrefillWs p;
+  int32_t* tab;   // OnlineTabs
+  void* hc;       // [R, d] candidate rows in the activation dtype
+  float* tmean;   // [B, d] text mean per sample
+  double* F;      // [R] F_itc per candidate
+  float* logits;  // [R, V] logit lens of the candidates
+  double* acc;    // [R] accumulated skip score per packed row
+  int32_t* flag;  // [R] admission flag per candidate
+  size_t bytes;
+};
+
+OnlineWs online_layout(const spider_decoder_cfg& c, int B, int R, int V, char* base) {
+  Carver cv{base};
+  OnlineWs w{};
+  w.p = prefill_layout(c, R, cv);
+  const size_t es = c.dtype == SPIDER_BF16 ? 2 : 4;
+  w.tab = reinterpret_cast<int32_t*>(cv.take((size_t)online_tabs(R, B).total * 4));
+  w.hc = cv.take((size_t)R * c.d * es);
+  w.tmean = reinterpret_cast<float*>(cv.take((size_t)B * c.d * 4));
+  w.F = reinterpret_cast<double*>(cv.take((size_t)R * 8));
+  w.logits = reinterpret_cast<float*>(cv.take((size_t)R * V * 4));
+  w.acc = reinterpret_cast<double*>(cv.take((size_t)R * 8));
+  w.flag = reinterpret_cast<int32_t*>(cv.take((size_t)R * 4));
+  w.bytes = cv.off;
   return w;
 }
 
@@ -375,124 +518,119 @@ spider_status validate_cfg(const spider_decoder_cfg* cfg) {
   return SPIDER_OK;
 }
 
-template <typename AT>
-spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weights* W, int B,
-                          const int32_t* cu, const void* x, const uint8_t* codes, float* h,
-                          const PrefillWs& ws, hipStream_t st) {
-  const bool bf16 = c.dtype == SPIDER_BF16;
-  const int R = cu[B];
-  const int d = c.d, dh = d / c.H, half = dh / 2;
-  // ---- host tables
-  std::vector<int32_t> tab;
-  tab.reserve(table_ints_bound(c.L, R));
-  const int off_pos = 0, off_start = R;
-  tab.resize(2 * R);
-  int max_s = 1;
-  for (int b = 0; b < B; ++b) {
-    max_s = std::max(max_s, cu[b + 1] - cu[b]);
-    for (int r = cu[b]; r < cu[b + 1]; ++r) {
-      tab[off_pos + r] = r - cu[b];
-      tab[off_start + r] = cu[b];
+// Argument checks shared by both prefill entry points (rows = cu_seqlens[B] > 0).
+spider_status validate_prefill_args(const spider_decoder_cfg* cfg, const spider_layer_weights* layers,
+                                    const void* x, const float* h_out) {
+  SPIDER_REQUIRE(x && h_out, SPIDER_ERR_INVALID_ARG, "spider_prefill: x and h_out must be non-null");
+  for (int l = 0; l < cfg->L; ++l) {
+    const spider_layer_weights& w = layers[l];
+    SPIDER_REQUIRE(w.attn_norm && w.wq && w.wk && w.wv && w.wo && w.ffn_norm && w.wg && w.wu && w.wd,
+                   SPIDER_ERR_INVALID_ARG, "spider_prefill: null weight pointer in layer %d", l);
+  }
+  SPIDER_REQUIRE(((uintptr_t)h_out % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                 "spider_prefill: h_out must be 16-byte aligned");
+  for (int l = 0; l < cfg->L; ++l)
+    SPIDER_REQUIRE(((uintptr_t)layers[l].attn_norm % 16) == 0 &&
+                       ((uintptr_t)layers[l].ffn_norm % 16) == 0,
+                   SPIDER_ERR_UNSUPPORTED, "spider_prefill: norm weights must be 16-byte aligned");
+  if (cfg->dtype == SPIDER_BF16) {
+    SPIDER_REQUIRE(((uintptr_t)x % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                   "spider_prefill: x must be 16-byte aligned");
+    for (int l = 0; l < cfg->L; ++l) {
+      const spider_layer_weights& w = layers[l];
+      const void* m[7] = {w.wq, w.wk, w.wv, w.wo, w.wg, w.wu, w.wd};
+      for (int i = 0; i < 7; ++i)
+        SPIDER_REQUIRE(((uintptr_t)m[i] % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                       "spider_prefill: weight matrices must be 16-byte aligned (layer %d)", l);
     }
   }
-  std::vector<LayerTables> lt(c.L);
-  std::map<std::string, std::pair<int, int>> seen[2];  // column -> (list offset, slot offset)
-  for (int l = 0; l < c.L; ++l) {
-    const uint8_t* col = codes + (size_t)l * R;
-    for (int which = 0; which < 2; ++which) {
-      const uint8_t bit = which == 0 ? 1 : 2;
-      std::string key(R, '\0');
-      int cnt = 0;
-      for (int r = 0; r < R; ++r) {
-        const bool active = !(col[r] & bit);
-        key[r] = active ? 1 : 0;
-        cnt += active;
-      }
-      auto it = seen[which].find(key);
-      std::pair<int, int> offs;
-      if (it != seen[which].end()) {
-        offs = it->second;
-      } else {
-        const int off_list = (int)tab.size();
-        for (int r = 0; r < R; ++r)
-          if (key[r]) tab.push_back(r);
-        const int off_slot = (int)tab.size();
-        int s = 0;
-        for (int r = 0; r < R; ++r) tab.push_back(key[r] ? s++ : -1);
-        offs = {off_list, off_slot};
-        seen[which][key] = offs;
-      }
-      if (which == 0) {
-        lt[l].nA = cnt;
-        lt[l].offA = offs.first;
-        lt[l].offSlotA = offs.second;
-      } else {
-        lt[l].nF = cnt;
-        lt[l].offF = offs.first;
-        lt[l].offSlotF = offs.second;
-      }
-    }
-  }
-  // ---- upload through the pinned staging buffer
-  const size_t tbytes = tab.size() * sizeof(int32_t);
-  if (g_stage.pending) {
-    SPIDER_HIP(hipEventSynchronize(g_stage.ev));
-    g_stage.pending = false;
-  }
-  if (g_stage.cap < tbytes) {
-    if (g_stage.host) SPIDER_HIP(hipHostFree(g_stage.host));
-    g_stage.host = nullptr;
-    g_stage.cap = 0;
-    SPIDER_HIP(hipHostMalloc(&g_stage.host, tbytes));
-    g_stage.cap = tbytes;
-  }
-  if (!g_stage.ev) SPIDER_HIP(hipEventCreateWithFlags(&g_stage.ev, hipEventDisableTiming));
-  std::memcpy(g_stage.host, tab.data(), tbytes);
-  SPIDER_HIP(hipMemcpyAsync(ws.tables, g_stage.host, tbytes, hipMemcpyHostToDevice, st));
-  SPIDER_HIP(hipEventRecord(g_stage.ev, st));
-  g_stage.pending = true;
+  return SPIDER_OK;
+}
 
-  const int32_t* dpos = ws.tables + off_pos;
-  const int32_t* dstart = ws.tables + off_start;
-  // ---- rope table and residual init
-  {
-    const int64_t n = (int64_t)max_s * half;
-    rope_table_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(ws.rope, max_s, half, dh,
-                                                                  std::log2((double)c.theta));
-    SPIDER_LAUNCHED("rope_table");
-  }
-  {
-    ProfScope ps(KC_EMBED, st);
-    const int64_t n = (int64_t)R * d;
-    embed_kernel<AT><<<(unsigned)((n + 255) / 256), 256, 0, st>>>(reinterpret_cast<const AT*>(x), h, n);
-    SPIDER_LAUNCHED("embed");
-  }
-  const int split_max = split_max_for_rows(R);
-  const int64_t pstride = (int64_t)R * d;
-  // pending residual partials
+spider_status validate_cu(int B, const int32_t* cu_seqlens, const spider_layer_weights* layers) {
+  SPIDER_REQUIRE(B >= 1, SPIDER_ERR_INVALID_ARG, "spider_prefill: B must be >= 1");
+  SPIDER_REQUIRE(cu_seqlens && layers, SPIDER_ERR_INVALID_ARG,
+                 "spider_prefill: cu_seqlens and layers must be non-null");
+  SPIDER_REQUIRE(cu_seqlens[0] == 0, SPIDER_ERR_SHAPE, "spider_prefill: cu_seqlens[0] must be 0");
+  for (int b = 0; b < B; ++b)
+    SPIDER_REQUIRE(cu_seqlens[b + 1] >= cu_seqlens[b], SPIDER_ERR_SHAPE,
+                   "spider_prefill: cu_seqlens must be non-decreasing");
+  return SPIDER_OK;
+}
+
+// The layer forward of one prefill call.  Row tables live in device memory
+// at `tab` (LayerTables offsets are relative to it); the residual partials of
+// the last O or down GEMM stay pending until the next norm (or flush) adds
+// them to h.
+template <typename AT>
+struct PrefillRun {
+  const spider_decoder_cfg& c;
+  const spider_layer_weights* W;
+  float* h;
+  const PrefillWs& ws;
+  const int32_t* tab;
+  const int32_t* dpos;    // [R] position of each row within its sample
+  const int32_t* dstart;  // [R] first row of the sample that owns each row
+  int R, max_s;
+  hipStream_t st;
   int pend_split = 0;
   const int32_t* pend_slot = nullptr;
-  AT* xn = reinterpret_cast<AT*>(ws.xn);
-  AT* qb = reinterpret_cast<AT*>(ws.q);
-  AT* kb = reinterpret_cast<AT*>(ws.k);
-  AT* vb = reinterpret_cast<AT*>(ws.v);
-  AT* ob = reinterpret_cast<AT*>(ws.o);
-  AT* act = reinterpret_cast<AT*>(ws.act);
-  // split-K caps: the QKV partials are re-read by the finalize kernel and the
-  // O/down partials by the next norm, so splitting is kept modest
-  auto gemm = [&](GemmArgs& ga, int cap) {
-    const int sm = std::min(split_max, cap);
-    return bf16 ? launch_gemm_bf16(ga, sm, st) : launch_gemm_f32(ga, sm, st);
-  };
 
-  for (int l = 0; l < c.L; ++l) {
+  bool bf16() const { return c.dtype == SPIDER_BF16; }
+  int64_t pstride() const { return (int64_t)R * c.d; }
+
+  hipError_t gemm(GemmArgs& ga, int cap) {
+    const int sm = std::min(split_max_for_rows(R), cap);
+    return bf16() ? launch_gemm_bf16(ga, sm, st) : launch_gemm_f32(ga, sm, st);
+  }
+
+  // RoPE table and h = x
+  spider_status begin(const void* x) {
+    const int half = c.d / c.H / 2, dh = c.d / c.H;
+    {
+      const int64_t n = (int64_t)max_s * half;
+      rope_table_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(ws.rope, max_s, half, dh,
+                                                                    std::log2((double)c.theta));
+      SPIDER_LAUNCHED("rope_table");
+    }
+    {
+      ProfScope ps(KC_EMBED, st);
+      const int64_t n = (int64_t)R * c.d;
+      embed_kernel<AT><<<(unsigned)((n + 255) / 256), 256, 0, st>>>(reinterpret_cast<const AT*>(x), h, n);
+      SPIDER_LAUNCHED("embed");
+    }
+    return SPIDER_OK;
+  }
+
+  // adds the pending residual partials to h
+  spider_status flush() {
+    if (pend_split == 0) return SPIDER_OK;
+    ProfScope ps(KC_RESIDUAL, st);
+    launch_norm<AT>(R, h, c.d, ws.Pres, pend_split, pstride(), pend_slot, nullptr, 0.f, nullptr, 0,
+                    static_cast<AT*>(nullptr), st);
+    SPIDER_LAUNCHED("residual_add");
+    pend_split = 0;
+    pend_slot = nullptr;
+    return SPIDER_OK;
+  }
+
+  spider_status layer(int l, const LayerTables& T) {
     const spider_layer_weights& w = W[l];
-    const LayerTables& T = lt[l];
+    const int d = c.d, dh = d / c.H;
+    const int64_t ps_ = pstride();
+    AT* xn = reinterpret_cast<AT*>(ws.xn);
+    AT* qb = reinterpret_cast<AT*>(ws.q);
+    AT* kb = reinterpret_cast<AT*>(ws.k);
+    AT* vb = reinterpret_cast<AT*>(ws.v);
+    AT* ob = reinterpret_cast<AT*>(ws.o);
+    AT* act = reinterpret_cast<AT*>(ws.act);
+    // split-K caps: the QKV partials are re-read by the finalize kernel and the
+    // O/down partials by the next norm, so splitting is kept modest
     if (T.nA > 0) {
       {
         ProfScope ps(KC_RMSNORM, st);
-        launch_norm<AT>(R, h, d, ws.Pres, pend_split, pstride, pend_slot, w.attn_norm, c.eps,
-                        nullptr, 1, xn, st);
+        launch_norm<AT>(R, h, d, ws.Pres, pend_split, ps_, pend_slot, w.attn_norm, c.eps, nullptr, 1,
+                        xn, st);
         SPIDER_LAUNCHED("rmsnorm(attn)");
         pend_split = 0;
         pend_slot = nullptr;
@@ -502,9 +640,9 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
       ga.K = d;
       ga.lda = d;
       ga.epilogue = EPI_PARTIAL_F32;
-      ga.g[0] = GemmGroup{xn, ws.tables + T.offA, T.nA, w.wq, nullptr, d, ws.Pq, d, pstride, 0, 0, 0};
-      ga.g[1] = GemmGroup{xn, nullptr, R, w.wk, nullptr, d, ws.Pk, d, pstride, 0, 0, 0};
-      ga.g[2] = GemmGroup{xn, nullptr, R, w.wv, nullptr, d, ws.Pv, d, pstride, 0, 0, 0};
+      ga.g[0] = GemmGroup{xn, tab + T.offA, T.nA, w.wq, nullptr, d, ws.Pq, d, ps_, 0, 0, 0};
+      ga.g[1] = GemmGroup{xn, nullptr, R, w.wk, nullptr, d, ws.Pk, d, ps_, 0, 0, 0};
+      ga.g[2] = GemmGroup{xn, nullptr, R, w.wv, nullptr, d, ws.Pv, d, ps_, 0, 0, 0};
       {
         ProfScope ps(KC_GEMM_QKV, st);
         hipError_t e = gemm(ga, 2);
@@ -512,18 +650,18 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
       }
       {
         ProfScope ps(KC_QKV_FINALIZE, st);
-        const int64_t ldvt = bf16 ? vt_rows(R) : 0;
-        const int vblocks = bf16 ? (vt_rows(R) / 32) * (d / 64) : R;
+        const int64_t ldvt = bf16() ? vt_rows(R) : 0;
+        const int vblocks = bf16() ? (vt_rows(R) / 32) * (d / 64) : R;
         qkv_finalize_kernel<AT><<<T.nA + R + vblocks, 256, 0, st>>>(
-            ws.Pq, ws.Pk, ws.Pv, ga.split, pstride, T.nA, R, d, dh, ws.tables + T.offA, dpos, ws.rope, qb,
-            kb, vb, ldvt);
+            ws.Pq, ws.Pk, ws.Pv, ga.split, ps_, T.nA, R, d, dh, tab + T.offA, dpos, ws.rope, qb, kb, vb,
+            ldvt);
         SPIDER_LAUNCHED("qkv_finalize");
       }
       {
         ProfScope ps(KC_ATTENTION, st);
-        AttnArgs aa{qb, ws.tables + T.offA, kb, vb, bf16 ? (int64_t)vt_rows(R) : 0, dstart, ob, T.nA, R,
+        AttnArgs aa{qb, tab + T.offA, kb, vb, bf16() ? (int64_t)vt_rows(R) : 0, dstart, ob, T.nA, R,
                     c.H, dh, d, (float)(1.0 / std::sqrt((double)dh))};
-        hipError_t e = bf16 ? launch_attention_bf16(aa, st) : launch_attention_f32(aa, max_s, st);
+        hipError_t e = bf16() ? launch_attention_bf16(aa, st) : launch_attention_f32(aa, max_s, st);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "attention: %s", hipGetErrorString(e));
       }
       GemmArgs go{};
@@ -531,20 +669,20 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
       go.K = d;
       go.lda = d;
       go.epilogue = EPI_PARTIAL_F32;
-      go.g[0] = GemmGroup{ob, nullptr, T.nA, w.wo, nullptr, d, ws.Pres, d, pstride, 0, 0, 0};
+      go.g[0] = GemmGroup{ob, nullptr, T.nA, w.wo, nullptr, d, ws.Pres, d, ps_, 0, 0, 0};
       {
         ProfScope ps(KC_GEMM_O, st);
         hipError_t e = gemm(go, 8);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_o: %s", hipGetErrorString(e));
       }
       pend_split = go.split;
-      pend_slot = ws.tables + T.offSlotA;
+      pend_slot = tab + T.offSlotA;
     }
     if (T.nF > 0) {
       {
         ProfScope ps(KC_RMSNORM, st);
-        launch_norm<AT>(R, h, d, ws.Pres, pend_split, pstride, pend_slot, w.ffn_norm, c.eps,
-                        ws.tables + T.offSlotF, 0, xn, st);
+        launch_norm<AT>(R, h, d, ws.Pres, pend_split, ps_, pend_slot, w.ffn_norm, c.eps,
+                        tab + T.offSlotF, 0, xn, st);
         SPIDER_LAUNCHED("rmsnorm(ffn)");
         pend_split = 0;
         pend_slot = nullptr;
@@ -565,22 +703,161 @@ spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weight
       gd.K = c.d_ff;
       gd.lda = c.d_ff;
       gd.epilogue = EPI_PARTIAL_F32;
-      gd.g[0] = GemmGroup{act, nullptr, T.nF, w.wd, nullptr, d, ws.Pres, d, pstride, 0, 0, 0};
+      gd.g[0] = GemmGroup{act, nullptr, T.nF, w.wd, nullptr, d, ws.Pres, d, ps_, 0, 0, 0};
       {
         ProfScope ps(KC_GEMM_DOWN, st);
         hipError_t e = gemm(gd, 8);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_down: %s", hipGetErrorString(e));
       }
       pend_split = gd.split;
-      pend_slot = ws.tables + T.offSlotF;
+      pend_slot = tab + T.offSlotF;
+    }
+    return SPIDER_OK;
+  }
+};
+
+// positions within the sample and sample starts of every row; returns the
+// longest sample
+int fill_positions(int B, const int32_t* cu, int32_t* pos, int32_t* start) {
+  int max_s = 1;
+  for (int b = 0; b < B; ++b) {
+    max_s = std::max(max_s, cu[b + 1] - cu[b]);
+    for (int r = cu[b]; r < cu[b + 1]; ++r) {
+      pos[r] = r - cu[b];
+      start[r] = cu[b];
     }
   }
-  if (pend_split > 0) {
-    ProfScope ps(KC_RESIDUAL, st);
-    launch_norm<AT>(R, h, d, ws.Pres, pend_split, pstride, pend_slot, nullptr, 0.f, nullptr, 0,
-                    static_cast<AT*>(nullptr), st);
-    SPIDER_LAUNCHED("residual_add");
+  return max_s;
+}
+
+template <typename AT>
+spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weights* W, int B,
+                          const int32_t* cu, const void* x, const uint8_t* codes, float* h,
+                          const PrefillWs& ws, hipStream_t st) {
+  const int R = cu[B];
+  // tables: positions [R], sample starts [R], then the row lists of every layer
+  std::vector<int32_t> tab;
+  tab.reserve(table_ints_bound(c.L, R));
+  tab.resize(2 * R);
+  const int max_s = fill_positions(B, cu, tab.data(), tab.data() + R);
+  std::vector<LayerTables> lt(c.L);
+  TableBuilder tb{tab, 0};
+  for (int l = 0; l < c.L; ++l) lt[l] = tb.add(codes + (size_t)l * R, R);
+  SPIDER_TRY(upload_ints(tab.data(), tab.size(), ws.tables, st));
+
+  PrefillRun<AT> run{c, W, h, ws, ws.tables, ws.tables, ws.tables + R, R, max_s, st};
+  SPIDER_TRY(run.begin(x));
+  for (int l = 0; l < c.L; ++l) SPIDER_TRY(run.layer(l, lt[l]));
+  return run.flush();
+}
+
+struct OnlineParams {
+  int n_text;
+  const void* wu;
+  int V;
+  const double* slc_sel;
+  const uint8_t* target;
+  double w1, w2, t_skip;
+};
+
+// Prefill with the online controller: at every layer l < floor(L/2) the
+// visual rows not yet in skip mode are scored on the hidden state entering
+// layer l, admitted rows get their frozen target bypassed from layer l on,
+// and layer l runs with the updated row lists.  The admission flags come back
+// to the host once per decision-window layer (the stream is synchronised
+// there); the row lists of layer l are built after it.
+template <typename AT>
+spider_status run_prefill_online(const spider_decoder_cfg& c, const spider_layer_weights* W, int B,
+                                 const int32_t* cu, const void* x, const OnlineParams& op,
+                                 uint8_t* codes, int32_t* admit_out, float* s_sa_out, float* h,
+                                 const OnlineWs& ows, hipStream_t st) {
+  const bool bf16 = c.dtype == SPIDER_BF16;
+  const int R = cu[B], L = c.L, Wn = c.L / 2, d = c.d;
+  const OnlineTabs ot = online_tabs(R, B);
+  std::memset(codes, 0, (size_t)L * R);
+  std::vector<int32_t> admit(R, -1);
+
+  std::vector<int32_t> fixed(ot.reg[0], 0);
+  const int max_s = fill_positions(B, cu, fixed.data() + ot.pos, fixed.data() + ot.start);
+  std::copy(cu, cu + B + 1, fixed.begin() + ot.cu);
+  SPIDER_TRY(upload_ints(fixed.data(), fixed.size(), ows.tab, st));
+
+  PrefillRun<AT> run{c, W, h, ows.p, ows.tab, ows.tab + ot.pos, ows.tab + ot.start, R, max_s, st};
+  SPIDER_TRY(run.begin(x));
+  SPIDER_HIP(launch_fill_zero(ows.acc, (size_t)R * sizeof(double), st));
+  if (s_sa_out && Wn > 0) SPIDER_HIP(launch_fill_zero(s_sa_out, (size_t)Wn * R * sizeof(float), st));
+
+  std::vector<int32_t> cand, lists;
+  LayerTables T;
+  for (int l = 0; l < L; ++l) {
+    if (l < Wn) {
+      cand.clear();
+      for (int b = 0; b < B; ++b)
+        for (int r = cu[b]; r < cu[b + 1] - op.n_text; ++r)
+          if (admit[r] < 0) cand.push_back(r);
+      const int nc = (int)cand.size();
+      if (nc > 0) {
+        for (int b = 0; b < B; ++b)
+          for (int r = cu[b]; r < cu[b + 1] - op.n_text; ++r)
+            if (admit[r] < 0) cand.push_back(b);
+        SPIDER_TRY(run.flush());
+        int32_t* dcand = ows.tab + ot.cand;
+        SPIDER_TRY(upload_ints(cand.data(), cand.size(), dcand, st));
+        {
+          ProfScope ps(KC_LENS_PREP, st);
+          hipError_t e = launch_text_mean(h, d, ows.tab + ot.cu, B, op.n_text, ows.tmean, st);
+          if (e == hipSuccess) e = launch_lens_prep(bf16, h, d, dcand, dcand + nc, nc, ows.tmean, ows.hc, ows.F, st);
+          SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lens_prep: %s", hipGetErrorString(e));
+        }
+        {
+          ProfScope ps(KC_GEMM_LENS, st);
+          GemmArgs gl{};
+          gl.ngroups = 1;
+          gl.K = d;
+          gl.lda = d;
+          gl.epilogue = EPI_PARTIAL_F32;
+          gl.g[0] = GemmGroup{ows.hc, nullptr, nc, op.wu, nullptr, op.V, ows.logits, op.V,
+                              (int64_t)nc * op.V, 0, 0, 0};
+          hipError_t e = bf16 ? launch_gemm_bf16(gl, 1, st) : launch_gemm_f32(gl, 1, st);
+          SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_lens: %s", hipGetErrorString(e));
+        }
+        {
+          ProfScope ps(KC_LENS_ADMIT, st);
+          LensAdmitArgs p{std::log((double)op.V), op.w1, op.w2 * op.slc_sel[l], op.t_skip, ows.acc, ows.flag,
+                          s_sa_out ? s_sa_out + (size_t)l * R : nullptr};
+          hipError_t e = launch_lens_admit(ows.logits, op.V, dcand, nc, ows.F, p, st);
+          SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lens_admit: %s", hipGetErrorString(e));
+        }
+        const size_t fbytes = (size_t)nc * sizeof(int32_t);
+        if (g_back.cap < fbytes) {
+          if (g_back.host) SPIDER_HIP(hipHostFree(g_back.host));
+          g_back.host = nullptr;
+          g_back.cap = 0;
+          SPIDER_HIP(hipHostMalloc(&g_back.host, fbytes));
+          g_back.cap = fbytes;
+        }
+        SPIDER_HIP(hipMemcpyAsync(g_back.host, ows.flag, fbytes, hipMemcpyDeviceToHost, st));
+        SPIDER_HIP(hipStreamSynchronize(st));
+        const int32_t* flag = reinterpret_cast<const int32_t*>(g_back.host);
+        const uint8_t bit = op.target[l] == 1 ? 2 : 1;
+        for (int i = 0; i < nc; ++i) {
+          if (!flag[i]) continue;
+          const int r = cand[i];
+          admit[r] = l;
+          for (int l2 = l; l2 < L; ++l2) codes[(size_t)l2 * R + r] |= bit;
+        }
+      }
+    }
+    if (l <= Wn) {  // row lists change only inside the window
+      lists.clear();
+      TableBuilder tb{lists, ot.reg[l & 1]};
+      T = tb.add(codes + (size_t)l * R, R);
+      SPIDER_TRY(upload_ints(lists.data(), lists.size(), ows.tab + ot.reg[l & 1], st));
+    }
+    SPIDER_TRY(run.layer(l, T));
   }
+  SPIDER_TRY(run.flush());
+  if (admit_out) std::copy(admit.begin(), admit.end(), admit_out);
   return SPIDER_OK;
 }
 
@@ -601,24 +878,12 @@ extern "C" spider_status spider_prefill(const spider_decoder_cfg* cfg,
                                         const uint8_t* codes, float* h_out, void* workspace,
                                         size_t workspace_bytes, spider_stream stream) {
   clear_error();
-  spider_status v = validate_cfg(cfg);
-  if (v != SPIDER_OK) return v;
-  SPIDER_REQUIRE(B >= 1, SPIDER_ERR_INVALID_ARG, "spider_prefill: B must be >= 1");
-  SPIDER_REQUIRE(cu_seqlens && layers, SPIDER_ERR_INVALID_ARG,
-                 "spider_prefill: cu_seqlens and layers must be non-null");
-  SPIDER_REQUIRE(cu_seqlens[0] == 0, SPIDER_ERR_SHAPE, "spider_prefill: cu_seqlens[0] must be 0");
-  for (int b = 0; b < B; ++b)
-    SPIDER_REQUIRE(cu_seqlens[b + 1] >= cu_seqlens[b], SPIDER_ERR_SHAPE,
-                   "spider_prefill: cu_seqlens must be non-decreasing");
+  SPIDER_TRY(validate_cfg(cfg));
+  SPIDER_TRY(validate_cu(B, cu_seqlens, layers));
   const int R = cu_seqlens[B];
   if (R == 0) return SPIDER_OK;
-  SPIDER_REQUIRE(x && h_out && codes, SPIDER_ERR_INVALID_ARG,
-                 "spider_prefill: x, h_out and codes must be non-null");
-  for (int l = 0; l < cfg->L; ++l) {
-    const spider_layer_weights& w = layers[l];
-    SPIDER_REQUIRE(w.attn_norm && w.wq && w.wk && w.wv && w.wo && w.ffn_norm && w.wg && w.wu && w.wd,
-                   SPIDER_ERR_INVALID_ARG, "spider_prefill: null weight pointer in layer %d", l);
-  }
+  SPIDER_REQUIRE(codes, SPIDER_ERR_INVALID_ARG, "spider_prefill: codes must be non-null");
+  SPIDER_TRY(validate_prefill_args(cfg, layers, x, h_out));
   for (size_t i = 0; i < (size_t)cfg->L * R; ++i)
     SPIDER_REQUIRE(codes[i] <= 3, SPIDER_ERR_INVALID_ARG,
                    "spider_prefill: code %u at %zu is not in [0, 3]", (unsigned)codes[i], i);
@@ -628,26 +893,67 @@ extern "C" spider_status spider_prefill(const spider_decoder_cfg* cfg,
                  workspace_bytes);
   SPIDER_REQUIRE(((uintptr_t)workspace % 256) == 0, SPIDER_ERR_WORKSPACE,
                  "spider_prefill: workspace must be 256-byte aligned");
-  SPIDER_REQUIRE(((uintptr_t)h_out % 16) == 0, SPIDER_ERR_UNSUPPORTED,
-                 "spider_prefill: h_out must be 16-byte aligned");
-  for (int l = 0; l < cfg->L; ++l)
-    SPIDER_REQUIRE(((uintptr_t)layers[l].attn_norm % 16) == 0 &&
-                       ((uintptr_t)layers[l].ffn_norm % 16) == 0,
-                   SPIDER_ERR_UNSUPPORTED, "spider_prefill: norm weights must be 16-byte aligned");
-  if (cfg->dtype == SPIDER_BF16) {
-    SPIDER_REQUIRE(((uintptr_t)x % 16) == 0, SPIDER_ERR_UNSUPPORTED,
-                   "spider_prefill: x must be 16-byte aligned");
-    for (int l = 0; l < cfg->L; ++l) {
-      const spider_layer_weights& w = layers[l];
-      const void* m[7] = {w.wq, w.wk, w.wv, w.wo, w.wg, w.wu, w.wd};
-      for (int i = 0; i < 7; ++i)
-        SPIDER_REQUIRE(((uintptr_t)m[i] % 16) == 0, SPIDER_ERR_UNSUPPORTED,
-                       "spider_prefill: weight matrices must be 16-byte aligned (layer %d)", l);
-    }
-  }
   const PrefillWs ws = prefill_layout(*cfg, R, reinterpret_cast<char*>(workspace));
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (cfg->dtype == SPIDER_BF16)
     return run_prefill<uint16_t>(*cfg, layers, B, cu_seqlens, x, codes, h_out, ws, st);
   return run_prefill<float>(*cfg, layers, B, cu_seqlens, x, codes, h_out, ws, st);
+}
+
+extern "C" size_t spider_prefill_online_workspace_size(const spider_decoder_cfg* cfg, int B, int rows,
+                                                       int V) {
+  if (!cfg || cfg->L < 1 || cfg->d < 1 || cfg->H < 1 || cfg->d % cfg->H || B < 1 || rows < 0 || V < 1)
+    return 0;
+  return online_layout(*cfg, B, std::max(rows, 1), V, nullptr).bytes;
+}
+
+extern "C" spider_status spider_prefill_online(
+    const spider_decoder_cfg* cfg, const spider_layer_weights* layers, int B, const int32_t* cu_seqlens,
+    const void* x, int n_text, const void* w_unembed, int V, const double* slc_sel, const uint8_t* target,
+    double w1, double w2, double T_skip, uint8_t* codes_out, int32_t* admit_out, float* s_sa_out,
+    float* h_out, void* workspace, size_t workspace_bytes, spider_stream stream) {
+  clear_error();
+  SPIDER_TRY(validate_cfg(cfg));
+  SPIDER_TRY(validate_cu(B, cu_seqlens, layers));
+  SPIDER_REQUIRE(n_text >= 1, SPIDER_ERR_INVALID_ARG, "spider_prefill_online: n_text must be >= 1");
+  for (int b = 0; b < B; ++b)
+    SPIDER_REQUIRE(cu_seqlens[b + 1] - cu_seqlens[b] >= n_text, SPIDER_ERR_SHAPE,
+                   "spider_prefill_online: sample %d has fewer than n_text rows", b);
+  SPIDER_REQUIRE(V >= 2 && w_unembed, SPIDER_ERR_INVALID_ARG,
+                 "spider_prefill_online: w_unembed must be non-null with V >= 2");
+  SPIDER_REQUIRE(((uintptr_t)w_unembed % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                 "spider_prefill_online: w_unembed must be 16-byte aligned");
+  SPIDER_REQUIRE(cfg->dtype != SPIDER_BF16 || V % 64 == 0, SPIDER_ERR_UNSUPPORTED,
+                 "spider_prefill_online: bf16 path needs V a multiple of 64");
+  SPIDER_REQUIRE(std::isfinite(w1) && std::isfinite(w2) && std::isfinite(T_skip), SPIDER_ERR_INVALID_ARG,
+                 "spider_prefill_online: w1, w2 and T_skip must be finite");
+  const int Wn = cfg->L / 2;
+  if (Wn > 0) {
+    SPIDER_REQUIRE(slc_sel && target, SPIDER_ERR_INVALID_ARG,
+                   "spider_prefill_online: slc_sel and target must be non-null");
+    for (int l = 0; l < Wn; ++l) {
+      SPIDER_REQUIRE(std::isfinite(slc_sel[l]), SPIDER_ERR_INVALID_ARG,
+                     "spider_prefill_online: slc_sel[%d] is not finite", l);
+      SPIDER_REQUIRE(target[l] <= 1, SPIDER_ERR_INVALID_ARG,
+                     "spider_prefill_online: target[%d] must be 0 or 1", l);
+    }
+  }
+  const int R = cu_seqlens[B];
+  if (R == 0) return SPIDER_OK;
+  SPIDER_REQUIRE(codes_out, SPIDER_ERR_INVALID_ARG, "spider_prefill_online: codes_out must be non-null");
+  SPIDER_TRY(validate_prefill_args(cfg, layers, x, h_out));
+  const OnlineWs need = online_layout(*cfg, B, R, V, nullptr);
+  SPIDER_REQUIRE(workspace && workspace_bytes >= need.bytes, SPIDER_ERR_WORKSPACE,
+                 "spider_prefill_online: workspace of %zu bytes needed, %zu given", need.bytes,
+                 workspace_bytes);
+  SPIDER_REQUIRE(((uintptr_t)workspace % 256) == 0, SPIDER_ERR_WORKSPACE,
+                 "spider_prefill_online: workspace must be 256-byte aligned");
+  const OnlineWs ows = online_layout(*cfg, B, R, V, reinterpret_cast<char*>(workspace));
+  const OnlineParams op{n_text, w_unembed, V, slc_sel, target, w1, w2, T_skip};
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (cfg->dtype == SPIDER_BF16)
+    return run_prefill_online<uint16_t>(*cfg, layers, B, cu_seqlens, x, op, codes_out, admit_out, s_sa_out,
+                                        h_out, ows, st);
+  return run_prefill_online<float>(*cfg, layers, B, cu_seqlens, x, op, codes_out, admit_out, s_sa_out,
+                                   h_out, ows, st);
 }

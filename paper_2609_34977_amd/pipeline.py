@@ -2,7 +2,9 @@
 
 score (GPU) -> select + assembly (GPU) -> [one device-to-host copy of the
 sample boundaries] -> skip plan (host, Algorithm 1 admission or a per-layer
-mask) -> prefill (GPU).  This module only sequences library calls and packs
+mask) -> prefill (GPU); or, with the online policy, the prefill whose
+controller scores and admits the visual rows on the device layer by layer
+(spider_prefill_online).  This module only sequences library calls and packs
 the per-sample skip codes into the [L, rows] layout of the prefill (visual
 rows of a sample first, text rows never skip); buffers are allocated once.
 """
@@ -19,7 +21,7 @@ from . import _lib
 
 @dataclass
 class SkipPolicy:
-    kind: str                                  # "layer_mask" | "adaptive"
+    kind: str                                  # "layer_mask" | "adaptive" | "online"
     layer_mask: Optional[np.ndarray] = None    # [L, 2] bool (attention, FFN)
     s_sa: Optional[np.ndarray] = None          # [B, L//2, n_vis_max] float32
     slc_sel: Optional[np.ndarray] = None       # [L] float64
@@ -27,6 +29,7 @@ class SkipPolicy:
     w1: float = 3.0
     w2: float = 1.0
     T_skip: float = 20.0
+    w_unembed: Optional[torch.Tensor] = None   # [V, d] (online)
 
 
 class Pipeline:
@@ -48,6 +51,8 @@ class Pipeline:
         self.prefill_ws = torch.empty(_lib.prefill_workspace_size(dec, self.B, max_rows) + 256,
                                       dtype=torch.uint8, device=device)
         self.h = torch.empty(max_rows, dec.d, dtype=torch.float32, device=device)
+        self.max_rows = max_rows
+        self.online_ws = None
         self.cu_host = torch.empty(self.B + 1, dtype=torch.int32, pin_memory=True)
 
     def codes(self, cu: np.ndarray, policy: SkipPolicy) -> np.ndarray:
@@ -75,8 +80,18 @@ class Pipeline:
         self.cu_host.copy_(sel["cu_seqlens"], non_blocking=True)
         torch.cuda.current_stream(self.device).synchronize()
         cu = self.cu_host.numpy().copy()
-        codes = self.codes(cu, policy)
         rows = int(cu[-1])
+        if policy.kind == "online":
+            V = int(policy.w_unembed.shape[0])
+            if self.online_ws is None:
+                nb = _lib.prefill_online_workspace_size(self.dec, self.B, self.max_rows, V)
+                self.online_ws = torch.empty(nb + 256, dtype=torch.uint8, device=self.device)
+            h, codes, admit, _ = _lib.prefill_online(
+                self.dec, None, cu, sel["x"][:rows], self.n_text, policy.w_unembed, policy.slc_sel,
+                policy.target, policy.w1, policy.w2, policy.T_skip, s_sa=False, out=self.h[:rows],
+                workspace=self.online_ws, weight_table=self.wtable)
+            return {"score": sc, "select": sel, "cu": cu, "codes": codes, "admit": admit, "h": h}
+        codes = self.codes(cu, policy)
         h = _lib.prefill(self.dec, None, cu, sel["x"][:rows], codes, out=self.h[:rows],
                          workspace=self.prefill_ws, weight_table=self.wtable)
         return {"score": sc, "select": sel, "cu": cu, "codes": codes, "h": h}

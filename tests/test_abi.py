@@ -192,6 +192,40 @@ def test_prefill_validation_before_any_hip_call(L):
     assert lib_mod.prefill_workspace_size(bf, 1, 192) > 0
 
 
+def _online_call(L, cfg, cu, n_text=4, V=32000, wu=0x1000, sel=None, tgt=None, w1=1.0, T=1.0,
+                 ws_bytes=1 << 40):
+    W = (lib_mod.LayerWeights * cfg.L)()
+    for i in range(cfg.L):
+        W[i] = lib_mod.LayerWeights(*([0x1000] * 9))
+    cu = np.ascontiguousarray(cu, np.int32)
+    rows = int(cu[-1])
+    sel = np.zeros(cfg.L, np.float64) if sel is None else np.ascontiguousarray(sel, np.float64)
+    tgt = np.zeros(cfg.L, np.uint8) if tgt is None else np.ascontiguousarray(tgt, np.uint8)
+    codes = np.zeros((cfg.L, max(rows, 1)), np.uint8)
+    return L.spider_prefill_online(ctypes.byref(cfg), W, len(cu) - 1, cu.ctypes.data, 0x1000, n_text,
+                                   wu, V, sel.ctypes.data, tgt.ctypes.data, w1, 0.5, T,
+                                   codes.ctypes.data, None, None, 0x1000, 0x100000, ws_bytes, None)
+
+
+def test_prefill_online_validation_before_any_hip_call(L):
+    bf = lib_mod.decoder_cfg(4, 4096, 32, 11008, lib_mod.BF16)
+    f32 = lib_mod.decoder_cfg(4, 128, 4, 344, lib_mod.F32)
+    assert _online_call(L, bf, [0, 10], n_text=0) == INVALID
+    assert _online_call(L, bf, [0, 10, 13], n_text=4) == SHAPE       # sample 1 shorter than n_text
+    assert _online_call(L, bf, [0, 10], V=32001) == UNSUPPORTED      # bf16 GEMM needs V % 64 == 0
+    assert _online_call(L, bf, [0, 10], V=1) == INVALID
+    assert _online_call(L, bf, [0, 10], wu=None) == INVALID
+    assert _online_call(L, bf, [0, 10], wu=0x1008) == UNSUPPORTED
+    assert _online_call(L, bf, [0, 10], tgt=[0, 2, 0, 0]) == INVALID
+    assert _online_call(L, bf, [0, 10], sel=[0.0, np.nan, 0, 0]) == INVALID
+    assert _online_call(L, bf, [0, 10], T=np.inf) == INVALID
+    assert _online_call(L, bf, [0, 10], ws_bytes=100) == WORKSPACE
+    assert _online_call(L, bf, [0, 10, 10], n_text=4) == SHAPE       # empty sample
+    # any V for fp32; entries past the window are not read
+    assert _online_call(L, f32, [0, 10], V=1001, tgt=[0, 1, 7, 7], ws_bytes=100) == WORKSPACE
+    assert lib_mod.prefill_online_workspace_size(bf, 1, 192, 32000) > lib_mod.prefill_workspace_size(bf, 1, 192)
+
+
 def test_profiler_host_side(L):
     lib_mod.profile_enable(True)
     d = lib_mod.profile_read()

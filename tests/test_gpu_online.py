@@ -1,0 +1,169 @@
+"""GPU prefill with the online skip controller (spider_prefill_online) against
+the oracle's online prefill (Sec. 4.2.1, Eq. 4, Eq. 6, Algorithm 1).
+
+The admission test acc >= T_skip turns floating point into a decision, so each
+case picks T_skip such that every evaluation of the oracle's trajectory stays
+at least `margin` away from it (the GPU and the oracle then take the same
+decisions unless their S_sa differ by more than the margin, which the S_sa
+bar below rules out).  Candidates for T_skip are the midpoints of the widest
+gaps between the scores the rows would reach by the end of the window with
+no admissions; each candidate is checked by a full oracle run.
+
+Bars:
+* admission layers and the whole mask: identical;
+* S_sa: layer 0 reads the input rows themselves, so only the accumulation
+  order of the lens GEMM differs (|dS| <= 1e-4); later layers read hidden
+  states that already carry the prefill's own error (the bf16 bar of 2e-2
+  relative on h), |dS| <= 1e-2 in bf16 and 1e-4 in fp32;
+* h: max relative error per sample <= 2e-2 (bf16) / 1e-4 (fp32), as for
+  spider_prefill.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import asl_skip as ak
+from oracle.online import prefill_online
+from synth import get_workload
+from synth.decoder_inputs import layer_weights
+from synth.online_inputs import decoder_rows, unembed
+from synth.skip_inputs import slc_tables, synthetic_policy
+from gpu_common import need_gpu, rel_err, log
+
+W1, W2 = 3.0, 1.0   # the paper's ratio w1 / w2 = 3
+
+CASES = {
+    # name: (workload, layers, cu_seqlens, n_text, V)
+    "tiny_fp32_four_window_layers": ("tiny", 8, [0, 80], 32, 1000),
+    "tiny_fp32_three_samples_one_text_only": ("tiny", 4, [0, 81, 113, 150], 32, 999),
+    "7b_192_visual_one_window_layer": ("llava15_7b", 2, [0, 256], 64, 32000),
+    "7b_two_samples_ragged": ("llava15_7b", 2, [0, 131, 324], 64, 32000),
+    "next_320_visual_lds_lens": ("llava_next_7b", 2, [0, 384], 64, 32000),
+    "7b_two_window_layers": ("llava15_7b", 4, [0, 128], 64, 32000),
+}
+
+
+def _policy(n_layers):
+    """Raw contribution tables of a replaced-layer list drawn for this depth."""
+    return slc_tables(synthetic_policy(n_layers, max(1, n_layers // 4), seed=n_layers), n_layers)
+
+
+def _layer_margins(S, admit, sel, T, vis_rows):
+    """Per window layer: min |acc_l - T| over the rows the oracle scored there."""
+    acc = np.zeros(len(vis_rows))
+    out = []
+    for l in range(S.shape[0]):
+        live = np.array([admit[r] < 0 or admit[r] >= l for r in vis_rows])
+        acc = np.where(live, acc + (W1 * S[l, vis_rows] + W2 * sel[l]), acc)
+        out.append(float(np.min(np.abs(acc[live] - T))) if live.any() else np.inf)
+    return out
+
+
+def _thresholds(S_free, sel, vis_rows, n_max=8):
+    """Midpoints of the widest gaps between the scores the rows would reach by
+    the last window layer if nobody were admitted (middle 80 %), widest first;
+    admissions then spread over the window."""
+    W = S_free.shape[0]
+    a = np.sort(sum(W1 * S_free[l, vis_rows] + W2 * sel[l] for l in range(W)))
+    lo, hi = np.quantile(a, 0.1), np.quantile(a, 0.9)
+    gaps = [(a[i + 1] - a[i], 0.5 * (a[i] + a[i + 1])) for i in range(len(a) - 1)
+            if lo <= a[i] and a[i + 1] <= hi]
+    gaps.sort(reverse=True)
+    return [t for _, t in gaps[:n_max]]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", list(CASES))
+def test_online_prefill_parity(case):
+    L = need_gpu()
+    wl, n_layers, cu, n_text, V = CASES[case]
+    dec = get_workload(wl).dec
+    bf16 = dec.dtype == "bf16"
+    recipe = "bf16" if bf16 else "f32"
+    cu = np.array(cu, np.int32)
+    rows = int(cu[-1])
+    Wn = n_layers // 2
+    log(f"[online] case={case} L={n_layers} d={dec.d} rows={rows} V={V}")
+    x = decoder_rows(dec, cu, n_text, seed=1)
+    wu_cpu = unembed(dec, V, seed=2)
+    vis_rows = [r for b in range(len(cu) - 1) for r in range(int(cu[b]), int(cu[b + 1]) - n_text)]
+
+    # oracle: its own policy, weights and thresholds
+    sa, sf = _policy(n_layers)
+    na, nf = ak.slc_normalize(sa, sf)
+    m, sel = ak.skip_targets(na, nf)
+    cfg_o = dataclasses.replace(dec, L=n_layers)
+    wts = lambda l: {k: v.float().numpy() for k, v in layer_weights(dec, l, 0, "cpu").items()}
+    xo = x.float().numpy()
+    wuo = wu_cpu.float().numpy()
+
+    def oracle(T):
+        return prefill_online(xo, wts, cu, n_text, wuo, sel, m, W1, W2, T, cfg_o, recipe=recipe)
+
+    _, _, _, S_free = oracle(np.inf)
+    margin_need = [1e-3] + [2e-2 if bf16 else 1e-3] * (Wn - 1)
+    chosen = None
+    for T in _thresholds(S_free, sel, vis_rows):
+        ref = oracle(T)
+        mg = _layer_margins(ref[3], ref[2], sel, T, vis_rows)
+        log(f"  T_skip={T:.6f}: margins {['%.2e' % v for v in mg]}")
+        if all(v >= need for v, need in zip(mg, margin_need)):
+            chosen = (T, ref)
+            break
+    assert chosen is not None, "no threshold keeps the oracle's decisions clear of it"
+    T, (h_o, codes_o, admit_o, S_o) = chosen
+    hist = np.bincount(admit_o[vis_rows] + 1, minlength=Wn + 1)
+    log(f"  T_skip={T:.6f}: never admitted {hist[0]}, admitted per window layer {hist[1:].tolist()}")
+
+    # GPU: its own policy call, weights and unembedding on the device
+    sel_g, tgt_g = L.slc_policy(sa, sf, 1e-8)
+    W = [layer_weights(dec, l, 0, "cuda") for l in range(n_layers)]
+    cfg = L.decoder_cfg(n_layers, dec.d, dec.H, dec.d_ff, L.BF16 if bf16 else L.F32, dec.eps, dec.theta)
+    wu = wu_cpu.cuda()
+    h, codes, admit, S = L.prefill_online(cfg, W, cu, x.cuda(), n_text, wu, sel_g, tgt_g, W1, W2, T)
+    torch.cuda.synchronize()
+    h = h.cpu().numpy()
+    S = S.cpu().numpy()
+
+    for l in range(Wn):
+        cand = [r for r in vis_rows if admit_o[r] < 0 or admit_o[r] >= l]
+        e = float(np.max(np.abs(S[l, cand] - S_o[l, cand]))) if cand else 0.0
+        log(f"  layer {l}: {len(cand)} scored, max |dS_sa| {e:.2e}")
+        assert e <= (1e-4 if (l == 0 or not bf16) else 1e-2), (l, e)
+        others = np.setdiff1d(np.arange(rows), cand)
+        assert np.all(S[l, others] == 0.0)
+    assert np.array_equal(admit, admit_o.astype(np.int32))
+    assert np.array_equal(codes, codes_o)
+    tol = 2e-2 if bf16 else 1e-4
+    for b in range(len(cu) - 1):
+        if cu[b + 1] == cu[b]:
+            continue
+        e = rel_err(h[cu[b]:cu[b + 1]], h_o[cu[b]:cu[b + 1]])
+        log(f"  sample {b}: max rel err {e:.2e}")
+        assert e <= tol, f"sample {b}: {e}"
+
+
+@pytest.mark.gpu
+def test_online_matches_static_prefill_with_its_mask_and_is_deterministic():
+    """The online call's h equals spider_prefill run with the mask it built, bit for bit."""
+    L = need_gpu()
+    dec = get_workload("llava15_7b").dec
+    n_layers, n_text, V = 4, 64, 32000
+    cu = np.array([0, 96, 224], np.int32)
+    x = decoder_rows(dec, cu, n_text, seed=3).cuda()
+    wu = unembed(dec, V, seed=4, device="cuda")
+    sa, sf = _policy(n_layers)
+    sel, tgt = L.slc_policy(sa, sf, 1e-8)
+    W = [layer_weights(dec, l, 0, "cuda") for l in range(n_layers)]
+    cfg = L.decoder_cfg(n_layers, dec.d, dec.H, dec.d_ff, L.BF16, dec.eps, dec.theta)
+    h1, codes1, admit1, S1 = L.prefill_online(cfg, W, cu, x, n_text, wu, sel, tgt, W1, W2, 3.5)
+    h2, codes2, admit2, S2 = L.prefill_online(cfg, W, cu, x, n_text, wu, sel, tgt, W1, W2, 3.5)
+    hs = L.prefill(cfg, W, cu, x, codes1)
+    torch.cuda.synchronize()
+    log(f"[online] static-mask check: admitted {int((admit1 >= 0).sum())} rows")
+    assert np.array_equal(codes1, codes2) and np.array_equal(admit1, admit2)
+    assert torch.equal(h1, h2) and torch.equal(S1, S2)
+    assert torch.equal(h1, hs)
+    assert np.all(codes1[:, cu[1] - n_text:cu[1]] == 0) and np.all(codes1[:, cu[2] - n_text:] == 0)
