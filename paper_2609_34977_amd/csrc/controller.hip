@@ -6,9 +6,12 @@
 //   lens_prep   per candidate row i of sample b: a copy of h_i in the
 //               activation dtype (the logit-lens GEMM operand) and
 //               F_itc = (1 + cos(h_i, q_b)) / 2 (double)
-//   [GEMM]      logits = copy x W_unembed^T (fp32, the decoder GEMMs)
-//   lens_admit  E_ii = H(softmax(logits)) / ln V with H = ln S - T / S,
-//               S = sum e^(z - max), T = sum e^(z - max) (z - max);
+//   [GEMM]      z = copy x W_unembed^T (the decoder GEMMs, fp32 accumulation):
+//               bf16 with V % 128 == 0 reduces each row's 128-column tiles
+//               to (max, S, T) in the GEMM epilogue, else writes the logits
+//   lens_admit  E_ii = H(softmax(z)) / ln V with H = ln S - T / S,
+//               S = sum e^(z - max), T = sum e^(z - max) (z - max) (tile
+//               statistics merged in double in a fixed order);
 //               S_sa = max(0, 1 - (E_ii + F_itc)); acc_i += w1 S_sa + w2 sel_l;
 //               flag_i = acc_i >= T_skip
 //
@@ -39,17 +42,26 @@ __device__ __forceinline__ void block_sum_d(double (&v)[N], double (*red)[4]) {
   for (int i = 0; i < N; ++i) v[i] = (red[i][0] + red[i][1]) + (red[i][2] + red[i][3]);
 }
 
-// grid (ceil(d / 256), B); text rows of sample b are cu[b+1]-n_text .. cu[b+1]-1
+// grid (ceil(d / 64), B): 64 columns x 4 row slices per block; slice j sums
+// the text rows j, j+4, ... in order (double), then (s0 + s1) + (s2 + s3).
+// Text rows of sample b are cu[b+1]-n_text .. cu[b+1]-1.
 __global__ void __launch_bounds__(256) text_mean_kernel(const float* __restrict__ h, int d,
                                                         const int32_t* __restrict__ cu, int n_text,
                                                         float* __restrict__ tmean) {
+  __shared__ double part[4][64];
   const int b = blockIdx.y;
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= d) return;
+  const int cl = threadIdx.x & 63, j = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + cl;
   const int r1 = cu[b + 1];
   double s = 0.0;
-  for (int r = r1 - n_text; r < r1; ++r) s += (double)h[(int64_t)r * d + c];
-  tmean[(int64_t)b * d + c] = (float)(s / n_text);
+  if (c < d) {
+#pragma unroll 4
+    for (int r = r1 - n_text + j; r < r1; r += 4) s += (double)h[(int64_t)r * d + c];
+  }
+  part[j][cl] = s;
+  __syncthreads();
+  if (j == 0 && c < d)
+    tmean[(int64_t)b * d + c] = (float)(((part[0][cl] + part[1][cl]) + (part[2][cl] + part[3][cl])) / n_text);
 }
 
 // one block per candidate; d % 4 == 0
@@ -90,6 +102,19 @@ __global__ void __launch_bounds__(256) lens_prep_kernel(const float* __restrict_
   }
 }
 
+// Shared tail of the two admission kernels (thread 0 of the candidate's block).
+__device__ __forceinline__ void admit_row(double S, double T, int c, const int32_t* __restrict__ cand,
+                                          const double* __restrict__ F, const LensAdmitArgs& p) {
+  const double H = log(S) - T / S;
+  const double E = H / p.log_v;
+  const double ssa = fmax(0.0, 1.0 - (E + F[c]));
+  const int r = cand[c];
+  const double a = p.acc[r] + (p.w1 * ssa + p.w2_sel);
+  p.acc[r] = a;
+  p.flag[c] = a >= p.t_skip ? 1 : 0;
+  if (p.s_out) p.s_out[r] = (float)ssa;
+}
+
 // one block per candidate: normalised entropy of softmax(logits row), Eq. 4,
 // accumulation and admission test
 __global__ void __launch_bounds__(256) lens_admit_kernel(const float* __restrict__ logits, int V,
@@ -116,16 +141,46 @@ __global__ void __launch_bounds__(256) lens_admit_kernel(const float* __restrict
   }
   double st[2] = {(double)s, (double)t};
   block_sum_d<2>(st, redd);
-  if (threadIdx.x == 0) {
-    const double H = log(st[0]) - st[1] / st[0];
-    const double E = H / p.log_v;
-    const double ssa = fmax(0.0, 1.0 - (E + F[c]));
-    const int r = cand[c];
-    const double a = p.acc[r] + (p.w1 * ssa + p.w2_sel);
-    p.acc[r] = a;
-    p.flag[c] = a >= p.t_skip ? 1 : 0;
-    if (p.s_out) p.s_out[r] = (float)ssa;
+  if (threadIdx.x == 0) admit_row(st[0], st[1], c, cand, F, p);
+}
+
+struct StatD {
+  double m, s, t;
+};
+
+__device__ __forceinline__ StatD stat_merge(StatD a, StatD b) {
+  const double m = fmax(a.m, b.m);
+  const double da = a.m - m, db = b.m - m;
+  const double ea = exp(da), eb = exp(db);
+  return {m, ea * a.s + eb * b.s, ea * (a.t + a.s * da) + eb * (b.t + b.s * db)};
+}
+
+// one wave per candidate: merges the row's per-tile statistics (tile j =
+// lane, lane + 64, ... in order, then a fixed butterfly over the lanes)
+__global__ void __launch_bounds__(64) lens_admit_stats_kernel(const float* __restrict__ stats, int ntiles,
+                                                              const int32_t* __restrict__ cand,
+                                                              const double* __restrict__ F,
+                                                              LensAdmitArgs p) {
+  const int c = blockIdx.x, lane = threadIdx.x;
+  const floatx4* row = reinterpret_cast<const floatx4*>(stats) + (int64_t)c * ntiles;
+  StatD st{0.0, 0.0, 0.0};
+  bool have = false;
+  for (int j = lane; j < ntiles; j += 64) {
+    const floatx4 v = row[j];
+    const StatD x{(double)v[0], (double)v[1], (double)v[2]};
+    st = have ? stat_merge(st, x) : x;
+    have = true;
   }
+  // lanes without a tile (ntiles < 64) take the neutral piece of their partner
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const StatD other{__shfl_xor(st.m, o, 64), __shfl_xor(st.s, o, 64), __shfl_xor(st.t, o, 64)};
+    const bool other_have = __shfl_xor((int)have, o, 64) != 0;
+    if (have && other_have) st = (lane & o) ? stat_merge(other, st) : stat_merge(st, other);
+    else if (other_have) st = other;
+    have = have || other_have;
+  }
+  if (lane == 0) admit_row(st.s, st.t, c, cand, F, p);
 }
 
 __global__ void __launch_bounds__(256) fill_zero_kernel(uint32_t* __restrict__ p, int64_t n) {
@@ -138,7 +193,7 @@ __global__ void __launch_bounds__(256) fill_zero_kernel(uint32_t* __restrict__ p
 hipError_t launch_text_mean(const float* h, int d, const int32_t* cu, int B, int n_text, float* tmean,
                             hipStream_t st) {
   if (B <= 0) return hipSuccess;
-  text_mean_kernel<<<dim3((unsigned)ceil_div(d, 256), (unsigned)B), 256, 0, st>>>(h, d, cu, n_text, tmean);
+  text_mean_kernel<<<dim3((unsigned)ceil_div(d, 64), (unsigned)B), 256, 0, st>>>(h, d, cu, n_text, tmean);
   return hipGetLastError();
 }
 
@@ -160,6 +215,14 @@ hipError_t launch_lens_admit(const float* logits, int V, const int32_t* cand, in
                              const LensAdmitArgs& p, hipStream_t st) {
   if (nc <= 0) return hipSuccess;
   lens_admit_kernel<<<nc, 256, 0, st>>>(logits, V, cand, F, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_lens_admit_stats(const float* stats, int ntiles, const int32_t* cand, int nc,
+                                   const double* F, const LensAdmitArgs& p, hipStream_t st) {
+  if (nc <= 0) return hipSuccess;
+  if (ntiles <= 0) return hipErrorInvalidValue;
+  lens_admit_stats_kernel<<<nc, 64, 0, st>>>(stats, ntiles, cand, F, p);
   return hipGetLastError();
 }
 

@@ -280,7 +280,20 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-template <int MT, int LEAD, bool DUAL>
+// Softmax statistics of one row piece: max, sum e^(z-max), sum e^(z-max) (z-max).
+struct SoftStat {
+  float m, s, t;
+};
+
+// Merge of two pieces (b.m and a.m finite): rescale both to the larger max.
+__device__ __forceinline__ SoftStat soft_merge(SoftStat a, SoftStat b) {
+  const float m = fmaxf(a.m, b.m);
+  const float da = a.m - m, db = b.m - m;
+  const float ea = expf(da), eb = expf(db);
+  return {m, ea * a.s + eb * b.s, ea * fmaf(a.s, da, a.t) + eb * fmaf(b.s, db, b.t)};
+}
+
+template <int MT, int LEAD, bool DUAL, bool LENS = false>
 __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   constexpr int KB = 64;
   constexpr int BM = 32 * MT;
@@ -421,6 +434,55 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
           }
         }
     }
+  } else if constexpr (LENS) {
+    // the block's BM x 128 logits go through LDS (row pitch 132 floats); each
+    // row is reduced by 256/BM threads (64 rows: 4, 128: 2, 192/256: 1) over
+    // consecutive column ranges, merged across those threads in fixed order
+    constexpr int PITCH = 132;
+    constexpr int TPR = BM <= 64 ? 4 : (BM <= 128 ? 2 : 1);
+    constexpr int CPT = 128 / TPR;
+    static_assert(BM * PITCH * 4 <= STAGES * STAGE_BYTES, "lens tile fits the ring");
+    __syncthreads();
+    float* sm = reinterpret_cast<float*>(ring);
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        sm[(32 * i + 8 * (r >> 2) + 4 * hi + (r & 3)) * PITCH + 32 * wave + lo] = acc[i][r];
+    __syncthreads();
+    const int row = tid / TPR, part = tid % TPR;
+    SoftStat st{-INFINITY, 0.f, 0.f};
+    if (row < BM) {
+      const float* z = sm + row * PITCH + part * CPT;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int c = 0; c < CPT; c += 4) {
+        const floatx4 v = *reinterpret_cast<const floatx4*>(z + c);
+        mx = fmaxf(mx, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+      }
+      float se = 0.f, te = 0.f;
+#pragma unroll
+      for (int c = 0; c < CPT; c += 4) {
+        const floatx4 v = *reinterpret_cast<const floatx4*>(z + c);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float u = v[e] - mx;
+          const float x = expf(u);
+          se += x;
+          te = fmaf(x, u, te);
+        }
+      }
+      st = {mx, se, te};
+    }
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) {
+      const SoftStat other{__shfl_xor(st.m, o, 64), __shfl_xor(st.s, o, 64), __shfl_xor(st.t, o, 64)};
+      st = (part & o) ? soft_merge(other, st) : soft_merge(st, other);
+    }
+    const int m = tc.m0 + row;
+    if (row < BM && part == 0 && m < M)
+      *reinterpret_cast<floatx4*>(reinterpret_cast<float*>(G.out) +
+                                  ((int64_t)m * G.ldo + tc.n0 / 128) * 4) = floatx4{st.m, st.s, st.t, 0.f};
   } else {
 #pragma unroll
     for (int i = 0; i < MT; ++i)
@@ -531,10 +593,10 @@ void launch_cfg(const GemmArgs& a, hipStream_t st) {
   gemm_bf16_kernel<BM, BN, WGM, WGN, 4, DUAL><<<a.total_tiles, 256, 0, st>>>(a);
 }
 
-template <int MT, bool DUAL>
+template <int MT, bool DUAL, bool LENS = false>
 void launch_stream(const GemmArgs& a, hipStream_t st) {
   constexpr int LEAD = MT <= 2 ? 3 : 2;
-  gemm_stream_kernel<MT, LEAD, DUAL><<<a.total_tiles, 256, 0, st>>>(a);
+  gemm_stream_kernel<MT, LEAD, DUAL, LENS><<<a.total_tiles, 256, 0, st>>>(a);
 }
 
 }  // namespace
@@ -548,6 +610,23 @@ int gemm_split_for(int M, int N, int K, bool dual, bool bf16, int split_max) {
 hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
   int maxM = 0;
   for (int i = 0; i < a.ngroups; ++i) maxM = std::max(maxM, a.g[i].M);
+  if (a.epilogue == EPI_LENS_STATS) {
+    if (maxM > 256 || a.K % 64) return hipErrorInvalidValue;
+    for (int i = 0; i < a.ngroups; ++i)
+      if (a.g[i].N % 128) return hipErrorInvalidValue;
+    a.split = 1;
+    a.k_per_split = a.K;
+    const int bm = std::max(64, (maxM + 63) / 64 * 64);
+    fill_tiles(a, bm, 128);
+    if (a.total_tiles == 0) return hipSuccess;
+    switch (bm) {
+      case 64: launch_stream<2, false, true>(a, st); break;
+      case 128: launch_stream<4, false, true>(a, st); break;
+      case 192: launch_stream<6, false, true>(a, st); break;
+      default: launch_stream<8, false, true>(a, st); break;
+    }
+    return hipGetLastError();
+  }
   const bool dual = a.epilogue == EPI_SWIGLU;
   TileCfg tc = pick_bf16_tile(maxM, dual);
   for (int i = 0; i < a.ngroups; ++i)

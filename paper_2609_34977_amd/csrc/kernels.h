@@ -22,7 +22,10 @@ struct GemmGroup {
 
 enum GemmEpilogue {
   EPI_PARTIAL_F32 = 0,  // out fp32 [split][M][N]: this split's partial sums
-  EPI_SWIGLU = 1        // out act dtype [M][N] = silu(A W^T) * (A W2^T); split must be 1
+  EPI_SWIGLU = 1,       // out act dtype [M][N] = silu(A W^T) * (A W2^T); split must be 1
+  EPI_LENS_STATS = 2    // out fp32 [M][N/128][4]: per row and 128-column tile of z = A W^T,
+                        // (max z, sum e^(z-max), sum e^(z-max) (z-max), 0); bf16 only,
+                        // M <= 256, N % 128 == 0, K % 64 == 0, no split
 };
 
 struct GemmArgs {
@@ -80,6 +83,9 @@ struct LensAdmitArgs {
 // Per candidate c (logits row c of [nc, V]): E_ii, S_sa, acc update, flag.
 hipError_t launch_lens_admit(const float* logits, int V, const int32_t* cand, int nc, const double* F,
                              const LensAdmitArgs& p, hipStream_t st);
+// The same from EPI_LENS_STATS tiles: stats [nc][ntiles][4].
+hipError_t launch_lens_admit_stats(const float* stats, int ntiles, const int32_t* cand, int nc,
+                                   const double* F, const LensAdmitArgs& p, hipStream_t st);
 // Zero `bytes` (a multiple of 4) of device memory with a kernel.
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 

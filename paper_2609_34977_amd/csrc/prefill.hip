@@ -472,11 +472,17 @@ struct OnlineWs {
   void* hc;       // [R, d] candidate rows in the activation dtype
   float* tmean;   // [B, d] text mean per sample
   double* F;      // [R] F_itc per candidate
-  float* logits;  // [R, V] logit lens of the candidates
+  float* logits;  // [R, V] logit lens of the candidates (unfused path), else null
+  float* stats;   // [R, V/128, 4] per-tile softmax statistics (fused bf16 path), else null
   double* acc;    // [R] accumulated skip score per packed row
   int32_t* flag;  // [R] admission flag per candidate
   size_t bytes;
 };
+
+// bf16 with V a multiple of 128: the lens GEMM's epilogue reduces each row's
+// 128-column tiles to softmax statistics (no logits in memory); otherwise
+// the GEMM writes fp32 logits and a separate kernel reduces them.
+bool lens_fused(const spider_decoder_cfg& c, int V) { return c.dtype == SPIDER_BF16 && V % 128 == 0; }
 
 OnlineWs online_layout(const spider_decoder_cfg& c, int B, int R, int V, char* base) {
   Carver cv{base};
@@ -487,7 +493,10 @@ OnlineWs online_layout(const spider_decoder_cfg& c, int B, int R, int V, char* b
   w.hc = cv.take((size_t)R * c.d * es);
   w.tmean = reinterpret_cast<float*>(cv.take((size_t)B * c.d * 4));
   w.F = reinterpret_cast<double*>(cv.take((size_t)R * 8));
-  w.logits = reinterpret_cast<float*>(cv.take((size_t)R * V * 4));
+  if (lens_fused(c, V))
+    w.stats = reinterpret_cast<float*>(cv.take((size_t)R * (V / 128) * 16));
+  else
+    w.logits = reinterpret_cast<float*>(cv.take((size_t)R * V * 4));
   w.acc = reinterpret_cast<double*>(cv.take((size_t)R * 8));
   w.flag = reinterpret_cast<int32_t*>(cv.take((size_t)R * 4));
   w.bytes = cv.off;
@@ -809,23 +818,42 @@ spider_status run_prefill_online(const spider_decoder_cfg& c, const spider_layer
           if (e == hipSuccess) e = launch_lens_prep(bf16, h, d, dcand, dcand + nc, nc, ows.tmean, ows.hc, ows.F, st);
           SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lens_prep: %s", hipGetErrorString(e));
         }
+        const bool fused = lens_fused(c, op.V);
+        const int ntiles = op.V / 128;
         {
           ProfScope ps(KC_GEMM_LENS, st);
           GemmArgs gl{};
           gl.ngroups = 1;
           gl.K = d;
           gl.lda = d;
-          gl.epilogue = EPI_PARTIAL_F32;
-          gl.g[0] = GemmGroup{ows.hc, nullptr, nc, op.wu, nullptr, op.V, ows.logits, op.V,
-                              (int64_t)nc * op.V, 0, 0, 0};
-          hipError_t e = bf16 ? launch_gemm_bf16(gl, 1, st) : launch_gemm_f32(gl, 1, st);
+          hipError_t e = hipSuccess;
+          if (fused) {
+            // up to 256 candidates per launch (one pass over the unembedding each)
+            const int nchunk = (nc + 255) / 256;
+            const int per = (nc + nchunk - 1) / nchunk;
+            gl.epilogue = EPI_LENS_STATS;
+            for (int c0 = 0; c0 < nc && e == hipSuccess; c0 += per) {
+              const int mc = std::min(per, nc - c0);
+              GemmArgs gc = gl;
+              gc.g[0] = GemmGroup{reinterpret_cast<const uint16_t*>(ows.hc) + (size_t)c0 * d, nullptr, mc,
+                                  op.wu, nullptr, op.V, ows.stats + (size_t)c0 * ntiles * 4, ntiles, 0,
+                                  0, 0, 0};
+              e = launch_gemm_bf16(gc, 1, st);
+            }
+          } else {
+            gl.epilogue = EPI_PARTIAL_F32;
+            gl.g[0] = GemmGroup{ows.hc, nullptr, nc, op.wu, nullptr, op.V, ows.logits, op.V,
+                                (int64_t)nc * op.V, 0, 0, 0};
+            e = bf16 ? launch_gemm_bf16(gl, 1, st) : launch_gemm_f32(gl, 1, st);
+          }
           SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_lens: %s", hipGetErrorString(e));
         }
         {
           ProfScope ps(KC_LENS_ADMIT, st);
           LensAdmitArgs p{std::log((double)op.V), op.w1, op.w2 * op.slc_sel[l], op.t_skip, ows.acc, ows.flag,
                           s_sa_out ? s_sa_out + (size_t)l * R : nullptr};
-          hipError_t e = launch_lens_admit(ows.logits, op.V, dcand, nc, ows.F, p, st);
+          hipError_t e = fused ? launch_lens_admit_stats(ows.stats, ntiles, dcand, nc, ows.F, p, st)
+                               : launch_lens_admit(ows.logits, op.V, dcand, nc, ows.F, p, st);
           SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lens_admit: %s", hipGetErrorString(e));
         }
         const size_t fbytes = (size_t)nc * sizeof(int32_t);

@@ -9,6 +9,11 @@ bar below rules out).  Candidates for T_skip are the midpoints of the widest
 gaps between the scores the rows would reach by the end of the window with
 no admissions; each candidate is checked by a full oracle run.
 
+The bf16 cases with V % 128 == 0 take the fused lens (softmax statistics in
+the GEMM epilogue; 64, 100, 128, 192, 196 candidates cover every row-tile
+shape, 320 candidates two launches); V = 32064 and the fp32 cases take the
+logits path.
+
 Bars:
 * admission layers and the whole mask: identical;
 * S_sa: layer 0 reads the input rows themselves, so only the accumulation
@@ -42,6 +47,8 @@ CASES = {
     "7b_two_samples_ragged": ("llava15_7b", 2, [0, 131, 324], 64, 32000),
     "next_320_visual_lds_lens": ("llava_next_7b", 2, [0, 384], 64, 32000),
     "7b_two_window_layers": ("llava15_7b", 4, [0, 128], 64, 32000),
+    "7b_100_visual": ("llava15_7b", 2, [0, 164], 64, 32000),
+    "7b_unfused_lens_v32064": ("llava15_7b", 2, [0, 192], 64, 32064),
 }
 
 
