@@ -296,6 +296,9 @@ __device__ __forceinline__ SoftStat soft_merge(SoftStat a, SoftStat b) {
 template <int MT, int LEAD, bool DUAL, bool LENS = false>
 __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   constexpr int KB = 64;
+  // weights are read once: the SwiGLU and lens launches (split 1, whole K per
+  // block) load them non-temporal (measured 2-6 % faster there, no gain with split-K)
+  constexpr int kWeightPolicy = (DUAL || LENS) ? 2 : 0;
   constexpr int BM = 32 * MT;
   constexpr int BN = DUAL ? 64 : 128;  // output columns per block
   constexpr int STAGES = LEAD + 1;
@@ -346,7 +349,7 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
       __builtin_amdgcn_global_load_lds(
           reinterpret_cast<const void*>(pw[q] + kb * KB),
           (__attribute__((address_space(3))) void*)(ring + st * STAGE_BYTES + A_BYTES + (wave * 4 + q) * 1024),
-          16, 0, 0);
+          16, 0, kWeightPolicy);
 #pragma unroll
     for (int j = 0; j < MT; ++j)
       __builtin_amdgcn_global_load_lds(
