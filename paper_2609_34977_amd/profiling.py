@@ -27,7 +27,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 # kernel class -> (source files whose text defines its kernels, dispatch-name pattern)
 CLASSES = {
     "gemm_gateup": (("csrc/gemm.hip", "csrc/kernels.h", "csrc/common.h"),
-                    r"gemm_stream_kernel<\d+, \d+, true>|gemm_bf16_kernel<\d+, \d+, \d+, \d+, \d+, true"),
+                    r"gemm_stream_kernel<\d+, \d+, true\b|gemm_bf16_kernel<\d+, \d+, \d+, \d+, \d+, true"),
 }
 
 
