@@ -62,7 +62,29 @@ def anchor_scores(cls_attn_tile: np.ndarray, col0: int = 1, n: int | None = None
     return (acc / np.float32(H)).astype(np.float32)
 
 
+def anchor_scores_colmean(attn_tile: np.ndarray) -> np.ndarray:
+    """Anchor scores of an encoder without [CLS] (Sec. 4.1.1): the attention each
+    patch receives, averaged over heads and over the patches attending to it.
+
+    ``attn_tile`` is [H, n, n] (head, query patch, key patch).  Returns float64
+    [n]: a[j] = mean over h and i of attn[h, i, j].
+    """
+    A = np.asarray(attn_tile, dtype=np.float64)
+    return A.mean(axis=(0, 1))
+
+
 # --------------------------------------------------------------------------- 2
+def budget_ratio(n: int, rv_num: int, rv_den: int, r_num: int = 7, r_den: int = 10):
+    """Budgets from a retention ratio R_v of an input-dependent token count (the
+    Qwen3-VL setting of the appendix): keep = floor(n * R_v), then budget(keep).
+    Exact rational arithmetic; returns (keep, k_anc, n_cmp)."""
+    if n < 0 or rv_den <= 0 or rv_num < 0 or rv_num > rv_den:
+        raise ValueError("bad ratio arguments")
+    keep = (n * rv_num) // rv_den
+    k_anc, n_cmp = budget(keep, r_num, r_den)
+    return keep, k_anc, n_cmp
+
+
 def budget(keep: int, r_num: int = 7, r_den: int = 10):
     """Anchor and complementary budgets (Sec. 4.1.1-4.1.2): k = floor(keep*r), keep - k."""
     if keep < 0 or r_den <= 0 or r_num < 0 or r_num > r_den:
@@ -239,18 +261,20 @@ def select(cluster: np.ndarray, s32: np.ndarray, n_cmp: int, K: int, mode: str =
 # --------------------------------------------------------------------------- tile
 def prune_tile(cls_attn_tile, feats_tile, keep: int, r_num: int = 7, r_den: int = 10,
                K: int = 4, max_iter: int = 10, mode: str = "literal", col0: int = 1,
-               row0: int = 1, cluster_override=None):
+               row0: int = 1, cluster_override=None, a=None):
     """Whole MSV-Prune for one tile (Alg. 1, stage 1).
 
     ``feats_tile``: list of [row0 + n, d] arrays, last = F^L.  Returns a dict
     with a, anchors, cluster (-1 = anchor), s (float64, +inf for anchors),
     s32, mvec, kmeans margin, quotas, idx (ascending kept patch indices).
     ``cluster_override`` replaces the K-means assignment of the non-anchor
-    tokens (used to score a known clustering).
+    tokens (used to score a known clustering).  ``a`` (length n) replaces the
+    [CLS] anchor scores (e.g. anchor_scores_colmean for encoders without
+    [CLS]); ``cls_attn_tile`` is then not read.
     """
     feats = [np.asarray(F, dtype=np.float64)[row0:] for F in feats_tile]
     n = feats[0].shape[0]
-    a = anchor_scores(cls_attn_tile, col0, n)
+    a = anchor_scores(cls_attn_tile, col0, n) if a is None else np.asarray(a, np.float64)
     k_anc, n_cmp = budget(keep, r_num, r_den)
     k_anc = min(k_anc, n)
     anchors = anchor_set(a, k_anc)
