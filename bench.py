@@ -49,6 +49,9 @@ def parse():
                    help="run one plain device copy of this size after warm-up (counter calibration)")
     p.add_argument("--score-sweep", action="store_true",
                    help="instead of the step: time scoring over 20/64/256/512 tiles (one JSON line each)")
+    p.add_argument("--colmean-sweep", action="store_true",
+                   help="instead of the step: time the anchor scores of encoders without [CLS] "
+                        "(column means of 16-head attention maps) over 1/8/64 tiles of 576 and 1024 patches")
     p.add_argument("--online", action="store_true",
                    help="decoder mask from the online skip controller on the device (logit lens over a "
                         "32000-token unembedding, w1=3, w2=1, T_skip=20) instead of the workload's mask")
@@ -223,6 +226,43 @@ def score_sweep(w, dev, args):
         torch.cuda.empty_cache()
 
 
+def colmean_sweep(dev):
+    """spider_anchor_colmean over G tiles of [16, n, n] fp32 maps: time per call (HIP events
+    around its two launches) and the algorithmic bytes (every map element read once, the
+    scores written once) over that time."""
+    from synth.vision import attention_maps
+    from paper_2609_34977_amd import _lib
+
+    H = 16
+    for n in (576, 1024):
+        for G in (1, 8, 64):
+            A = attention_maps(G, H, n, seed=0, device=dev)
+            out = torch.empty(G, n, dtype=torch.float32, device=dev)
+            for _ in range(3):
+                _lib.anchor_colmean(A, out)
+            torch.cuda.synchronize()
+            _lib.profile_mask(["anchor_colmean"])
+            _lib.profile_enable(True)
+            iters = 20
+            t0 = time.perf_counter()
+            for _ in range(iters):
+                _lib.anchor_colmean(A, out)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            prof = _lib.profile_read()["anchor_colmean"]
+            _lib.profile_enable(False)
+            _lib.profile_mask(None)
+            us = prof[1] * 1e3 / iters
+            byts = G * H * n * n * 4 + G * n * 4
+            ach = byts / (us * 1e-6) / 1e9
+            print(json.dumps({"mode": "colmean_sweep", "tiles": G, "heads": H, "patches": n,
+                              "us_per_call": us, "wall_us_per_call": (t1 - t0) * 1e6 / iters,
+                              "algorithmic_bytes": byts, "achieved_GBs": ach,
+                              "frac_of_hbm_peak": ach / HBM_PEAK_GBS}), flush=True)
+            del A, out
+            torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -238,6 +278,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.score_sweep:
         score_sweep(w, dev, args)
+        return
+    if args.colmean_sweep:
+        colmean_sweep(dev)
         return
     t_setup = time.perf_counter()
     attn, feats, src, text, W, pol = build_inputs(w, dev)

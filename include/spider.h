@@ -63,6 +63,35 @@ int spider_version(void);
  * ------------------------------------------------------------------------ */
 spider_status spider_budget(int keep, int r_num, int r_den, int* n_anchor, int* n_cmp);
 
+/* Budgets from a retention ratio R_v = rv_num / rv_den of an input-dependent
+ * token count n (the setting used for Qwen3-VL in the appendix): keep =
+ * floor(n * rv_num / rv_den) in exact integer arithmetic, then n_anchor and
+ * n_cmp as spider_budget(keep, r_num, r_den).  Requires n >= 0, rv_den > 0,
+ * 0 <= rv_num <= rv_den and spider_budget's conditions.  Host only. */
+spider_status spider_budget_ratio(int n, int rv_num, int rv_den, int r_num, int r_den, int* keep,
+                                  int* n_anchor, int* n_cmp);
+
+/* ------------------------------------------------------------------------
+ * spider_anchor_colmean - anchor scores of an encoder without [CLS]
+ * (Sec. 4.1.1: the mean attention each patch token receives):
+ *   a_out[g*n + j] = (1 / (H*n)) * sum_h sum_i attn[g, h, i, j]
+ * with element (g,h,i,j) at attn[g*stride_g + h*stride_h + i*stride_row + j]
+ * (query patch i, key patch j; device fp32, 16-byte aligned; n, the strides
+ * multiples of 4).  fp32 accumulation in a fixed order (per head, 128-row
+ * chunks summed by rows in ascending order within each of four interleaved
+ * row sets; the chunk sums, numbered head-major, added in ascending order
+ * within four interleaved sets, the sets combined pairwise), one IEEE
+ * division: identical inputs give identical bits.  The result feeds spider_score with
+ * cls_attn = NULL.  Limits: 1 <= n <= 4096, 1 <= H <= 1024, 1 <= G <= 65535.
+ * Workspace: spider_anchor_colmean_workspace_size(G, H, n) bytes, 256-byte
+ * aligned (chunk sums; contents on entry ignored).
+ * ------------------------------------------------------------------------ */
+size_t spider_anchor_colmean_workspace_size(int G, int H, int n);
+
+spider_status spider_anchor_colmean(int G, int H, int n, const float* attn, int64_t stride_g,
+                                    int64_t stride_h, int64_t stride_row, float* a_out,
+                                    void* workspace, size_t workspace_bytes, spider_stream stream);
+
 /* ------------------------------------------------------------------------
  * spider_score - MSV-Prune scoring of G independent tiles (Sec. 4.1, Eq. 1
  * and Eq. 3, Algorithm 1 stage 1).  For every tile g and patch i < n:
@@ -87,11 +116,14 @@ spider_status spider_budget(int keep, int r_num, int r_den, int* n_anchor, int* 
  *   cls_attn  device fp32; element (g,h,c) at cls_attn[g*attn_stride_g +
  *             h*attn_stride_h + c]; patch i is column attn_col0 + i (the CLS
  *             row of the last tapped layer's attention, column 0 = CLS).
+ *             NULL (with H = 0, strides and attn_col0 ignored): a_out holds
+ *             the anchor scores on entry (e.g. from spider_anchor_colmean for
+ *             encoders without [CLS]) and is left unchanged.
  *   feats     HOST array of n_layers device pointers (tapped layers, the last
  *             one is F^L), each of dtype feat_dtype; patch i of tile g is row
  *             feat_row0 + i: element (g,row,c) at feats[l][g*feat_stride_g +
  *             row*feat_stride_row + c].
- *   Limits: 1 <= n <= 4096, 1 <= H, 1 <= d_v <= 2048, 1 <= n_layers <= 8,
+ *   Limits: 1 <= n <= 4096, 1 <= H (0 with given scores), 1 <= d_v <= 2048, 1 <= n_layers <= 8,
  *   1 <= K <= 8, 0 <= n_anchor <= n, kmeans_max_iter >= 1.
  * Outputs (device, [G,n], row stride n): a_out fp32, cluster_out int32,
  *   s_out fp32, m_out fp32 (may be NULL).

@@ -44,6 +44,9 @@ _SIGS = {
     "spider_last_error": ([], ctypes.c_char_p),
     "spider_version": ([], _I),
     "spider_budget": ([_I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I)], _I),
+    "spider_budget_ratio": ([_I, _I, _I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I), ctypes.POINTER(_I)], _I),
+    "spider_anchor_colmean_workspace_size": ([_I, _I, _I], _SZ),
+    "spider_anchor_colmean": ([_I, _I, _I, _VP, _I64, _I64, _I64, _VP, _VP, _SZ, _VP], _I),
     "spider_score_workspace_size": ([_I, _I, _I, _I, _I], _SZ),
     "spider_score": ([_I, _I, _I, _I, _I, _VP, _I64, _I64, _I, ctypes.POINTER(_VP), _I, _I64, _I64,
                       _I, _I, _I, _I, _VP, _VP, _VP, _VP, _VP, _SZ, _VP], _I),
@@ -123,6 +126,14 @@ def budget(keep: int, r_num: int = 7, r_den: int = 10):
     return a.value, c.value
 
 
+def budget_ratio(n: int, rv_num: int, rv_den: int, r_num: int = 7, r_den: int = 10):
+    """(keep, n_anchor, n_cmp) for a retention ratio rv_num / rv_den of n tokens."""
+    k, a, c = _I(), _I(), _I()
+    _check(lib().spider_budget_ratio(n, rv_num, rv_den, r_num, r_den, ctypes.byref(k), ctypes.byref(a),
+                                     ctypes.byref(c)))
+    return k.value, a.value, c.value
+
+
 def slc_policy(slc_attn, slc_ffn, eps: float = 1e-8):
     sa = np.ascontiguousarray(slc_attn, dtype=np.float32)
     sf = np.ascontiguousarray(slc_ffn, dtype=np.float32)
@@ -150,18 +161,46 @@ def plan_skips(s_sa, slc_sel, target, w1: float, w2: float, T_skip: float, L: in
 
 
 # ----------------------------------------------------------------- device calls
-def score(cls_attn: torch.Tensor, feats: Sequence[torch.Tensor], n_anchor: int, K: int = 4,
-          max_iter: int = 10, attn_col0: int = 1, feat_row0: int = 1, n: Optional[int] = None):
-    """MSV-Prune scoring of G tiles.  cls_attn [G,H,T] fp32, feats list of [G,T,d_v]."""
-    G, H, T = cls_attn.shape
-    n = T - attn_col0 if n is None else n
+def anchor_colmean(attn: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Anchor scores without [CLS]: attn [G, H, n, n] fp32 (any strides with unit column
+    stride) -> a [G, n] fp32, the mean over heads and query rows."""
+    G, H, n, n2 = attn.shape
+    if n2 != n or attn.stride(3) != 1:
+        raise ValueError("attn must be [G, H, n, n] with contiguous rows")
+    dev = attn.device
+    if out is None:
+        out = torch.empty(G, n, dtype=torch.float32, device=dev)
+    L = lib()
+    wsz = L.spider_anchor_colmean_workspace_size(G, H, n)
+    ws = _ws(wsz, dev)
+    _check(L.spider_anchor_colmean(G, H, n, _ptr(attn), attn.stride(0), attn.stride(1), attn.stride(2),
+                                   _ptr(out), _aligned(ws), wsz, _stream(dev)))
+    return out
+
+
+def score(cls_attn: Optional[torch.Tensor], feats: Sequence[torch.Tensor], n_anchor: int, K: int = 4,
+          max_iter: int = 10, attn_col0: int = 1, feat_row0: int = 1, n: Optional[int] = None,
+          a: Optional[torch.Tensor] = None):
+    """MSV-Prune scoring of G tiles.  cls_attn [G,H,T] fp32, feats list of [G,T,d_v];
+    or cls_attn None and a [G, n] fp32 given anchor scores (encoders without [CLS])."""
     f0 = feats[0]
     d_v = f0.shape[-1]
-    dev = cls_attn.device
+    if cls_attn is None:
+        if a is None:
+            raise ValueError("give cls_attn or the anchor scores a")
+        G, n = a.shape
+        H, T = 0, 0
+        dev = a.device
+    else:
+        G, H, T = cls_attn.shape
+        n = T - attn_col0 if n is None else n
+        dev = cls_attn.device
     for f in feats:
         if f.dtype != f0.dtype or f.shape != f0.shape or f.stride() != f0.stride():
             raise ValueError("all tapped layers must share dtype, shape and strides")
-    a = torch.empty(G, n, dtype=torch.float32, device=dev)
+    # given scores are copied: the library reads them from (and leaves them in) a_out
+    a = a.float().contiguous().clone() if cls_attn is None else torch.empty(G, n, dtype=torch.float32,
+                                                                            device=dev)
     cl = torch.empty(G, n, dtype=torch.int32, device=dev)
     s = torch.empty(G, n, dtype=torch.float32, device=dev)
     m = torch.empty(G, n, dtype=torch.float32, device=dev)
@@ -169,8 +208,10 @@ def score(cls_attn: torch.Tensor, feats: Sequence[torch.Tensor], n_anchor: int, 
     wsz = L.spider_score_workspace_size(G, n, d_v, len(feats), K)
     ws = _ws(wsz, dev)
     fptr = (ctypes.c_void_p * len(feats))(*[f.data_ptr() for f in feats])
-    _check(L.spider_score(G, n, H, d_v, len(feats), _ptr(cls_attn), cls_attn.stride(0),
-                          cls_attn.stride(1), attn_col0, fptr, _dt(f0), f0.stride(0), f0.stride(1),
+    _check(L.spider_score(G, n, H, d_v, len(feats), _ptr(cls_attn),
+                          cls_attn.stride(0) if cls_attn is not None else 0,
+                          cls_attn.stride(1) if cls_attn is not None else 0, attn_col0, fptr, _dt(f0),
+                          f0.stride(0), f0.stride(1),
                           feat_row0, n_anchor, K, max_iter, _ptr(a), _ptr(cl), _ptr(s), _ptr(m),
                           _aligned(ws), wsz, _stream(dev)))
     return {"a": a, "cluster": cl, "s": s, "m": m}

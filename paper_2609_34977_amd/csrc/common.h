@@ -65,6 +65,7 @@ enum KernelClass {
   KC_LENS_PREP,
   KC_GEMM_LENS,
   KC_LENS_ADMIT,
+  KC_COLMEAN,
   KC_COUNT
 };
 

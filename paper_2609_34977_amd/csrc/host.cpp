@@ -71,7 +71,7 @@ const char* kClassNames[KC_COUNT] = {
     "score_prep", "anchor_topk", "kmeans",   "anchor_maxsim", "score_final",
     "select",     "assemble",    "embed",    "rmsnorm",       "gemm_qkv",
     "qkv_finalize", "attention", "gemm_o",   "gemm_gateup",   "gemm_down",
-    "residual_add", "lens_prep", "gemm_lens", "lens_admit"};
+    "residual_add", "lens_prep", "gemm_lens", "lens_admit", "anchor_colmean"};
 }  // namespace
 
 void prof_begin(int cls, hipStream_t s) {
@@ -128,7 +128,7 @@ extern "C" {
 
 const char* spider_last_error(void) { return g_error.c_str(); }
 
-int spider_version(void) { return 100; }
+int spider_version(void) { return 101; }
 
 spider_status spider_budget(int keep, int r_num, int r_den, int* n_anchor, int* n_cmp) {
   clear_error();
@@ -138,6 +138,22 @@ spider_status spider_budget(int keep, int r_num, int r_den, int* n_anchor, int* 
   long long k = (long long)keep * r_num / r_den;
   *n_anchor = (int)k;
   *n_cmp = keep - (int)k;
+  return SPIDER_OK;
+}
+
+spider_status spider_budget_ratio(int n, int rv_num, int rv_den, int r_num, int r_den, int* keep,
+                                  int* n_anchor, int* n_cmp) {
+  clear_error();
+  SPIDER_REQUIRE(keep && n_anchor && n_cmp, SPIDER_ERR_INVALID_ARG, "spider_budget_ratio: null output");
+  SPIDER_REQUIRE(n >= 0 && rv_den > 0 && rv_num >= 0 && rv_num <= rv_den, SPIDER_ERR_INVALID_ARG,
+                 "spider_budget_ratio: need n >= 0, rv_den > 0, 0 <= rv_num <= rv_den");
+  const int kp = (int)((long long)n * rv_num / rv_den);
+  int a = 0, c = 0;
+  const spider_status s = spider_budget(kp, r_num, r_den, &a, &c);
+  if (s != SPIDER_OK) return s;
+  *keep = kp;
+  *n_anchor = a;
+  *n_cmp = c;
   return SPIDER_OK;
 }
 

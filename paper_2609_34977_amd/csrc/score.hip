@@ -112,7 +112,7 @@ __global__ void __launch_bounds__(256) score_prep_kernel(
     ss = wave_sum(ss);
     if (lane == 0) nu[((int64_t)g * n_layers + l) * n + i] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
   }
-  if (lane == 0) {
+  if (lane == 0 && attn) {  // null: the anchor scores are given in a_out
     const float* col = attn + (int64_t)g * as_g + col0 + i;
     float acc = 0.f;
     for (int h = 0; h < H; ++h) acc = __fadd_rn(acc, col[(int64_t)h * as_h]);
@@ -768,8 +768,12 @@ extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers
                                       void* workspace, size_t workspace_bytes,
                                       spider_stream stream) {
   clear_error();
-  SPIDER_REQUIRE(G >= 1 && n >= 1 && H >= 1 && d_v >= 1 && n_layers >= 1, SPIDER_ERR_INVALID_ARG,
-                 "spider_score: G, n, H, d_v and n_layers must be >= 1");
+  SPIDER_REQUIRE(G >= 1 && n >= 1 && d_v >= 1 && n_layers >= 1, SPIDER_ERR_INVALID_ARG,
+                 "spider_score: G, n, d_v and n_layers must be >= 1");
+  // cls_attn == NULL with H == 0: a_out already holds the anchor scores (input)
+  const bool given_a = cls_attn == nullptr;
+  SPIDER_REQUIRE(given_a ? H == 0 : H >= 1, SPIDER_ERR_INVALID_ARG,
+                 "spider_score: H must be >= 1 with CLS attention, 0 with given anchor scores");
   SPIDER_REQUIRE(n <= kMaxN, SPIDER_ERR_UNSUPPORTED, "spider_score: n = %d exceeds 4096", n);
   SPIDER_REQUIRE(d_v <= 2048, SPIDER_ERR_UNSUPPORTED, "spider_score: d_v = %d exceeds 2048", d_v);
   SPIDER_REQUIRE(n_layers <= 8, SPIDER_ERR_UNSUPPORTED, "spider_score: at most 8 tapped layers");
@@ -780,13 +784,14 @@ extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers
                  "spider_score: n_anchor = %d outside [0, n = %d]", n_anchor, n);
   SPIDER_REQUIRE(kmeans_max_iter >= 1, SPIDER_ERR_INVALID_ARG,
                  "spider_score: kmeans_max_iter must be >= 1");
-  SPIDER_REQUIRE(cls_attn && feats && a_out && cluster_out && s_out, SPIDER_ERR_INVALID_ARG,
+  SPIDER_REQUIRE(feats && a_out && cluster_out && s_out, SPIDER_ERR_INVALID_ARG,
                  "spider_score: null pointer argument");
   SPIDER_REQUIRE(feat_dtype == SPIDER_F32 || feat_dtype == SPIDER_BF16, SPIDER_ERR_INVALID_ARG,
                  "spider_score: bad feature dtype");
-  SPIDER_REQUIRE(attn_col0 >= 0 && feat_row0 >= 0 && attn_stride_h >= attn_col0 + n &&
-                     attn_stride_g >= (int64_t)H * attn_stride_h,
+  SPIDER_REQUIRE(given_a || (attn_col0 >= 0 && attn_stride_h >= attn_col0 + n &&
+                              attn_stride_g >= (int64_t)H * attn_stride_h),
                  SPIDER_ERR_SHAPE, "spider_score: attention strides do not cover [H, col0 + n]");
+  SPIDER_REQUIRE(feat_row0 >= 0, SPIDER_ERR_SHAPE, "spider_score: feat_row0 must be >= 0");
   SPIDER_REQUIRE(feat_stride_row >= d_v && feat_stride_g >= (int64_t)(feat_row0 + n) * feat_stride_row,
                  SPIDER_ERR_SHAPE, "spider_score: feature strides do not cover [row0 + n, d_v]");
   SPIDER_REQUIRE(feat_stride_row % 8 == 0 && feat_stride_g % 8 == 0 && d_v % 8 == 0,

@@ -145,3 +145,22 @@ def vision_inputs(cfg: ScoreCfg, seed: int = 0, tie_stress: bool = False):
             a = (np.round(a * 64.0) / 64.0).astype(np.float32)
         return torch.from_numpy(a), [torch.from_numpy(x) for x in f]
     return llava_taps(cfg, seed, tie_stress)
+
+
+def attention_maps(G: int, H: int, n: int, seed: int = 0, device="cpu") -> torch.Tensor:
+    """Full self-attention maps [G, H, n, n] fp32 of an encoder without [CLS]:
+    per (tile, head, query) a softmax over keys of 2 N(0,1) logits, plus +3 on a
+    seeded 5 % of key patches per tile (patches most queries attend to, the
+    peaked profile of ViT attention).  Logits from the counter generator (same
+    bits on every device); the softmax is evaluated in float64 on the host
+    when device is "cpu", else in float32 on the device (sweeps only)."""
+    from .counter_rng import normal_f32
+    z = normal_f32((G, H, n, n), seed, 4400, 2.0, device=device)
+    r = rng(seed, 4401)
+    boost = torch.zeros(G, 1, 1, n, dtype=torch.float32)
+    for g in range(G):
+        boost[g, 0, 0, r.choice(n, max(1, n // 20), replace=False)] = 3.0
+    z = z + boost.to(device)
+    if torch.device(device).type == "cpu":
+        return torch.softmax(z.double(), dim=-1).float()
+    return torch.softmax(z, dim=-1)

@@ -226,6 +226,51 @@ def test_prefill_online_validation_before_any_hip_call(L):
     assert lib_mod.prefill_online_workspace_size(bf, 1, 192, 32000) > lib_mod.prefill_workspace_size(bf, 1, 192)
 
 
+@pytest.mark.parametrize("n,num,den", [(576, 1, 2), (1000, 2, 5), (7, 1, 2), (1369, 1, 2), (50, 1, 1), (50, 0, 3)])
+def test_budget_ratio_matches_oracle(L, n, num, den):
+    assert lib_mod.budget_ratio(n, num, den) == mp.budget_ratio(n, num, den)
+    assert lib_mod.budget_ratio(n, num, den, 1, 2) == mp.budget_ratio(n, num, den, 1, 2)
+
+
+def test_budget_ratio_rejects_bad_arguments(L):
+    k, a, c = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    for args in [(-1, 1, 2), (10, 3, 2), (10, 1, 0), (10, -1, 2)]:
+        assert L.spider_budget_ratio(*args, 7, 10, ctypes.byref(k), ctypes.byref(a), ctypes.byref(c)) == INVALID
+    assert L.spider_budget_ratio(10, 1, 2, 11, 10, ctypes.byref(k), ctypes.byref(a), ctypes.byref(c)) == INVALID
+
+
+def _colmean_call(L, G=2, H=16, n=576, attn=0x1000, sg=None, sh=None, sr=None, ws=0x100000, wsb=1 << 40):
+    sr = n if sr is None else sr
+    sh = n * sr if sh is None else sh
+    sg = H * sh if sg is None else sg
+    return L.spider_anchor_colmean(G, H, n, attn, sg, sh, sr, 0x2000, ws, wsb, None)
+
+
+def test_anchor_colmean_validation_before_any_hip_call(L):
+    assert _colmean_call(L, G=0) == INVALID
+    assert _colmean_call(L, n=4100) == UNSUPPORTED
+    assert _colmean_call(L, H=2000) == UNSUPPORTED
+    assert _colmean_call(L, attn=None) == INVALID
+    assert _colmean_call(L, sr=500) == SHAPE
+    assert _colmean_call(L, n=574) == UNSUPPORTED          # n % 4
+    assert _colmean_call(L, attn=0x1004) == UNSUPPORTED    # 16-byte alignment
+    assert _colmean_call(L, wsb=100) == WORKSPACE
+    assert _colmean_call(L, ws=0x100010) == WORKSPACE
+    assert lib_mod.anchor_colmean.__doc__
+    assert L.spider_anchor_colmean_workspace_size(1, 16, 576) == 16 * 5 * 576 * 4
+
+
+def test_score_with_given_anchor_scores_validation(L):
+    feats = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    # H must be 0 when cls_attn is NULL, >= 1 otherwise
+    assert L.spider_score(1, 576, 16, 1024, 2, None, 0, 0, 0, feats, lib_mod.BF16, 577 * 1024, 1024, 1,
+                          89, 4, 10, 0x3000, 0x4000, 0x5000, None, 0x100000, 1 << 40, None) == INVALID
+    assert L.spider_score(1, 576, 0, 1024, 2, 0x1000, 577, 577, 1, feats, lib_mod.BF16, 577 * 1024, 1024, 1,
+                          89, 4, 10, 0x3000, 0x4000, 0x5000, None, 0x100000, 1 << 40, None) == INVALID
+    assert L.spider_score(1, 576, 0, 1024, 2, None, 0, 0, 0, feats, lib_mod.BF16, 577 * 1024, 1024, 1,
+                          89, 4, 10, 0x3000, 0x4000, 0x5000, None, 0x100000, 100, None) == WORKSPACE
+
+
 def test_profiler_host_side(L):
     lib_mod.profile_enable(True)
     d = lib_mod.profile_read()
