@@ -62,6 +62,22 @@ def anchor_scores(cls_attn_tile: np.ndarray, col0: int = 1, n: int | None = None
     return (acc / np.float32(H)).astype(np.float32)
 
 
+def cls_attention(q_cls: np.ndarray, keys: np.ndarray, scale: float) -> np.ndarray:
+    """The [CLS] row of a ViT layer's self-attention rebuilt from its query and
+    keys, for encoders that never store attention maps (Sec. 4.1.1 reads this
+    row): per head h, softmax over tokens j of scale * q_cls[h] . keys[j, h].
+
+    ``q_cls`` is [H, dh], ``keys`` [T, H, dh] (token 0 = [CLS]).  Returns
+    float64 [H, T]; anchor_scores() then averages it over heads.
+    """
+    q = np.asarray(q_cls, dtype=np.float64)
+    k = np.asarray(keys, dtype=np.float64)
+    z = np.einsum("hc,jhc->hj", q, k) * float(scale)
+    z = z - z.max(axis=1, keepdims=True)
+    e = np.exp(z)
+    return e / e.sum(axis=1, keepdims=True)
+
+
 def anchor_scores_colmean(attn_tile: np.ndarray) -> np.ndarray:
     """Anchor scores of an encoder without [CLS] (Sec. 4.1.1): the attention each
     patch receives, averaged over heads and over the patches attending to it.
