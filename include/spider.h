@@ -88,6 +88,25 @@ spider_status spider_budget_ratio(int n, int rv_num, int rv_den, int r_num, int 
  * ------------------------------------------------------------------------ */
 size_t spider_anchor_colmean_workspace_size(int G, int H, int n);
 
+/* ------------------------------------------------------------------------
+ * spider_cls_attention - the [CLS] row of a ViT layer's self-attention rebuilt
+ * from its CLS query and keys, for encoders that never store attention maps
+ * (the row Sec. 4.1.1 averages over heads):
+ *   attn_out[(g*H + h)*n_tok + j] = softmax over j of scale * q[g,h,:] . k[g,j,h,:]
+ * with q element (g,h,c) at q[g*q_stride_g + h*dh + c] and k element (g,j,h,c)
+ * at k[g*k_stride_g + j*k_stride_row + h*dh + c] (token 0 = [CLS]); dtype of q
+ * and k bf16 or fp32 (device), output fp32 [G, H, n_tok] contiguous: pass it
+ * to spider_score with attn_stride_h = n_tok, attn_stride_g = H*n_tok,
+ * attn_col0 = 1.  fp32 arithmetic in a fixed order (dot products over c
+ * ascending, the row maximum subtracted, exponentials summed per thread in
+ * token order then in a fixed tree, one IEEE division per token).
+ * Limits: dh <= 256, n_tok <= 4097, G, H <= 65535; dh and the strides
+ * multiples of 4, q and k aligned to 4 elements.  No workspace.
+ * ------------------------------------------------------------------------ */
+spider_status spider_cls_attention(int G, int H, int dh, int n_tok, const void* q, int64_t q_stride_g,
+                                   const void* k, int64_t k_stride_g, int64_t k_stride_row,
+                                   spider_dtype dtype, float scale, float* attn_out, spider_stream stream);
+
 spider_status spider_anchor_colmean(int G, int H, int n, const float* attn, int64_t stride_g,
                                     int64_t stride_h, int64_t stride_row, float* a_out,
                                     void* workspace, size_t workspace_bytes, spider_stream stream);

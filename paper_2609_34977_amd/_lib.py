@@ -47,6 +47,7 @@ _SIGS = {
     "spider_budget_ratio": ([_I, _I, _I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I), ctypes.POINTER(_I)], _I),
     "spider_anchor_colmean_workspace_size": ([_I, _I, _I], _SZ),
     "spider_anchor_colmean": ([_I, _I, _I, _VP, _I64, _I64, _I64, _VP, _VP, _SZ, _VP], _I),
+    "spider_cls_attention": ([_I, _I, _I, _I, _VP, _I64, _VP, _I64, _I64, _I, _F, _VP, _VP], _I),
     "spider_score_workspace_size": ([_I, _I, _I, _I, _I], _SZ),
     "spider_score": ([_I, _I, _I, _I, _I, _VP, _I64, _I64, _I, ctypes.POINTER(_VP), _I, _I64, _I64,
                       _I, _I, _I, _I, _VP, _VP, _VP, _VP, _VP, _SZ, _VP], _I),
@@ -175,6 +176,20 @@ def anchor_colmean(attn: torch.Tensor, out: Optional[torch.Tensor] = None) -> to
     ws = _ws(wsz, dev)
     _check(L.spider_anchor_colmean(G, H, n, _ptr(attn), attn.stride(0), attn.stride(1), attn.stride(2),
                                    _ptr(out), _aligned(ws), wsz, _stream(dev)))
+    return out
+
+
+def cls_attention(q: torch.Tensor, k: torch.Tensor, scale: float, out: Optional[torch.Tensor] = None):
+    """[CLS] attention rows from q [G, H, dh] and keys k [G, T, H, dh] (last two dims
+    contiguous) -> [G, H, T] fp32."""
+    G, H, dh = q.shape
+    T = k.shape[1]
+    if k.shape != (G, T, H, dh) or q.stride(2) != 1 or q.stride(1) != dh or k.stride(3) != 1 or k.stride(2) != dh:
+        raise ValueError("q must be [G, H, dh] and k [G, T, H, dh] with contiguous heads")
+    if out is None:
+        out = torch.empty(G, H, T, dtype=torch.float32, device=q.device)
+    _check(lib().spider_cls_attention(G, H, dh, T, _ptr(q), q.stride(0), _ptr(k), k.stride(0), k.stride(1),
+                                      _dt(q), scale, _ptr(out), _stream(q.device)))
     return out
 
 

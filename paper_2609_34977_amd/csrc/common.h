@@ -66,6 +66,7 @@ enum KernelClass {
   KC_GEMM_LENS,
   KC_LENS_ADMIT,
   KC_COLMEAN,
+  KC_CLS_ATTN,
   KC_COUNT
 };
 

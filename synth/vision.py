@@ -164,3 +164,24 @@ def attention_maps(G: int, H: int, n: int, seed: int = 0, device="cpu") -> torch
     if torch.device(device).type == "cpu":
         return torch.softmax(z.double(), dim=-1).float()
     return torch.softmax(z, dim=-1)
+
+
+def cls_query_keys(G: int, H: int, dh: int, T: int, seed: int = 0, dtype: str = "bf16"):
+    """CLS query [G, H, dh] and keys [G, T, H, dh] of a ViT layer (token 0 = [CLS]):
+    N(0, 1) entries, and on a seeded 20 % of the patch tokens of each tile the keys
+    of every head get b times that head's query added, b uniform in [0.5, 2]
+    (salient patches of graded strength: the peaked [CLS] profile of CLIP with a
+    spread of ranks among the patches a budget keeps).  Rounded once to bf16 (or
+    kept fp32)."""
+    r = rng(seed, 4500)
+    q = r.standard_normal((G, H, dh))
+    k = r.standard_normal((G, T, H, dh))
+    for g in range(G if T > 1 else 0):
+        sal = 1 + r.choice(T - 1, max(1, (T - 1) // 5), replace=False)
+        b = r.uniform(0.5, 2.0, size=len(sal))
+        k[g, sal] += b[:, None, None] * q[g][None]
+    qt = torch.from_numpy(q.astype(np.float32))
+    kt = torch.from_numpy(k.astype(np.float32))
+    if dtype == "bf16":
+        return f32_to_bf16_rne(qt), f32_to_bf16_rne(kt)
+    return qt, kt

@@ -271,6 +271,24 @@ def test_score_with_given_anchor_scores_validation(L):
                           89, 4, 10, 0x3000, 0x4000, 0x5000, None, 0x100000, 100, None) == WORKSPACE
 
 
+def test_cls_attention_validation_before_any_hip_call(L):
+    def call(G=1, H=16, dh=64, T=577, q=0x1000, sqg=None, k=0x2000, skg=None, skr=None, dt=lib_mod.BF16, sc=0.125):
+        sqg = H * dh if sqg is None else sqg
+        skr = H * dh if skr is None else skr
+        skg = T * skr if skg is None else skg
+        return L.spider_cls_attention(G, H, dh, T, q, sqg, k, skg, skr, dt, sc, 0x3000, None)
+    assert call(G=0) == INVALID
+    assert call(q=None) == INVALID
+    assert call(dt=7) == INVALID
+    assert call(sc=float("nan")) == INVALID
+    assert call(dh=512) == UNSUPPORTED
+    assert call(T=5000) == UNSUPPORTED
+    assert call(skr=100) == SHAPE
+    assert call(dh=62) == UNSUPPORTED
+    assert call(q=0x1004) == UNSUPPORTED      # bf16 needs 8-byte alignment
+    assert call(q=0x1008, dt=lib_mod.F32) == UNSUPPORTED
+
+
 def test_profiler_host_side(L):
     lib_mod.profile_enable(True)
     d = lib_mod.profile_read()
