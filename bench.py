@@ -56,6 +56,9 @@ def parse():
                    help="decoder mask from the online skip controller on the device (logit lens over a "
                         "32000-token unembedding, w1=3, w2=1, T_skip=20) instead of the workload's mask")
     p.add_argument("--vocab", type=int, default=32000)
+    p.add_argument("--projector", action="store_true",
+                   help="prune before the projector: the step also runs LLaVA's two-layer GELU projector "
+                        "(ViT width -> decoder width) on the kept rows only")
     return p.parse_args()
 
 
@@ -289,9 +292,15 @@ def main():
     sc, dec = w.score, w.dec
     cfg = _lib.decoder_cfg(dec.L, dec.d, dec.H, dec.d_ff,
                            _lib.BF16 if dec.dtype == "bf16" else _lib.F32, dec.eps, dec.theta)
+    projector = None
+    if args.projector:
+        from synth.decoder_inputs import projector_inputs, projector_weights
+        projector = projector_weights(w, dev)
+        src = projector_inputs(w, dev)
     pipe = Pipeline(G=sc.G, n=sc.n, K=sc.K, keep=sc.keep, r_num=sc.r_num, r_den=sc.r_den,
                     kmeans_iter=sc.kmeans_iter, tiles_per_sample=w.tiles_per_sample,
-                    n_text=w.n_text, quota_mode=w.quota_mode, dec=cfg, weights=W, device=dev)
+                    n_text=w.n_text, quota_mode=w.quota_mode, dec=cfg, weights=W, device=dev,
+                    projector=projector)
     torch.cuda.synchronize()
     print(f"# setup {time.perf_counter() - t_setup:.1f} s", file=sys.stderr, flush=True)
 
@@ -370,7 +379,8 @@ def main():
         "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": dec.dtype, "data": "synthetic",
-        "config": {"workload": f"{w.name}_keep{sc.keep}" + ("_online" if args.online else ""),
+        "config": {"workload": f"{w.name}_keep{sc.keep}" + ("_online" if args.online else "")
+                   + ("_projector" if args.projector else ""),
                    "batch": B, "tiles": sc.G,
                    "visual_tokens_per_tile": sc.n, "keep_per_tile": sc.keep,
                    "text_tokens": w.n_text, "decoder_rows": rows, "decoder_layers": dec.L,
@@ -390,7 +400,7 @@ def main():
         "kernel_ms_per_step": {k: round(v, 4) for k, v in kernel_ms.items()},
         "launches_per_step": launches,
     }
-    if not args.no_cpu_baseline and not args.online:
+    if not args.no_cpu_baseline and not args.online and not args.projector:
         print("# cpu baseline", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, min(args.cpu_layers, dec.L), W)
     print(json.dumps(res), flush=True)

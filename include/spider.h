@@ -177,13 +177,16 @@ spider_status spider_score(int G, int n, int H, int d_v, int n_layers,
  *             row (up to cap) is -1; count_out[g] = count.
  *   cap must be >= min(n, n_anchor + n_cmp + K) (the largest count Eq. 2 can
  *   produce when n_anchor patches are anchors).
- * Assembly (skipped when src == NULL): B = G / tiles_per_sample samples; the
- *   packed decoder input x_out holds, per sample b, the kept rows of its
- *   tiles in tile order (row i of tile g = src[g*src_stride_g + i*d_model])
- *   followed by its n_text text rows (text[b*n_text*d_model + t*d_model]),
- *   samples one after another; cu_seqlens_out[0..B] (device int32) gets the
- *   sample boundaries.  src/text/x_out have dtype act_dtype.  x_out must hold
- *   B*(tiles_per_sample*cap + n_text) rows of d_model.  In quota_mode 0 the
+ * Assembly (skipped when src and x_out are both NULL): B = G / tiles_per_sample
+ *   samples; the packed decoder input x_out holds, per sample b, the kept rows
+ *   of its tiles in tile order (row i of tile g = src[g*src_stride_g +
+ *   i*d_model]) followed by its n_text text rows (text[b*n_text*d_model +
+ *   t*d_model]), samples one after another; cu_seqlens_out[0..B] (device
+ *   int32) gets the sample boundaries.  With src == NULL and x_out given only
+ *   the text rows and the boundaries are written: the kept rows are then
+ *   projected into place by spider_project_kept.  src/text/x_out have dtype
+ *   act_dtype.  x_out must hold B*(tiles_per_sample*cap + n_text) rows of
+ *   d_model.  In quota_mode 0 the
  *   caller reads cu_seqlens_out (one device-to-host copy) to size the
  *   prefill; in quota_mode 1 every count is n_anchor + min(n_cmp, n - n_anchor).
  * No workspace.  Limits: 1 <= n <= 4096, 1 <= K <= 8, tiles_per_sample >= 1
@@ -195,6 +198,35 @@ spider_status spider_select(int G, int n, const int32_t* cluster, const float* s
                             int tiles_per_sample, const void* src, int64_t src_stride_g,
                             int d_model, spider_dtype act_dtype, const void* text, int n_text,
                             void* x_out, int32_t* cu_seqlens_out, spider_stream stream);
+
+/* ------------------------------------------------------------------------
+ * spider_project_kept - the multimodal projector on the kept rows only
+ * (pruning happens in the ViT feature space, before the projector: the
+ * appendix's reading for LLaVA and its AnyRes tiles).  For every tile g and
+ * slot r < count[g] (idx, count as written by spider_select, idx row stride
+ * cap), with x the feature row of patch idx[g*cap + r] (element (g,row,c) at
+ * feats[g*feat_stride_g + row*feat_stride_row + c], patch i in row
+ * feat_row0 + i):
+ *   x_out[dst] = W2 GELU(W1 x + b1) + b2,   GELU(t) = t (1 + erf(t/sqrt 2)) / 2
+ * where dst is the row spider_select's assembly gives that kept token (kept
+ * rows of a sample's tiles in tile order, then its n_text text rows).
+ * W1 [d_hid, d_in], W2 [d_out, d_hid] in nn.Linear layout and dtype; b1 [d_hid],
+ * b2 [d_out] fp32 or NULL (zero).  Precision (bf16): GEMMs accumulate in fp32,
+ * bias and GELU in fp32, the hidden rows and the outputs rounded to bf16;
+ * (fp32): everything fp32.  Slots past count[g] are computed on a valid row
+ * and never stored.  Requires feat_stride_g to be a multiple of
+ * feat_stride_row; bf16: d_in, d_hid, d_out multiples of 64, feats/W1/W2
+ * 16-byte aligned, feat_stride_row a multiple of 8.
+ * Workspace: spider_project_kept_workspace_size(G, cap, d_hid, d_out, dtype).
+ * ------------------------------------------------------------------------ */
+size_t spider_project_kept_workspace_size(int G, int cap, int d_hid, int d_out, spider_dtype dtype);
+
+spider_status spider_project_kept(int G, int tiles_per_sample, int cap, const int32_t* idx,
+                                  const int32_t* count, const void* feats, int64_t feat_stride_g,
+                                  int64_t feat_stride_row, int feat_row0, int d_in, const void* w1,
+                                  const float* b1, int d_hid, const void* w2, const float* b2, int d_out,
+                                  int n_text, spider_dtype dtype, void* x_out, void* workspace,
+                                  size_t workspace_bytes, spider_stream stream);
 
 /* ------------------------------------------------------------------------
  * Offline sub-layer contribution policy (Sec. 4.2.2, Eq. 5).  Host only.

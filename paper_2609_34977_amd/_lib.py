@@ -48,6 +48,9 @@ _SIGS = {
     "spider_anchor_colmean_workspace_size": ([_I, _I, _I], _SZ),
     "spider_anchor_colmean": ([_I, _I, _I, _VP, _I64, _I64, _I64, _VP, _VP, _SZ, _VP], _I),
     "spider_cls_attention": ([_I, _I, _I, _I, _VP, _I64, _VP, _I64, _I64, _I, _F, _VP, _VP], _I),
+    "spider_project_kept_workspace_size": ([_I, _I, _I, _I, _I], _SZ),
+    "spider_project_kept": ([_I, _I, _I, _VP, _VP, _VP, _I64, _I64, _I, _I, _VP, _VP, _I, _VP, _VP, _I, _I, _I,
+                             _VP, _VP, _SZ, _VP], _I),
     "spider_score_workspace_size": ([_I, _I, _I, _I, _I], _SZ),
     "spider_score": ([_I, _I, _I, _I, _I, _VP, _I64, _I64, _I, ctypes.POINTER(_VP), _I, _I64, _I64,
                       _I, _I, _I, _I, _VP, _VP, _VP, _VP, _VP, _SZ, _VP], _I),
@@ -234,8 +237,11 @@ def score(cls_attn: Optional[torch.Tensor], feats: Sequence[torch.Tensor], n_anc
 
 def select(cluster: torch.Tensor, s: torch.Tensor, n_anchor: int, n_cmp: int, K: int = 4,
            quota_mode: int = 0, cap: Optional[int] = None, tiles_per_sample: int = 1,
-           src: Optional[torch.Tensor] = None, text: Optional[torch.Tensor] = None):
-    """Quotas + selection (+ optional assembly of [kept visual | text] rows)."""
+           src: Optional[torch.Tensor] = None, text: Optional[torch.Tensor] = None,
+           text_only: bool = False, x_out: Optional[torch.Tensor] = None):
+    """Quotas + selection (+ optional assembly of [kept visual | text] rows).  With
+    text_only (and text given, src None) only the text rows and the boundaries are
+    placed; spider_project_kept then writes the kept rows."""
     G, n = cluster.shape
     dev = cluster.device
     if cap is None:
@@ -245,18 +251,41 @@ def select(cluster: torch.Tensor, s: torch.Tensor, n_anchor: int, n_cmp: int, K:
     x = cu = None
     d_model = n_text = 0
     dt = F32
-    if src is not None:
-        d_model = src.shape[-1]
-        dt = _dt(src)
+    if src is not None or text_only:
+        ref = src if src is not None else text
+        d_model = ref.shape[-1]
+        dt = _dt(ref)
         B = G // tiles_per_sample
         n_text = 0 if text is None else text.shape[1]
-        x = torch.empty(B * (tiles_per_sample * cap + n_text), d_model, dtype=src.dtype, device=dev)
+        x = x_out if x_out is not None else torch.empty(B * (tiles_per_sample * cap + n_text), d_model,
+                                                          dtype=ref.dtype, device=dev)
         cu = torch.empty(B + 1, dtype=torch.int32, device=dev)
     _check(lib().spider_select(G, n, _ptr(cluster), _ptr(s), n_anchor, n_cmp, K, quota_mode,
                                _ptr(idx), _ptr(cnt), cap, tiles_per_sample, _ptr(src),
                                src.stride(0) if src is not None else 0, d_model, dt, _ptr(text),
                                n_text, _ptr(x), _ptr(cu), _stream(dev)))
     return {"idx": idx, "count": cnt, "x": x, "cu_seqlens": cu}
+
+
+def project_kept(sel: dict, feats: torch.Tensor, proj: dict, tiles_per_sample: int = 1, n_text: int = 0,
+                 feat_row0: int = 1, workspace: Optional[torch.Tensor] = None):
+    """Projects the kept rows of ``sel`` (from select(..., text_only=True)) into sel["x"].
+    feats [G, T, d_in]; proj = {"w1" [d_hid, d_in], "b1" [d_hid] fp32 or None, "w2", "b2"}."""
+    idx, cnt, x = sel["idx"], sel["count"], sel["x"]
+    G, cap = idx.shape
+    w1, w2 = proj["w1"], proj["w2"]
+    d_hid, d_in = w1.shape
+    d_out = w2.shape[0]
+    dev = feats.device
+    L = lib()
+    wsz = L.spider_project_kept_workspace_size(G, cap, d_hid, d_out, _dt(feats))
+    if workspace is None or workspace.numel() < wsz + 256:
+        workspace = _ws(wsz, dev)
+    _check(L.spider_project_kept(G, tiles_per_sample, cap, _ptr(idx), _ptr(cnt), _ptr(feats), feats.stride(0),
+                                 feats.stride(1), feat_row0, d_in, _ptr(w1), _ptr(proj.get("b1")), d_hid,
+                                 _ptr(w2), _ptr(proj.get("b2")), d_out, n_text, _dt(feats), _ptr(x),
+                                 _aligned(workspace), wsz, _stream(dev)))
+    return x
 
 
 def decoder_cfg(L: int, d: int, H: int, d_ff: int, dtype: int, eps: float = 1e-5,

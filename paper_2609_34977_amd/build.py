@@ -21,7 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libspider.so")
 SOURCES = ["host.cpp", "score.hip", "select.hip", "gemm.hip", "attention.hip", "prefill.hip",
-           "controller.hip", "anchor.hip"]
+           "controller.hip", "anchor.hip", "projector.hip"]
 ARCH = "gfx950"
 
 

@@ -67,6 +67,7 @@ enum KernelClass {
   KC_LENS_ADMIT,
   KC_COLMEAN,
   KC_CLS_ATTN,
+  KC_PROJECTOR,
   KC_COUNT
 };
 

@@ -9,7 +9,7 @@
 //                 membership flags for anchors and each cluster's first N_k,
 //                 and a block scan that writes the kept indices ascending.
 // assemble_kernel grid (ceil(cap/8), G + B) x 256.  Blocks y < G copy the
-//                 kept rows of tile y, blocks y >= G copy the text rows of
+//                 kept rows of tile y (when src is given), blocks y >= G copy the text rows of
 //                 sample y - G; every block derives its destination row from
 //                 the tile counts (a short serial prefix over at most G
 //                 values), block (0,0) writes cu_seqlens.  16-byte copies.
@@ -187,6 +187,7 @@ __global__ void __launch_bounds__(256) assemble_kernel(
     cu_seqlens[threadIdx.x] = (int32_t)packed_row(count, threadIdx.x * tps, tps, n_text);
   const int chunks = row_bytes / 16;
   if (y < G) {
+    if (!src) return;
     const int cnt = count[y];
     const int64_t base = packed_row(count, y, tps, n_text);
     for (int r = blockIdx.x * 8; r < min(cnt, blockIdx.x * 8 + 8); ++r) {
@@ -233,7 +234,9 @@ extern "C" spider_status spider_select(int G, int n, const int32_t* cluster, con
                  "spider_select: cap = %d is below min(n, n_anchor + n_cmp + K) = %lld", cap, need_cap);
   SPIDER_REQUIRE(tiles_per_sample >= 1 && G % tiles_per_sample == 0, SPIDER_ERR_SHAPE,
                  "spider_select: tiles_per_sample must divide G");
-  const bool assemble = src != nullptr;
+  // assembly: with src, kept rows and text rows; with x_out but no src, the
+  // text rows and boundaries only (the kept rows come from spider_project_kept)
+  const bool assemble = src != nullptr || x_out != nullptr;
   size_t esz = 0;
   if (assemble) {
     SPIDER_REQUIRE(act_dtype == SPIDER_F32 || act_dtype == SPIDER_BF16, SPIDER_ERR_INVALID_ARG,
@@ -241,7 +244,7 @@ extern "C" spider_status spider_select(int G, int n, const int32_t* cluster, con
     esz = act_dtype == SPIDER_BF16 ? 2 : 4;
     SPIDER_REQUIRE(d_model >= 8 && d_model % 8 == 0, SPIDER_ERR_UNSUPPORTED,
                    "spider_select: d_model must be a positive multiple of 8");
-    SPIDER_REQUIRE(src_stride_g >= (int64_t)n * d_model && src_stride_g % 8 == 0, SPIDER_ERR_SHAPE,
+    SPIDER_REQUIRE(!src || (src_stride_g >= (int64_t)n * d_model && src_stride_g % 8 == 0), SPIDER_ERR_SHAPE,
                    "spider_select: src_stride_g must be >= n*d_model and a multiple of 8");
     SPIDER_REQUIRE(x_out && cu_seqlens_out, SPIDER_ERR_INVALID_ARG,
                    "spider_select: assembly needs x_out and cu_seqlens_out");

@@ -1,6 +1,7 @@
 """One pass of the pruned-and-skipped prefill through the C ABI.
 
-score (GPU) -> select + assembly (GPU) -> [one device-to-host copy of the
+score (GPU) -> select + assembly (GPU) [-> projector on the kept rows (GPU)]
+-> [one device-to-host copy of the
 sample boundaries] -> skip plan (host, Algorithm 1 admission or a per-layer
 mask) -> prefill (GPU); or, with the online policy, the prefill whose
 controller scores and admits the visual rows on the device layer by layer
@@ -35,7 +36,7 @@ class SkipPolicy:
 class Pipeline:
     def __init__(self, *, G: int, n: int, K: int, keep: int, r_num: int, r_den: int,
                  kmeans_iter: int, tiles_per_sample: int, n_text: int, quota_mode: int,
-                 dec: _lib.DecoderCfg, weights, device):
+                 dec: _lib.DecoderCfg, weights, device, projector: Optional[dict] = None):
         self.G, self.n, self.K = G, n, K
         self.n_anchor, self.n_cmp = _lib.budget(keep, r_num, r_den)
         self.n_anchor = min(self.n_anchor, n)
@@ -53,6 +54,11 @@ class Pipeline:
         self.h = torch.empty(max_rows, dec.d, dtype=torch.float32, device=device)
         self.max_rows = max_rows
         self.online_ws = None
+        # projector on the kept rows (weights dict w1, b1, w2, b2 on the device): the
+        # assembly then places the text rows only and the projector writes the kept rows
+        self.projector = projector
+        self.proj_ws = None
+        self.x_buf = None
         self.cu_host = torch.empty(self.B + 1, dtype=torch.int32, pin_memory=True)
 
     def codes(self, cu: np.ndarray, policy: SkipPolicy) -> np.ndarray:
@@ -74,9 +80,25 @@ class Pipeline:
         return out
 
     def step(self, cls_attn, feats, src, text, policy: SkipPolicy):
+        """``src``: visual rows already in the decoder width [G, n, d], or, with a
+        projector, the ViT rows it reads [G, n+1, d_v] (row 0 = [CLS])."""
         sc = _lib.score(cls_attn, feats, self.n_anchor, self.K, self.kmeans_iter)
-        sel = _lib.select(sc["cluster"], sc["s"], self.n_anchor, self.n_cmp, self.K,
-                          self.quota_mode, self.cap, self.tps, src, text)
+        if self.projector is not None:
+            if self.x_buf is None:
+                self.x_buf = torch.empty(self.max_rows, self.dec.d, dtype=text.dtype, device=self.device)
+            sel = _lib.select(sc["cluster"], sc["s"], self.n_anchor, self.n_cmp, self.K,
+                              self.quota_mode, self.cap, self.tps, text=text, text_only=True,
+                              x_out=self.x_buf)
+            if self.proj_ws is None:
+                L = _lib.lib()
+                w1, w2 = self.projector["w1"], self.projector["w2"]
+                nb = L.spider_project_kept_workspace_size(self.G, self.cap, w1.shape[0], w2.shape[0],
+                                                          _lib._dt(src))
+                self.proj_ws = torch.empty(nb + 256, dtype=torch.uint8, device=self.device)
+            _lib.project_kept(sel, src, self.projector, self.tps, self.n_text, workspace=self.proj_ws)
+        else:
+            sel = _lib.select(sc["cluster"], sc["s"], self.n_anchor, self.n_cmp, self.K,
+                              self.quota_mode, self.cap, self.tps, src, text)
         self.cu_host.copy_(sel["cu_seqlens"], non_blocking=True)
         torch.cuda.current_stream(self.device).synchronize()
         cu = self.cu_host.numpy().copy()

@@ -53,3 +53,24 @@ def visual_src(w: Workload, device="cpu") -> torch.Tensor:
 def text_rows(w: Workload, device="cpu") -> torch.Tensor:
     """[B, n_text, d] text rows, appended after each sample's kept visual rows."""
     return _tensor((w.B, w.n_text, w.dec.d), w.dec.dtype, w.seed, 4001, device)
+
+
+def projector_weights(w: Workload, device="cpu") -> dict:
+    """LLaVA's two-layer projector from the ViT width to the decoder width:
+    w1 [d_model, d_v], w2 [d_model, d_model] approximately N(0, 0.02) in the
+    workload dtype, biases b1, b2 fp32 N(0, 0.02)."""
+    d_v, d = w.score.d_v, w.dec.d
+    return {"w1": _tensor((d, d_v), w.dec.dtype, w.seed, 4600, device),
+            "w2": _tensor((d, d), w.dec.dtype, w.seed, 4601, device),
+            "b1": _tensor((d,), "f32", w.seed, 4602, device).float(),
+            "b2": _tensor((d,), "f32", w.seed, 4603, device).float()}
+
+
+def projector_inputs(w: Workload, device="cpu") -> torch.Tensor:
+    """[G, n+1, d_v] ViT rows the projector reads (LLaVA takes the layer before the
+    last; row 0 = [CLS]), approximately N(0, 1) in the workload dtype."""
+    shape = (w.score.G, w.score.n + 1, w.score.d_v)
+    if w.dec.dtype == "bf16":
+        return normal_bf16(shape, w.seed, 4604, 1.0, device=device)
+    x = rng(w.seed, 50000 + 4604).standard_normal(shape).astype(np.float32)
+    return torch.from_numpy(x).to(device)
