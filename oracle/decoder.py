@@ -86,8 +86,10 @@ def attention(q, k, v, cu) -> np.ndarray:
     return out
 
 
-def layer_forward(h, w, cu, code_row, cfg, recipe="bf16", dtype=np.float64):
-    """One decoder layer over all packed rows; ``code_row`` [rows] uint8 bypass codes."""
+def layer_forward(h, w, cu, code_row, cfg, recipe="bf16", dtype=np.float64, kv=None):
+    """One decoder layer over all packed rows; ``code_row`` [rows] uint8 bypass codes.
+    ``kv`` (a list) receives this layer's keys after RoPE and values [rows, d], as
+    attention used them (every row, bypassing or not)."""
     rnd = round_bf16 if recipe == "bf16" else (lambda t: t)
     L_d, H = cfg.d, cfg.H
     dh = L_d // H
@@ -104,6 +106,8 @@ def layer_forward(h, w, cu, code_row, cfg, recipe="bf16", dtype=np.float64):
     q = f(rnd(rope(q.reshape(rows, H, dh), pos, cfg.theta)))
     k = f(rnd(rope(k.reshape(rows, H, dh), pos, cfg.theta)))
     v = f(rnd(v.reshape(rows, H, dh)))
+    if kv is not None:
+        kv.append((k.reshape(rows, L_d).copy(), v.reshape(rows, L_d).copy()))
     o = f(rnd(attention(q, k, v, cu).reshape(rows, L_d)))
     upd = o @ f(w["wo"]).T
     h = np.where(skip_attn[:, None], h, h + upd)
@@ -118,17 +122,18 @@ def layer_forward(h, w, cu, code_row, cfg, recipe="bf16", dtype=np.float64):
 
 
 def prefill(x, weights, cu_seqlens, codes, cfg, recipe="bf16", dtype=np.float64,
-            n_layers=None):
+            n_layers=None, kv=None):
     """Decoder prefill; returns the final residual stream h [rows, d] (before the final norm).
 
     ``weights`` is a list of per-layer dicts of arrays, or a callable
     ``layer -> dict`` (lets large weight sets be materialised one layer at a
-    time).  ``codes`` is [L, rows] uint8.
+    time).  ``codes`` is [L, rows] uint8.  ``kv`` (a list) receives every
+    layer's (keys after RoPE, values), the KV cache a decode step reads.
     """
     get = weights if callable(weights) else (lambda l: weights[l])
     cu = np.asarray(cu_seqlens, np.int64)
     h = np.asarray(x, dtype=dtype).copy()
     L = cfg.L if n_layers is None else n_layers
     for l in range(L):
-        h = layer_forward(h, get(l), cu, codes[l], cfg, recipe, dtype)
+        h = layer_forward(h, get(l), cu, codes[l], cfg, recipe, dtype, kv)
     return h
