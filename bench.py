@@ -56,6 +56,9 @@ def parse():
                    help="decoder mask from the online skip controller on the device (logit lens over a "
                         "32000-token unembedding, w1=3, w2=1, T_skip=20) instead of the workload's mask")
     p.add_argument("--vocab", type=int, default=32000)
+    p.add_argument("--decode", type=int, default=0,
+                   help="after the step, also time this many greedy decode steps (LM head included) over the "
+                        "KV cache of the pruned and skipped prefill; reported in the `decode` field")
     p.add_argument("--projector", action="store_true",
                    help="prune before the projector: the step also runs LLaVA's two-layer GELU projector "
                         "(ViT width -> decoder width) on the kept rows only")
@@ -229,6 +232,44 @@ def score_sweep(w, dev, args):
         torch.cuda.empty_cache()
 
 
+def decode_latency(w, pipe, out, dev, args):
+    """Greedy decoding after the step's prefill: spider_prefill_kv fills the KV cache of
+    the pruned and skipped prompt, then args.decode steps of spider_decode_step (one token
+    per sample, LM head over a vocabulary of args.vocab rows, arg max fed back through a
+    synthetic embedding table).  Reports time per decode step (HIP events around the loop)."""
+    from paper_2609_34977_amd import _lib
+    from synth.online_inputs import unembed
+    from synth.counter_rng import normal_bf16
+
+    cfg = pipe.dec
+    cu, codes = out["cu"], out["codes"]
+    rows, B = int(cu[-1]), len(cu) - 1
+    x = out["select"]["x"][:rows]
+    cap = int(max(cu[1:] - cu[:-1])) + args.decode + 1
+    kv = _lib.kv_cache(cfg, B, cap, dev)
+    wu = unembed(w.dec, args.vocab, w.seed, dev)
+    fn = torch.ones(cfg.d, dtype=torch.float32, device=dev)
+    emb = normal_bf16((args.vocab, cfg.d), w.seed, 4800, 0.02, device=dev)   # token embedding table
+    _lib.prefill_kv(cfg, None, cu, x, codes, kv, weight_table=pipe.wtable)
+    lens = (cu[1:] - cu[:-1]).astype(np.int32)
+    tok = torch.zeros(B, dtype=torch.int64, device=dev)
+    ws = _lib.decode_workspace(cfg, B, cap, args.vocab, dev)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for t in range(args.decode):
+        _, _, nxt = _lib.decode_step(cfg, None, lens + t, emb[tok], kv, fn, wu, weight_table=pipe.wtable,
+                                     workspace=ws)
+        tok = nxt.long()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.decode
+    return {"steps": args.decode, "ms_per_step": ms, "tokens_per_s": B / (ms * 1e-3), "batch": B,
+            "cache_rows_per_sample": [int(v) for v in (cu[1:] - cu[:-1])], "vocab": args.vocab,
+            "weights_bytes_per_step": 2 * (w.dec.L * (4 * w.dec.d ** 2 + 3 * w.dec.d * w.dec.d_ff)
+                                           + args.vocab * w.dec.d)}
+
+
 def colmean_sweep(dev):
     """spider_anchor_colmean over G tiles of [16, n, n] fp32 maps: time per call (HIP events
     around its two launches) and the algorithmic bytes (every map element read once, the
@@ -400,6 +441,8 @@ def main():
         "kernel_ms_per_step": {k: round(v, 4) for k, v in kernel_ms.items()},
         "launches_per_step": launches,
     }
+    if args.decode > 0:
+        res["decode"] = decode_latency(w, pipe, out, dev, args)
     if not args.no_cpu_baseline and not args.online and not args.projector:
         print("# cpu baseline", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, min(args.cpu_layers, dec.L), W)

@@ -312,10 +312,61 @@ typedef struct {
 
 size_t spider_prefill_workspace_size(const spider_decoder_cfg* cfg, int B, int rows);
 
+/* KV cache of the decoder: keys after RoPE and values of every layer, in
+ * cfg->dtype, layout [L][B][cap][d]: token at position p of sample b in layer l
+ * at ((l*B + b)*cap + p)*d.  Device memory owned by the caller. */
+typedef struct {
+  void* k;
+  void* v;
+  int cap;          /* token slots per sample */
+} spider_kv_cache;
+
 spider_status spider_prefill(const spider_decoder_cfg* cfg, const spider_layer_weights* layers,
                              int B, const int32_t* cu_seqlens, const void* x,
                              const uint8_t* codes, float* h_out,
                              void* workspace, size_t workspace_bytes, spider_stream stream);
+
+/* ------------------------------------------------------------------------
+ * spider_prefill_kv - spider_prefill that also fills the KV cache a decode
+ * step reads (the cache the pruned and skipped prefill leaves; Sec. 5 reports
+ * decode over it): for every layer and every row (also rows that bypass
+ * attention, whose keys and values later tokens still read) its key after
+ * RoPE and its value, exactly the values the prefill's attention used, at
+ * position 0.. of its sample.  Keys and values are produced in every layer,
+ * also where no prefill row is a query.  Arguments and workspace as
+ * spider_prefill, plus kv (every sample must fit: cu_seqlens[b+1] -
+ * cu_seqlens[b] <= kv->cap; bf16 cache 16-byte aligned).
+ * ------------------------------------------------------------------------ */
+spider_status spider_prefill_kv(const spider_decoder_cfg* cfg, const spider_layer_weights* layers, int B,
+                                const int32_t* cu_seqlens, const void* x, const uint8_t* codes,
+                                float* h_out, const spider_kv_cache* kv, void* workspace,
+                                size_t workspace_bytes, spider_stream stream);
+
+/* ------------------------------------------------------------------------
+ * spider_decode_step - one autoregressive step over the KV cache, then the LM
+ * head (Algorithm 1 ends with it).  Sample b's new token (input row x[b],
+ * device [B, d] in cfg->dtype) sits at position lens[b] (HOST int32 [B]:
+ * tokens already in sample b's cache, 0 <= lens[b] < kv->cap, lens[b] < 8192);
+ * it runs through every layer with nothing bypassed (same block, precision
+ * and RoPE as spider_prefill), its key and value are written into the cache
+ * at lens[b], and its query attends to cache positions 0..lens[b] (softmax and
+ * P.V in fp32).  The caller advances lens afterwards.
+ * Outputs: h_out device fp32 [B, d], the state after the last layer; with
+ * w_unembed ([V, d] in cfg->dtype, V % 64 == 0 in bf16) and final_norm (fp32
+ * [d]): logits_out (device fp32 [B, V], may be NULL) = W_unembed
+ * RMSNorm(h; final_norm) (the normalised row rounded to bf16 in the bf16
+ * path, fp32 accumulation) and next_out (device int32 [B], may be NULL) = the
+ * arg max, ties to the lowest id.  w_unembed NULL: no head (V ignored).
+ * Workspace: spider_decode_workspace_size(cfg, B, kv->cap, V) bytes (V = 0
+ * without the head).
+ * ------------------------------------------------------------------------ */
+size_t spider_decode_workspace_size(const spider_decoder_cfg* cfg, int B, int cap, int V);
+
+spider_status spider_decode_step(const spider_decoder_cfg* cfg, const spider_layer_weights* layers, int B,
+                                 const int32_t* lens, const void* x, const spider_kv_cache* kv,
+                                 const float* final_norm, const void* w_unembed, int V, float* h_out,
+                                 float* logits_out, int32_t* next_out, void* workspace,
+                                 size_t workspace_bytes, spider_stream stream);
 
 /* ------------------------------------------------------------------------
  * spider_prefill_online - spider_prefill driven by the online skip

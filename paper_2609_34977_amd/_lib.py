@@ -37,6 +37,10 @@ class LayerWeights(ctypes.Structure):
                 ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd")]
 
 
+class KVCache(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("cap", ctypes.c_int)]
+
+
 _VP, _I, _I64, _SZ, _F, _D = (ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t,
                               ctypes.c_float, ctypes.c_double)
 
@@ -65,6 +69,11 @@ _SIGS = {
     "spider_prefill_online": ([ctypes.POINTER(DecoderCfg), ctypes.POINTER(LayerWeights), _I, _VP, _VP,
                                _I, _VP, _I, _VP, _VP, _D, _D, _D, _VP, _VP, _VP, _VP, _VP, _SZ, _VP],
                               _I),
+    "spider_prefill_kv": ([ctypes.POINTER(DecoderCfg), ctypes.POINTER(LayerWeights), _I, _VP, _VP, _VP, _VP,
+                           ctypes.POINTER(KVCache), _VP, _SZ, _VP], _I),
+    "spider_decode_workspace_size": ([ctypes.POINTER(DecoderCfg), _I, _I, _I], _SZ),
+    "spider_decode_step": ([ctypes.POINTER(DecoderCfg), ctypes.POINTER(LayerWeights), _I, _VP, _VP,
+                            ctypes.POINTER(KVCache), _VP, _VP, _I, _VP, _VP, _VP, _VP, _SZ, _VP], _I),
     "spider_profile_enable": ([_I], _I),
     "spider_profile_mask": ([ctypes.c_uint32], _I),
     "spider_profile_classes": ([], _I),
@@ -363,6 +372,58 @@ def prefill_online(cfg: DecoderCfg, weights, cu_seqlens, x: torch.Tensor, n_text
                                        admit.ctypes.data if admit.size else None, _ptr(s_out),
                                        _ptr(out), _aligned(workspace), wsz, _stream(dev)))
     return out, codes, admit, s_out
+
+
+def kv_cache(cfg: DecoderCfg, B: int, cap: int, device, dtype=None):
+    """Allocates a KV cache [L][B][cap][d] (keys, values) and its descriptor."""
+    dt = dtype or (torch.bfloat16 if cfg.dtype == BF16 else torch.float32)
+    k = torch.zeros(cfg.L, B, cap, cfg.d, dtype=dt, device=device)
+    v = torch.zeros_like(k)
+    return {"k": k, "v": v, "desc": KVCache(k.data_ptr(), v.data_ptr(), cap)}
+
+
+def prefill_kv(cfg: DecoderCfg, weights, cu_seqlens, x: torch.Tensor, codes, kv: dict,
+               out: Optional[torch.Tensor] = None, weight_table=None) -> torch.Tensor:
+    """spider_prefill that also fills the KV cache ``kv`` (from kv_cache())."""
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    B = len(cu) - 1
+    rows = int(cu[-1])
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    dev = x.device
+    if out is None:
+        out = torch.empty(rows, cfg.d, dtype=torch.float32, device=dev)
+    wsz = prefill_workspace_size(cfg, B, rows)
+    ws = _ws(wsz, dev)
+    wt = weight_table if weight_table is not None else layer_weights(weights)
+    _check(lib().spider_prefill_kv(ctypes.byref(cfg), wt, B, cu.ctypes.data, _ptr(x),
+                                   c.ctypes.data if c.size else None, _ptr(out), ctypes.byref(kv["desc"]),
+                                   _aligned(ws), wsz, _stream(dev)))
+    return out
+
+
+def decode_workspace(cfg: DecoderCfg, B: int, cap: int, V: int, device) -> torch.Tensor:
+    return _ws(lib().spider_decode_workspace_size(ctypes.byref(cfg), B, cap, V), device)
+
+
+def decode_step(cfg: DecoderCfg, weights, lens, x: torch.Tensor, kv: dict, final_norm=None, w_unembed=None,
+                weight_table=None, workspace: Optional[torch.Tensor] = None):
+    """One decode step: x [B, d] new-token rows at positions lens (host ints).
+    Returns (h [B, d] fp32, logits [B, V] fp32 or None, next ids [B] int32 or None)."""
+    ln = np.ascontiguousarray(lens, dtype=np.int32)
+    B = len(ln)
+    dev = x.device
+    V = int(w_unembed.shape[0]) if w_unembed is not None else 0
+    h = torch.empty(B, cfg.d, dtype=torch.float32, device=dev)
+    logits = torch.empty(B, V, dtype=torch.float32, device=dev) if V else None
+    nxt = torch.empty(B, dtype=torch.int32, device=dev) if V else None
+    wsz = lib().spider_decode_workspace_size(ctypes.byref(cfg), B, kv["desc"].cap, V)
+    if workspace is None or workspace.numel() < wsz + 256:
+        workspace = _ws(wsz, dev)
+    wt = weight_table if weight_table is not None else layer_weights(weights)
+    _check(lib().spider_decode_step(ctypes.byref(cfg), wt, B, ln.ctypes.data, _ptr(x), ctypes.byref(kv["desc"]),
+                                    _ptr(final_norm), _ptr(w_unembed), V, _ptr(h), _ptr(logits), _ptr(nxt),
+                                    _aligned(workspace), wsz, _stream(dev)))
+    return h, logits, nxt
 
 
 # ----------------------------------------------------------------- profiler

@@ -68,6 +68,7 @@ enum KernelClass {
   KC_COLMEAN,
   KC_CLS_ATTN,
   KC_PROJECTOR,
+  KC_LM_HEAD,
   KC_COUNT
 };
 

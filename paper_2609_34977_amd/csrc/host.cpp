@@ -71,7 +71,7 @@ const char* kClassNames[KC_COUNT] = {
     "score_prep", "anchor_topk", "kmeans",   "anchor_maxsim", "score_final",
     "select",     "assemble",    "embed",    "rmsnorm",       "gemm_qkv",
     "qkv_finalize", "attention", "gemm_o",   "gemm_gateup",   "gemm_down",
-    "residual_add", "lens_prep", "gemm_lens", "lens_admit", "anchor_colmean", "cls_attention", "projector"};
+    "residual_add", "lens_prep", "gemm_lens", "lens_admit", "anchor_colmean", "cls_attention", "projector", "lm_head"};
 }  // namespace
 
 void prof_begin(int cls, hipStream_t s) {

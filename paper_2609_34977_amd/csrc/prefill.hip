@@ -290,6 +290,169 @@ __global__ void __launch_bounds__(256) qkv_finalize_kernel(
   }
 }
 
+// ------------------------------------------------------------------ KV cache and decode
+// Cache layout: keys (after RoPE) and values [L][B][cap][d] in the activation
+// dtype; token at position p of sample b in layer l at ((l*B + b)*cap + p)*d.
+
+// Copies one prefill layer's keys and values into the cache.  Values are
+// summed again from the split partials in the order the finalize kernel sums
+// them, so the cached values equal the ones the prefill's attention read.
+template <typename AT>
+__global__ void __launch_bounds__(256) kv_store_kernel(const AT* __restrict__ K, const float* __restrict__ Pv,
+                                                       int split, int64_t pstride, int d,
+                                                       const int32_t* __restrict__ row_sample,
+                                                       const int32_t* __restrict__ pos, AT* __restrict__ ck,
+                                                       AT* __restrict__ cv, int64_t layer_off, int cap) {
+  const int r = blockIdx.x;
+  const int64_t dst = layer_off + ((int64_t)row_sample[r] * cap + pos[r]) * d;
+  const AT* ks = K + (int64_t)r * d;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    ck[dst + c] = ks[c];
+    float x = 0.f;
+    for (int s = 0; s < split; ++s) x += Pv[s * pstride + (int64_t)r * d + c];
+    Act<AT>::store(cv + dst + c, x);
+  }
+}
+
+// Decode step, grid (B, 3): the new token of sample b at position lens[b].
+// Kind 0 sums the query partials and applies RoPE into Q[b]; kind 1 the key
+// (RoPE) and kind 2 the value, both written into the cache at lens[b].
+template <typename AT>
+__global__ void __launch_bounds__(256) decode_qkv_kernel(const float* __restrict__ Pq, const float* __restrict__ Pk,
+                                                         const float* __restrict__ Pv, int split, int64_t pstride,
+                                                         int d, int dh, const int32_t* __restrict__ lens,
+                                                         const float2* __restrict__ rope, AT* __restrict__ Q,
+                                                         AT* __restrict__ ck, AT* __restrict__ cv,
+                                                         int64_t layer_off, int cap) {
+  const int b = blockIdx.x, kind = blockIdx.y;
+  const float* src = (kind == 0 ? Pq : (kind == 1 ? Pk : Pv)) + (int64_t)b * d;
+  const int p = lens[b];
+  AT* dst = kind == 0 ? Q + (int64_t)b * d : (kind == 1 ? ck : cv) + layer_off + ((int64_t)b * cap + p) * d;
+  const int half = dh / 2;
+  for (int t = threadIdx.x; t < d / 2; t += 256) {
+    const int head = t / half, i = t - head * half;
+    const int c0 = head * dh + i, c1 = c0 + half;
+    float x0 = 0.f, x1 = 0.f;
+    for (int s = 0; s < split; ++s) {
+      x0 += src[s * pstride + c0];
+      x1 += src[s * pstride + c1];
+    }
+    if (kind < 2) {
+      const float2 cs = rope[(int64_t)p * half + i];
+      const float y0 = x0 * cs.x - x1 * cs.y;
+      const float y1 = x1 * cs.x + x0 * cs.y;
+      x0 = y0;
+      x1 = y1;
+    }
+    Act<AT>::store(dst + c0, x0);
+    Act<AT>::store(dst + c1, x1);
+  }
+}
+
+constexpr int kDecodeMaxKeys = 8192;
+constexpr int kDecodeMaxDh = 256;
+
+template <typename AT>
+__device__ __forceinline__ float act_load(const AT* p) {
+  if constexpr (std::is_same<AT, float>::value) return *p;
+  else return bf16_bits_to_f32(*p);
+}
+
+// grid (H, B): one query (the new token) against the cache rows 0..lens[b].
+// Logits fp32 (dot products over c ascending), softmax with the block max,
+// exponentials summed per thread in key order then in a fixed tree; P.V in
+// fp32: thread t sums keys j = g, g + G, ... (g = t / dh, G = 256 / dh) for
+// column t % dh, the G partial sums added in order, one division.
+template <typename AT>
+__global__ void __launch_bounds__(256) decode_attention_kernel(const AT* __restrict__ Q, const AT* __restrict__ ck,
+                                                               const AT* __restrict__ cv, int64_t layer_off, int cap,
+                                                               const int32_t* __restrict__ lens, int d, int dh,
+                                                               float scale, AT* __restrict__ O) {
+  __shared__ float qs[kDecodeMaxDh];
+  __shared__ float z[kDecodeMaxKeys];
+  __shared__ float red[4];
+  __shared__ float part[256];
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = lens[b] + 1;
+  for (int c = tid; c < dh; c += 256) qs[c] = act_load<AT>(Q + (int64_t)b * d + h * dh + c);
+  __syncthreads();
+  const AT* kb = ck + layer_off + (int64_t)b * cap * d + h * dh;
+  const AT* vb = cv + layer_off + (int64_t)b * cap * d + h * dh;
+  float mx = -INFINITY;
+  for (int j = tid; j < n; j += 256) {
+    const AT* kr = kb + (int64_t)j * d;
+    float acc = 0.f;
+    for (int c = 0; c < dh; ++c) acc = fmaf(qs[c], act_load<AT>(kr + c), acc);
+    const float v = acc * scale;
+    z[j] = v;
+    mx = fmaxf(mx, v);
+  }
+  mx = wave_max(mx);
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  float s = 0.f;
+  for (int j = tid; j < n; j += 256) {
+    const float e = expf(z[j] - mx);
+    z[j] = e;
+    s += e;
+  }
+  s = wave_sum(s);
+  if (lane == 0) red[wave] = s;
+  __syncthreads();
+  s = (red[0] + red[1]) + (red[2] + red[3]);
+  const int G = 256 / dh;
+  const int col = tid % dh, g = tid / dh;
+  float acc = 0.f;
+  if (g < G)
+    for (int j = g; j < n; j += G) acc = fmaf(z[j], act_load<AT>(vb + (int64_t)j * d + col), acc);
+  part[tid] = acc;
+  __syncthreads();
+  if (tid < dh) {
+    float o = part[tid];
+    for (int q = 1; q < G; ++q) o += part[q * dh + tid];
+    Act<AT>::store(O + (int64_t)b * d + h * dh + tid, __fdiv_rn(o, s));
+  }
+}
+
+// One block per row: logits = the split partials summed in order; the arg max
+// (ties to the lowest id) by a per-thread scan in id order and a fixed tree.
+__global__ void __launch_bounds__(256) logits_argmax_kernel(const float* __restrict__ P, int split, int64_t pstride,
+                                                            int V, float* __restrict__ logits,
+                                                            int32_t* __restrict__ next) {
+  __shared__ float bv[256];
+  __shared__ int bi[256];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  float best = -INFINITY;
+  int arg = 0x7fffffff;
+  for (int v = tid; v < V; v += 256) {
+    float x = 0.f;
+    for (int s = 0; s < split; ++s) x += P[s * pstride + (int64_t)b * V + v];
+    if (logits) logits[(int64_t)b * V + v] = x;
+    if (x > best) {
+      best = x;
+      arg = v;
+    }
+  }
+  bv[tid] = best;
+  bi[tid] = arg;
+  __syncthreads();
+  for (int o = 128; o >= 1; o >>= 1) {
+    if (tid < o) {
+      const float x = bv[tid + o];
+      const int i = bi[tid + o];
+      if (x > bv[tid] || (x == bv[tid] && i < bi[tid])) {
+        bv[tid] = x;
+        bi[tid] = i;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid == 0 && next) next[b] = bi[0];
+}
+
 // ------------------------------------------------------------------ host side
 struct LayerTables {
   int nA = 0, nF = 0;
@@ -407,7 +570,7 @@ struct PrefillWs {
 // Rows of the transposed V buffer: R rounded up to the 32-key blocks of attention.
 int vt_rows(int R) { return (R + 31) / 32 * 32; }
 
-size_t table_ints_bound(int L, int R) { return (size_t)R * 2 + (size_t)L * 4 * R + 64; }
+size_t table_ints_bound(int L, int R) { return (size_t)R * 3 + (size_t)L * 4 * R + 64; }
 
 struct Carver {
   char* base;
@@ -584,6 +747,11 @@ struct PrefillRun {
   hipStream_t st;
   int pend_split = 0;
   const int32_t* pend_slot = nullptr;
+  // optional KV cache output ([L][B][cap][d]) and the sample of every row
+  AT* ck = nullptr;
+  AT* cv = nullptr;
+  int kv_cap = 0, kv_B = 0;
+  const int32_t* row_sample = nullptr;
 
   bool bf16() const { return c.dtype == SPIDER_BF16; }
   int64_t pstride() const { return (int64_t)R * c.d; }
@@ -634,8 +802,10 @@ struct PrefillRun {
     AT* ob = reinterpret_cast<AT*>(ws.o);
     AT* act = reinterpret_cast<AT*>(ws.act);
     // split-K caps: the QKV partials are re-read by the finalize kernel and the
-    // O/down partials by the next norm, so splitting is kept modest
-    if (T.nA > 0) {
+    // O/down partials by the next norm, so splitting is kept modest.  With a KV
+    // cache the keys and values are produced in every layer, also where no row
+    // is a query.
+    if (T.nA > 0 || ck) {
       {
         ProfScope ps(KC_RMSNORM, st);
         launch_norm<AT>(R, h, d, ws.Pres, pend_split, ps_, pend_slot, w.attn_norm, c.eps, nullptr, 1,
@@ -645,13 +815,21 @@ struct PrefillRun {
         pend_slot = nullptr;
       }
       GemmArgs ga{};
-      ga.ngroups = 3;
       ga.K = d;
       ga.lda = d;
       ga.epilogue = EPI_PARTIAL_F32;
-      ga.g[0] = GemmGroup{xn, tab + T.offA, T.nA, w.wq, nullptr, d, ws.Pq, d, ps_, 0, 0, 0};
-      ga.g[1] = GemmGroup{xn, nullptr, R, w.wk, nullptr, d, ws.Pk, d, ps_, 0, 0, 0};
-      ga.g[2] = GemmGroup{xn, nullptr, R, w.wv, nullptr, d, ws.Pv, d, ps_, 0, 0, 0};
+      const GemmGroup gk{xn, nullptr, R, w.wk, nullptr, d, ws.Pk, d, ps_, 0, 0, 0};
+      const GemmGroup gv{xn, nullptr, R, w.wv, nullptr, d, ws.Pv, d, ps_, 0, 0, 0};
+      if (T.nA > 0) {
+        ga.ngroups = 3;
+        ga.g[0] = GemmGroup{xn, tab + T.offA, T.nA, w.wq, nullptr, d, ws.Pq, d, ps_, 0, 0, 0};
+        ga.g[1] = gk;
+        ga.g[2] = gv;
+      } else {
+        ga.ngroups = 2;
+        ga.g[0] = gk;
+        ga.g[1] = gv;
+      }
       {
         ProfScope ps(KC_GEMM_QKV, st);
         hipError_t e = gemm(ga, 2);
@@ -665,7 +843,14 @@ struct PrefillRun {
             ws.Pq, ws.Pk, ws.Pv, ga.split, ps_, T.nA, R, d, dh, tab + T.offA, dpos, ws.rope, qb, kb, vb,
             ldvt);
         SPIDER_LAUNCHED("qkv_finalize");
+        if (ck) {
+          kv_store_kernel<AT><<<R, 256, 0, st>>>(kb, ws.Pv, ga.split, ps_, d, row_sample, dpos, ck, cv,
+                                                 (int64_t)l * kv_B * kv_cap * d, kv_cap);
+          SPIDER_LAUNCHED("kv_store");
+        }
       }
+    }
+    if (T.nA > 0) {
       {
         ProfScope ps(KC_ATTENTION, st);
         AttnArgs aa{qb, tab + T.offA, kb, vb, bf16() ? (int64_t)vt_rows(R) : 0, dstart, ob, T.nA, R,
@@ -742,19 +927,30 @@ int fill_positions(int B, const int32_t* cu, int32_t* pos, int32_t* start) {
 template <typename AT>
 spider_status run_prefill(const spider_decoder_cfg& c, const spider_layer_weights* W, int B,
                           const int32_t* cu, const void* x, const uint8_t* codes, float* h,
-                          const PrefillWs& ws, hipStream_t st) {
+                          const PrefillWs& ws, hipStream_t st, const spider_kv_cache* kv = nullptr) {
   const int R = cu[B];
-  // tables: positions [R], sample starts [R], then the row lists of every layer
+  // tables: positions [R], sample starts [R], with a KV cache the sample of
+  // every row [R], then the row lists of every layer
   std::vector<int32_t> tab;
   tab.reserve(table_ints_bound(c.L, R));
-  tab.resize(2 * R);
+  tab.resize(kv ? 3 * R : 2 * R);
   const int max_s = fill_positions(B, cu, tab.data(), tab.data() + R);
+  if (kv)
+    for (int b = 0; b < B; ++b)
+      for (int r = cu[b]; r < cu[b + 1]; ++r) tab[2 * R + r] = b;
   std::vector<LayerTables> lt(c.L);
   TableBuilder tb{tab, 0};
   for (int l = 0; l < c.L; ++l) lt[l] = tb.add(codes + (size_t)l * R, R);
   SPIDER_TRY(upload_ints(tab.data(), tab.size(), ws.tables, st));
 
   PrefillRun<AT> run{c, W, h, ws, ws.tables, ws.tables, ws.tables + R, R, max_s, st};
+  if (kv) {
+    run.ck = reinterpret_cast<AT*>(kv->k);
+    run.cv = reinterpret_cast<AT*>(kv->v);
+    run.kv_cap = kv->cap;
+    run.kv_B = B;
+    run.row_sample = ws.tables + 2 * R;
+  }
   SPIDER_TRY(run.begin(x));
   for (int l = 0; l < c.L; ++l) SPIDER_TRY(run.layer(l, lt[l]));
   return run.flush();
@@ -889,6 +1085,174 @@ spider_status run_prefill_online(const spider_decoder_cfg& c, const spider_layer
   return SPIDER_OK;
 }
 
+// ------------------------------------------------------------------ decode
+constexpr int kHeadSplit = 8;
+
+struct DecodeWs {
+  PrefillWs p;     // activations and partials for B rows
+  float2* rope;    // [cap][dh/2]
+  int32_t* tab;    // identity row map [B], positions of the new tokens [B]
+  float* Plog;     // LM head partials [kHeadSplit][B][V]
+  size_t bytes;
+};
+
+DecodeWs decode_layout(const spider_decoder_cfg& c, int B, int cap, int V, char* base) {
+  Carver cv{base};
+  DecodeWs w{};
+  w.p = prefill_layout(c, B, cv);
+  const int half = c.d / c.H / 2;
+  w.rope = reinterpret_cast<float2*>(cv.take((size_t)cap * half * sizeof(float2)));
+  w.tab = reinterpret_cast<int32_t*>(cv.take((size_t)2 * B * sizeof(int32_t)));
+  w.Plog = V > 0 ? reinterpret_cast<float*>(cv.take((size_t)kHeadSplit * B * V * sizeof(float))) : nullptr;
+  w.bytes = cv.off;
+  return w;
+}
+
+// One decode step: every sample's new token (input row x[b], position lens[b])
+// runs through all layers with nothing bypassed, its key and value appended to
+// the cache; then the final norm, the LM head and the greedy choice.
+template <typename AT>
+spider_status run_decode(const spider_decoder_cfg& c, const spider_layer_weights* W, int B, const int32_t* lens,
+                         const void* x, const spider_kv_cache& kv, const float* final_norm, const void* wu, int V,
+                         float* h, float* logits, int32_t* next, const DecodeWs& ws, hipStream_t st) {
+  const bool bf16 = c.dtype == SPIDER_BF16;
+  const int d = c.d, dh = d / c.H, half = dh / 2;
+  const PrefillWs& p = ws.p;
+  std::vector<int32_t> tab(2 * B);
+  int max_pos = 0;
+  for (int b = 0; b < B; ++b) {
+    tab[b] = b;
+    tab[B + b] = lens[b];
+    max_pos = std::max(max_pos, lens[b]);
+  }
+  SPIDER_TRY(upload_ints(tab.data(), tab.size(), ws.tab, st));
+  const int32_t* ident = ws.tab;
+  const int32_t* dlens = ws.tab + B;
+  {
+    const int64_t n = (int64_t)(max_pos + 1) * half;
+    rope_table_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(ws.rope, max_pos + 1, half, dh,
+                                                                  std::log2((double)c.theta));
+    SPIDER_LAUNCHED("rope_table");
+  }
+  {
+    ProfScope ps(KC_EMBED, st);
+    const int64_t n = (int64_t)B * d;
+    embed_kernel<AT><<<(unsigned)((n + 255) / 256), 256, 0, st>>>(reinterpret_cast<const AT*>(x), h, n);
+    SPIDER_LAUNCHED("embed");
+  }
+  AT* xn = reinterpret_cast<AT*>(p.xn);
+  AT* qb = reinterpret_cast<AT*>(p.q);
+  AT* ob = reinterpret_cast<AT*>(p.o);
+  AT* act = reinterpret_cast<AT*>(p.act);
+  AT* ck = reinterpret_cast<AT*>(kv.k);
+  AT* cv = reinterpret_cast<AT*>(kv.v);
+  const int64_t ps_ = (int64_t)B * d;
+  const int sm = split_max_for_rows(B);
+  auto gemm = [&](GemmArgs& ga, int cap) {
+    const int s2 = std::min(sm, cap);
+    return bf16 ? launch_gemm_bf16(ga, s2, st) : launch_gemm_f32(ga, s2, st);
+  };
+  const float scale = (float)(1.0 / std::sqrt((double)dh));
+  int pend = 0;
+  for (int l = 0; l < c.L; ++l) {
+    const spider_layer_weights& w = W[l];
+    const int64_t loff = (int64_t)l * B * kv.cap * d;
+    {
+      ProfScope ps(KC_RMSNORM, st);
+      launch_norm<AT>(B, h, d, p.Pres, pend, ps_, pend ? ident : nullptr, w.attn_norm, c.eps, nullptr, 1, xn, st);
+      SPIDER_LAUNCHED("rmsnorm(attn)");
+      pend = 0;
+    }
+    GemmArgs ga{};
+    ga.ngroups = 3;
+    ga.K = d;
+    ga.lda = d;
+    ga.epilogue = EPI_PARTIAL_F32;
+    ga.g[0] = GemmGroup{xn, nullptr, B, w.wq, nullptr, d, p.Pq, d, ps_, 0, 0, 0};
+    ga.g[1] = GemmGroup{xn, nullptr, B, w.wk, nullptr, d, p.Pk, d, ps_, 0, 0, 0};
+    ga.g[2] = GemmGroup{xn, nullptr, B, w.wv, nullptr, d, p.Pv, d, ps_, 0, 0, 0};
+    {
+      ProfScope ps(KC_GEMM_QKV, st);
+      hipError_t e = gemm(ga, 2);
+      SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "decode gemm_qkv: %s", hipGetErrorString(e));
+    }
+    {
+      ProfScope ps(KC_QKV_FINALIZE, st);
+      decode_qkv_kernel<AT><<<dim3((unsigned)B, 3), 256, 0, st>>>(p.Pq, p.Pk, p.Pv, ga.split, ps_, d, dh, dlens,
+                                                                   ws.rope, qb, ck, cv, loff, kv.cap);
+      SPIDER_LAUNCHED("decode_qkv");
+    }
+    {
+      ProfScope ps(KC_ATTENTION, st);
+      decode_attention_kernel<AT><<<dim3((unsigned)c.H, (unsigned)B), 256, 0, st>>>(qb, ck, cv, loff, kv.cap,
+                                                                                     dlens, d, dh, scale, ob);
+      SPIDER_LAUNCHED("decode_attention");
+    }
+    GemmArgs go{};
+    go.ngroups = 1;
+    go.K = d;
+    go.lda = d;
+    go.epilogue = EPI_PARTIAL_F32;
+    go.g[0] = GemmGroup{ob, nullptr, B, w.wo, nullptr, d, p.Pres, d, ps_, 0, 0, 0};
+    {
+      ProfScope ps(KC_GEMM_O, st);
+      hipError_t e = gemm(go, 8);
+      SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "decode gemm_o: %s", hipGetErrorString(e));
+    }
+    pend = go.split;
+    {
+      ProfScope ps(KC_RMSNORM, st);
+      launch_norm<AT>(B, h, d, p.Pres, pend, ps_, ident, w.ffn_norm, c.eps, nullptr, 1, xn, st);
+      SPIDER_LAUNCHED("rmsnorm(ffn)");
+      pend = 0;
+    }
+    GemmArgs gu{};
+    gu.ngroups = 1;
+    gu.K = d;
+    gu.lda = d;
+    gu.epilogue = EPI_SWIGLU;
+    gu.g[0] = GemmGroup{xn, nullptr, B, w.wg, w.wu, c.d_ff, act, c.d_ff, 0, 0, 0, 0};
+    {
+      ProfScope ps(KC_GEMM_GATEUP, st);
+      hipError_t e = gemm(gu, 1);
+      SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "decode gemm_gateup: %s", hipGetErrorString(e));
+    }
+    GemmArgs gd{};
+    gd.ngroups = 1;
+    gd.K = c.d_ff;
+    gd.lda = c.d_ff;
+    gd.epilogue = EPI_PARTIAL_F32;
+    gd.g[0] = GemmGroup{act, nullptr, B, w.wd, nullptr, d, p.Pres, d, ps_, 0, 0, 0};
+    {
+      ProfScope ps(KC_GEMM_DOWN, st);
+      hipError_t e = gemm(gd, 8);
+      SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "decode gemm_down: %s", hipGetErrorString(e));
+    }
+    pend = gd.split;
+  }
+  {
+    ProfScope ps(KC_RESIDUAL, st);
+    launch_norm<AT>(B, h, d, p.Pres, pend, ps_, ident, nullptr, 0.f, nullptr, 0, static_cast<AT*>(nullptr), st);
+    SPIDER_LAUNCHED("residual_add");
+  }
+  if (wu) {
+    ProfScope ps(KC_LM_HEAD, st);
+    launch_norm<AT>(B, h, d, nullptr, 0, 0, nullptr, final_norm, c.eps, nullptr, 1, xn, st);
+    SPIDER_LAUNCHED("final_norm");
+    GemmArgs gh{};
+    gh.ngroups = 1;
+    gh.K = d;
+    gh.lda = d;
+    gh.epilogue = EPI_PARTIAL_F32;
+    gh.g[0] = GemmGroup{xn, nullptr, B, wu, nullptr, V, ws.Plog, V, (int64_t)B * V, 0, 0, 0};
+    hipError_t e = bf16 ? launch_gemm_bf16(gh, kHeadSplit, st) : launch_gemm_f32(gh, kHeadSplit, st);
+    SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lm head: %s", hipGetErrorString(e));
+    logits_argmax_kernel<<<B, 256, 0, st>>>(ws.Plog, gh.split, (int64_t)B * V, V, logits, next);
+    SPIDER_LAUNCHED("logits_argmax");
+  }
+  return SPIDER_OK;
+}
+
 }  // namespace
 }  // namespace spider
 
@@ -984,4 +1348,85 @@ extern "C" spider_status spider_prefill_online(
                                         h_out, ows, st);
   return run_prefill_online<float>(*cfg, layers, B, cu_seqlens, x, op, codes_out, admit_out, s_sa_out,
                                    h_out, ows, st);
+}
+
+extern "C" spider_status spider_prefill_kv(const spider_decoder_cfg* cfg, const spider_layer_weights* layers, int B,
+                                           const int32_t* cu_seqlens, const void* x, const uint8_t* codes,
+                                           float* h_out, const spider_kv_cache* kv, void* workspace,
+                                           size_t workspace_bytes, spider_stream stream) {
+  clear_error();
+  SPIDER_TRY(validate_cfg(cfg));
+  SPIDER_TRY(validate_cu(B, cu_seqlens, layers));
+  SPIDER_REQUIRE(kv && kv->k && kv->v && kv->cap >= 1, SPIDER_ERR_INVALID_ARG,
+                 "spider_prefill_kv: kv cache with k, v and cap >= 1 required");
+  for (int b = 0; b < B; ++b)
+    SPIDER_REQUIRE(cu_seqlens[b + 1] - cu_seqlens[b] <= kv->cap, SPIDER_ERR_SHAPE,
+                   "spider_prefill_kv: sample %d has more rows than the cache holds", b);
+  if (cfg->dtype == SPIDER_BF16)
+    SPIDER_REQUIRE(((uintptr_t)kv->k % 16) == 0 && ((uintptr_t)kv->v % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                   "spider_prefill_kv: cache must be 16-byte aligned");
+  const int R = cu_seqlens[B];
+  if (R == 0) return SPIDER_OK;
+  SPIDER_REQUIRE(codes, SPIDER_ERR_INVALID_ARG, "spider_prefill_kv: codes must be non-null");
+  SPIDER_TRY(validate_prefill_args(cfg, layers, x, h_out));
+  for (size_t i = 0; i < (size_t)cfg->L * R; ++i)
+    SPIDER_REQUIRE(codes[i] <= 3, SPIDER_ERR_INVALID_ARG,
+                   "spider_prefill_kv: code %u at %zu is not in [0, 3]", (unsigned)codes[i], i);
+  const PrefillWs need = prefill_layout(*cfg, R, nullptr);
+  SPIDER_REQUIRE(workspace && workspace_bytes >= need.bytes, SPIDER_ERR_WORKSPACE,
+                 "spider_prefill_kv: workspace of %zu bytes needed, %zu given", need.bytes, workspace_bytes);
+  SPIDER_REQUIRE(((uintptr_t)workspace % 256) == 0, SPIDER_ERR_WORKSPACE,
+                 "spider_prefill_kv: workspace must be 256-byte aligned");
+  const PrefillWs ws = prefill_layout(*cfg, R, reinterpret_cast<char*>(workspace));
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (cfg->dtype == SPIDER_BF16)
+    return run_prefill<uint16_t>(*cfg, layers, B, cu_seqlens, x, codes, h_out, ws, st, kv);
+  return run_prefill<float>(*cfg, layers, B, cu_seqlens, x, codes, h_out, ws, st, kv);
+}
+
+extern "C" size_t spider_decode_workspace_size(const spider_decoder_cfg* cfg, int B, int cap, int V) {
+  if (!cfg || cfg->L < 1 || cfg->d < 1 || cfg->H < 1 || cfg->d % cfg->H || B < 1 || cap < 1 || V < 0) return 0;
+  return decode_layout(*cfg, B, cap, V, nullptr).bytes;
+}
+
+extern "C" spider_status spider_decode_step(const spider_decoder_cfg* cfg, const spider_layer_weights* layers,
+                                            int B, const int32_t* lens, const void* x, const spider_kv_cache* kv,
+                                            const float* final_norm, const void* w_unembed, int V, float* h_out,
+                                            float* logits_out, int32_t* next_out, void* workspace,
+                                            size_t workspace_bytes, spider_stream stream) {
+  clear_error();
+  SPIDER_TRY(validate_cfg(cfg));
+  SPIDER_REQUIRE(B >= 1 && layers && lens, SPIDER_ERR_INVALID_ARG,
+                 "spider_decode_step: B >= 1, layers and lens required");
+  SPIDER_REQUIRE(kv && kv->k && kv->v && kv->cap >= 1, SPIDER_ERR_INVALID_ARG,
+                 "spider_decode_step: kv cache with k, v and cap >= 1 required");
+  SPIDER_REQUIRE(cfg->d / cfg->H <= kDecodeMaxDh, SPIDER_ERR_UNSUPPORTED, "spider_decode_step: dh must be <= 256");
+  for (int b = 0; b < B; ++b)
+    SPIDER_REQUIRE(lens[b] >= 0 && lens[b] < kv->cap && lens[b] + 1 <= kDecodeMaxKeys, SPIDER_ERR_SHAPE,
+                   "spider_decode_step: lens[%d] = %d outside [0, min(cap, 8192) - 1]", b, lens[b]);
+  if (w_unembed) {
+    SPIDER_REQUIRE(V >= 1 && final_norm, SPIDER_ERR_INVALID_ARG,
+                   "spider_decode_step: the LM head needs V >= 1 and final_norm");
+    SPIDER_REQUIRE(cfg->dtype != SPIDER_BF16 || V % 64 == 0, SPIDER_ERR_UNSUPPORTED,
+                   "spider_decode_step: bf16 LM head needs V a multiple of 64");
+    SPIDER_REQUIRE(((uintptr_t)w_unembed % 16) == 0 && ((uintptr_t)final_norm % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                   "spider_decode_step: w_unembed and final_norm must be 16-byte aligned");
+  }
+  SPIDER_TRY(validate_prefill_args(cfg, layers, x, h_out));
+  if (cfg->dtype == SPIDER_BF16)
+    SPIDER_REQUIRE(((uintptr_t)kv->k % 16) == 0 && ((uintptr_t)kv->v % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                   "spider_decode_step: cache must be 16-byte aligned");
+  const int Vh = w_unembed ? V : 0;
+  const DecodeWs need = decode_layout(*cfg, B, kv->cap, Vh, nullptr);
+  SPIDER_REQUIRE(workspace && workspace_bytes >= need.bytes, SPIDER_ERR_WORKSPACE,
+                 "spider_decode_step: workspace of %zu bytes needed, %zu given", need.bytes, workspace_bytes);
+  SPIDER_REQUIRE(((uintptr_t)workspace % 256) == 0, SPIDER_ERR_WORKSPACE,
+                 "spider_decode_step: workspace must be 256-byte aligned");
+  const DecodeWs ws = decode_layout(*cfg, B, kv->cap, Vh, reinterpret_cast<char*>(workspace));
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (cfg->dtype == SPIDER_BF16)
+    return run_decode<uint16_t>(*cfg, layers, B, lens, x, *kv, final_norm, w_unembed, Vh, h_out, logits_out,
+                                next_out, ws, st);
+  return run_decode<float>(*cfg, layers, B, lens, x, *kv, final_norm, w_unembed, Vh, h_out, logits_out, next_out,
+                           ws, st);
 }

@@ -289,6 +289,32 @@ def test_cls_attention_validation_before_any_hip_call(L):
     assert call(q=0x1008, dt=lib_mod.F32) == UNSUPPORTED
 
 
+def test_prefill_kv_and_decode_validation_before_any_hip_call(L):
+    bf = lib_mod.decoder_cfg(2, 4096, 32, 11008, lib_mod.BF16)
+    W = (lib_mod.LayerWeights * 2)()
+    for i in range(2):
+        W[i] = lib_mod.LayerWeights(*([0x1000] * 9))
+    cu = np.array([0, 10], np.int32)
+    codes = np.zeros((2, 10), np.uint8)
+    kv = lib_mod.KVCache(0x10000, 0x20000, 16)
+    call = lambda kvp, ws=1 << 40: L.spider_prefill_kv(ctypes.byref(bf), W, 1, cu.ctypes.data, 0x1000,
+                                                       codes.ctypes.data, 0x1000, kvp, 0x100000, ws, None)
+    assert call(None) == INVALID
+    assert call(ctypes.byref(lib_mod.KVCache(0x10000, 0x20000, 8))) == SHAPE      # sample longer than cap
+    assert call(ctypes.byref(lib_mod.KVCache(0x10008, 0x20000, 16))) == UNSUPPORTED
+    assert call(ctypes.byref(kv), ws=100) == WORKSPACE
+    dcall = lambda ln, wu=0x3000, V=32000, fn=0x4000, ws=1 << 40: L.spider_decode_step(
+        ctypes.byref(bf), W, len(ln), ln.ctypes.data, 0x1000, ctypes.byref(kv), fn, wu, V, 0x5000, None, None,
+        0x100000, ws, None)
+    assert dcall(np.array([5, 16], np.int32)) == SHAPE        # position past the cache
+    assert dcall(np.array([-1], np.int32)) == SHAPE
+    assert dcall(np.array([3], np.int32), V=32001) == UNSUPPORTED
+    assert dcall(np.array([3], np.int32), fn=None) == INVALID
+    assert dcall(np.array([3], np.int32), ws=100) == WORKSPACE
+    assert L.spider_decode_workspace_size(ctypes.byref(bf), 2, 16, 32000) > \
+        L.spider_decode_workspace_size(ctypes.byref(bf), 2, 16, 0) > 0
+
+
 def test_profiler_host_side(L):
     lib_mod.profile_enable(True)
     d = lib_mod.profile_read()
