@@ -58,7 +58,9 @@ __device__ inline TileCoord decode_tile(const GemmArgs& a, int t, int BM, int BN
   return {gi, m_tile * BM, n_tile * BN, s};
 }
 
-__device__ inline float silu(float g) { return g / (1.0f + __expf(-g)); }
+// silu(g) = g / (1 + e^-g) with the hardware reciprocal (1 ulp): the result is
+// rounded to bf16 or summed in fp32 afterwards, far coarser than that.
+__device__ inline float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 // Fields of group gi, read with constant offsets from the kernel arguments
 // (a dynamic index into the argument array would be materialised in scratch).
@@ -305,7 +307,6 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   constexpr int A_BYTES = BM * 128;
   constexpr int STAGE_BYTES = A_BYTES + 128 * 128;  // activations, then the 128 weight rows
   constexpr int PER_IT = 4 + MT;  // DMA instructions per wave per k-block: 4 weight, MT activation
-  static_assert(!DUAL || 2 * MT * 16 * 64 * 4 <= STAGES * STAGE_BYTES, "dual hand-over fits");
   __shared__ __attribute__((aligned(1024))) uint8_t ring[STAGES * STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -317,7 +318,6 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   const int kend = min(a.K, kbeg + a.k_per_split);
   const int nkb = kend > kbeg ? (kend - kbeg) / KB : 0;
   const int wrow0 = tc.n0 + 32 * (DUAL ? (wave & 1) : wave);  // first weight row of this wave
-  const int col = wrow0 + lo;                                    // this lane's output column
   const uint16_t* W = reinterpret_cast<const uint16_t*>(DUAL && wave >= 2 ? G.W2 : G.W);
   // weight DMA: instruction q fills the wave's rows 8q..8q+7; lane l takes row
   // 8q + l/8 and chunk (l%8) ^ (l/8)
@@ -390,10 +390,12 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
     __builtin_amdgcn_s_barrier();
     // EXACT: all loads issued here are consumed later, so the count holds; in
     // the remainder the compiler may drop unused weight loads, so wait for all
+    // k-block kb+LEAD goes to the slot that iteration kb-1 consumed (free since
+    // its barrier), before the MMAs of kb, so the loads overlap them
     auto body = [&](int kb, auto J, auto EXACT) {
       constexpr int j = decltype(J)::value;
-      compute(J);
       issue(min(kb + LEAD, nkb - 1), std::integral_constant<int, (j + LEAD) % STAGES>{});
+      compute(J);
       if constexpr (decltype(EXACT)::value) wait_vmcnt<(LEAD - 1) * PER_IT>();
       else wait_vmcnt<0>();
       __builtin_amdgcn_s_barrier();
@@ -410,32 +412,69 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
 
   // D layout of 32x32 MFMA: n = lane % 32, m = 8*(r/4) + 4*(lane/32) + r%4
   if constexpr (DUAL) {
-    __syncthreads();  // ring free: up waves hand their sums to the gate waves
+    // Waves 0/1 hold the gate sums of block columns [32w, 32w+32), waves 2/3 the
+    // up sums of the same columns.  Each (gate, up) pair splits the row tiles:
+    // the gate wave finishes tiles [0, MT/2), the up wave tiles [MT/2, MT),
+    // after trading the other half through LDS.  The bf16 results are staged
+    // as a BM x 64 row-major tile (pitch 72) and written with 16-byte stores,
+    // a whole 128-byte line per row.
+    constexpr int H = MT / 2;
+    constexpr int OPITCH = 72;
+    constexpr int XFER_BYTES = 4 * H * 64 * 16 * 4;
+    static_assert(MT % 2 == 0 && XFER_BYTES + BM * OPITCH * 2 <= STAGES * STAGE_BYTES, "dual epilogue fits");
+    __syncthreads();  // ring free
     float* xfer = reinterpret_cast<float*>(ring);
-    if (wave >= 2) {
+    uint16_t* ot = reinterpret_cast<uint16_t*>(ring + XFER_BYTES);
+    const int pr = wave & 1;
+    // (dir, i): dir 0 carries up tile i to the gate wave, dir 1 gate tile H + i to the up wave
+    auto slot = [&](int dir, int i) { return xfer + (((pr * 2 + dir) * H + i) * 64 + lane) * 16; };
+    auto put = [&](float* dst, const floatx16& v) {
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          *reinterpret_cast<floatx4*>(xfer + (((wave - 2) * MT + i) * 64 + lane) * 16 + 4 * v) =
-              floatx4{acc[i][4 * v], acc[i][4 * v + 1], acc[i][4 * v + 2], acc[i][4 * v + 3]};
-    }
-    __syncthreads();
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<floatx4*>(dst + 4 * q) = floatx4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+    };
     if (wave < 2) {
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
+      for (int i = 0; i < H; ++i) put(slot(1, i), acc[H + i]);
+    } else {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const floatx4 u = *reinterpret_cast<const floatx4*>(xfer + ((wave * MT + i) * 64 + lane) * 16 + 4 * v);
+      for (int i = 0; i < H; ++i) put(slot(0, i), acc[i]);
+    }
+    __syncthreads();
+    auto emit = [&](int tile, const floatx16& g, const float* u) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * v + e;
-            const int m = tc.m0 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
-            if (m < M)
-              reinterpret_cast<uint16_t*>(G.out)[(int64_t)m * G.ldo + col] =
-                  f32_to_bf16_bits(silu(acc[i][r]) * u[e]);
-          }
-        }
+      for (int r = 0; r < 16; ++r)
+        ot[(32 * tile + 8 * (r >> 2) + 4 * hi + (r & 3)) * OPITCH + 32 * pr + lo] = f32_to_bf16_bits(silu(g[r]) * u[r]);
+    };
+    if (wave < 2) {
+#pragma unroll
+      for (int i = 0; i < H; ++i) {
+        const float* up = slot(0, i);
+        float u[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) u[r] = up[r];
+        emit(i, acc[i], u);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < H; ++i) {
+        floatx16 g;
+        const float* gp = slot(1, i);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) g[r] = gp[r];
+        float u[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) u[r] = acc[H + i][r];
+        emit(H + i, g, u);
+      }
+    }
+    __syncthreads();
+    const int rows = min(BM, M - tc.m0);
+    uint16_t* op = reinterpret_cast<uint16_t*>(G.out) + (int64_t)tc.m0 * G.ldo + tc.n0;
+    for (int c = tid; c < rows * 8; c += 256) {
+      const int row = c >> 3, ch = c & 7;
+      *reinterpret_cast<u32x4*>(op + (int64_t)row * G.ldo + 8 * ch) =
+          *reinterpret_cast<const u32x4*>(ot + row * OPITCH + 8 * ch);
     }
   } else if constexpr (LENS) {
     // the block's BM x 128 logits go through LDS (row pitch 132 floats); each
@@ -487,14 +526,25 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
       *reinterpret_cast<floatx4*>(reinterpret_cast<float*>(G.out) +
                                   ((int64_t)m * G.ldo + tc.n0 / 128) * 4) = floatx4{st.m, st.s, st.t, 0.f};
   } else {
+    // fp32 partial sums go through LDS (row pitch 132 floats) so that every
+    // thread stores 16-byte pieces: 32 threads cover a 512-byte row segment
+    constexpr int PITCH = 132;
+    static_assert(BM * PITCH * 4 <= STAGES * STAGE_BYTES, "partial tile fits the ring");
+    __syncthreads();
+    float* sm = reinterpret_cast<float*>(ring);
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = tc.m0 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
-        if (m < M)
-          reinterpret_cast<float*>(G.out)[tc.s * G.sstride + (int64_t)m * G.ldo + col] = acc[i][r];
-      }
+      for (int r = 0; r < 16; ++r)
+        sm[(32 * i + 8 * (r >> 2) + 4 * hi + (r & 3)) * PITCH + 32 * wave + lo] = acc[i][r];
+    __syncthreads();
+    const int rows = min(BM, M - tc.m0);
+    float* op = reinterpret_cast<float*>(G.out) + tc.s * G.sstride + (int64_t)tc.m0 * G.ldo + tc.n0;
+    for (int c = tid; c < rows * 32; c += 256) {
+      const int row = c >> 5, ch = c & 31;
+      *reinterpret_cast<floatx4*>(op + (int64_t)row * G.ldo + 4 * ch) =
+          *reinterpret_cast<const floatx4*>(sm + row * PITCH + 4 * ch);
+    }
   }
 }
 
@@ -632,8 +682,13 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
   }
   const bool dual = a.epilogue == EPI_SWIGLU;
   TileCfg tc = pick_bf16_tile(maxM, dual);
+  // the streaming kernel's epilogue stores 16-byte pieces of output rows
+  auto vec_out = [&](const GemmGroup& g) {
+    const int per16 = dual ? 8 : 4;
+    return reinterpret_cast<uintptr_t>(g.out) % 16 == 0 && g.ldo % per16 == 0 && g.split_stride % per16 == 0;
+  };
   for (int i = 0; i < a.ngroups; ++i)
-    if (a.g[i].N % tc.BN || (tc.stream && a.K % 64)) {
+    if (a.g[i].N % tc.BN || (tc.stream && (a.K % 64 || !vec_out(a.g[i])))) {
       tc = maxM <= 256 ? TileCfg{std::max(64, (maxM + 63) / 64 * 64), dual ? 32 : 64, false}
                        : TileCfg{128, dual ? 64 : 128, false};
       break;
