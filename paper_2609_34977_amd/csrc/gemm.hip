@@ -311,6 +311,12 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hi = lane >> 5, lo = lane & 31;
+  constexpr int MH = MT / 2;
+  static_assert(MT % 2 == 0, "row tiles split over two waves");
+  const int mh = wave >> 1, nh = wave & 1;
+  // row of accumulator register r of row tile i, in the block (MMA D layout:
+  // column = lane % 32, row = 8 (r / 4) + 4 (lane / 32) + r % 4)
+  auto acc_row = [&](int i, int r) { return 32 * (MH * mh + i) + 8 * (r >> 2) + 4 * hi + (r & 3); };
   const TileCoord tc = decode_tile(a, xcd_remap(blockIdx.x, a.total_tiles), BM, BN);
   const GroupView G = group_view(a, tc.gi);
   const int M = G.M;
@@ -357,29 +363,36 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
           (__attribute__((address_space(3))) void*)(ring + st * STAGE_BYTES + (wave * MT + j) * 1024), 16,
           0, 0);
   };
+  // Wave tile (2 x 2 over the block): rows [32 MH mh, 32 MH (mh + 1)) against LDS
+  // weight rows [64 nh, 64 nh + 64) -- output columns n0 + 64 nh.. (dual: nh 0
+  // the gate rows, 1 the up rows of the block's 64 columns).  Accumulator
+  // 2 i + t holds row tile i and column tile t.  Per k-step a wave reads MH + 2
+  // fragments from LDS for 2 MH MMAs.
   auto compute = [&](auto S) {
     constexpr int st = decltype(S)::value;
     const uint8_t* tile = ring + st * STAGE_BYTES;
-    const uint8_t* wt = tile + A_BYTES + (32 * wave + lo) * 128;
-    bf16x8 wf[4];
+    const uint8_t* wt = tile + A_BYTES + (64 * nh + lo) * 128;
+    const uint8_t* at = tile + (32 * MH * mh + lo) * 128;
+    bf16x8 wf[2][2], af[2][MH];
+    auto frags = [&](int q, bf16x8 (&w)[2], bf16x8 (&x)[MH]) {
+      const int c = 16 * ((4 * hi + q) ^ (lo & 7));
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      wf[q] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wt + 16 * ((4 * hi + q) ^ (lo & 7))));
-    bf16x8 af[2][MT];
-    auto frags = [&](int q, bf16x8 (&dst)[MT]) {
+      for (int t = 0; t < 2; ++t)
+        w[t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wt + t * 32 * 128 + c));
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
-        dst[i] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(tile + (32 * i + lo) * 128 + 16 * ((4 * hi + q) ^ (lo & 7))));
+      for (int i = 0; i < MH; ++i)
+        x[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(at + i * 32 * 128 + c));
     };
-    frags(0, af[0]);
+    frags(0, wf[0], af[0]);
     static_for<0, 4>([&](auto Q) {
       constexpr int q = Q.value;
-      if constexpr (q + 1 < 4) frags(q + 1, af[(q + 1) & 1]);
+      if constexpr (q + 1 < 4) frags(q + 1, wf[(q + 1) & 1], af[(q + 1) & 1]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
-        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][i], wf[q], acc[i], 0, 0, 0);
+      for (int i = 0; i < MH; ++i)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+          acc[2 * i + t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][i], wf[q & 1][t], acc[2 * i + t], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     });
   };
@@ -412,60 +425,48 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
 
   // D layout of 32x32 MFMA: n = lane % 32, m = 8*(r/4) + 4*(lane/32) + r%4
   if constexpr (DUAL) {
-    // Waves 0/1 hold the gate sums of block columns [32w, 32w+32), waves 2/3 the
-    // up sums of the same columns.  Each (gate, up) pair splits the row tiles:
-    // the gate wave finishes tiles [0, MT/2), the up wave tiles [MT/2, MT),
-    // after trading the other half through LDS.  The bf16 results are staged
-    // as a BM x 64 row-major tile (pitch 72) and written with 16-byte stores,
-    // a whole 128-byte line per row.
-    constexpr int H = MT / 2;
+    // Waves (mh, 0) hold the gate sums of rows half mh, waves (mh, 1) the up sums
+    // of the same rows and columns.  Each pair splits the work by column tile:
+    // the gate wave finishes tile t = 0, the up wave t = 1, after trading the
+    // other tile through LDS.  The bf16 results are staged as a BM x 64
+    // row-major tile (pitch 72) and written with 16-byte stores, a whole
+    // 128-byte line per row.
     constexpr int OPITCH = 72;
-    constexpr int XFER_BYTES = 4 * H * 64 * 16 * 4;
-    static_assert(MT % 2 == 0 && XFER_BYTES + BM * OPITCH * 2 <= STAGES * STAGE_BYTES, "dual epilogue fits");
+    constexpr int XFER_BYTES = 4 * MH * 64 * 16 * 4;
+    static_assert(XFER_BYTES + BM * OPITCH * 2 <= STAGES * STAGE_BYTES, "dual epilogue fits");
     __syncthreads();  // ring free
     float* xfer = reinterpret_cast<float*>(ring);
     uint16_t* ot = reinterpret_cast<uint16_t*>(ring + XFER_BYTES);
-    const int pr = wave & 1;
-    // (dir, i): dir 0 carries up tile i to the gate wave, dir 1 gate tile H + i to the up wave
-    auto slot = [&](int dir, int i) { return xfer + (((pr * 2 + dir) * H + i) * 64 + lane) * 16; };
+    // (dir, i): dir 0 carries up tile (i, 0) to the gate wave, dir 1 gate tile (i, 1) to the up wave
+    auto slot = [&](int dir, int i) { return xfer + (((mh * 2 + dir) * MH + i) * 64 + lane) * 16; };
     auto put = [&](float* dst, const floatx16& v) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         *reinterpret_cast<floatx4*>(dst + 4 * q) = floatx4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
     };
-    if (wave < 2) {
+    if (nh == 0) {
 #pragma unroll
-      for (int i = 0; i < H; ++i) put(slot(1, i), acc[H + i]);
+      for (int i = 0; i < MH; ++i) put(slot(1, i), acc[2 * i + 1]);
     } else {
 #pragma unroll
-      for (int i = 0; i < H; ++i) put(slot(0, i), acc[i]);
+      for (int i = 0; i < MH; ++i) put(slot(0, i), acc[2 * i]);
     }
     __syncthreads();
-    auto emit = [&](int tile, const floatx16& g, const float* u) {
+    if (nh == 0) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        ot[(32 * tile + 8 * (r >> 2) + 4 * hi + (r & 3)) * OPITCH + 32 * pr + lo] = f32_to_bf16_bits(silu(g[r]) * u[r]);
-    };
-    if (wave < 2) {
-#pragma unroll
-      for (int i = 0; i < H; ++i) {
+      for (int i = 0; i < MH; ++i) {
         const float* up = slot(0, i);
-        float u[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) u[r] = up[r];
-        emit(i, acc[i], u);
+        for (int r = 0; r < 16; ++r)
+          ot[acc_row(i, r) * OPITCH + lo] = f32_to_bf16_bits(silu(acc[2 * i][r]) * up[r]);
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < H; ++i) {
-        floatx16 g;
+      for (int i = 0; i < MH; ++i) {
         const float* gp = slot(1, i);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) g[r] = gp[r];
-        float u[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) u[r] = acc[H + i][r];
-        emit(H + i, g, u);
+        for (int r = 0; r < 16; ++r)
+          ot[acc_row(i, r) * OPITCH + 32 + lo] = f32_to_bf16_bits(silu(gp[r]) * acc[2 * i + 1][r]);
       }
     }
     __syncthreads();
@@ -487,10 +488,11 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
     __syncthreads();
     float* sm = reinterpret_cast<float*>(ring);
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MH; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        sm[(32 * i + 8 * (r >> 2) + 4 * hi + (r & 3)) * PITCH + 32 * wave + lo] = acc[i][r];
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sm[acc_row(i, r) * PITCH + 64 * nh + 32 * t + lo] = acc[2 * i + t][r];
     __syncthreads();
     const int row = tid / TPR, part = tid % TPR;
     SoftStat st{-INFINITY, 0.f, 0.f};
@@ -533,10 +535,11 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
     __syncthreads();
     float* sm = reinterpret_cast<float*>(ring);
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MH; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        sm[(32 * i + 8 * (r >> 2) + 4 * hi + (r & 3)) * PITCH + 32 * wave + lo] = acc[i][r];
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sm[acc_row(i, r) * PITCH + 64 * nh + 32 * t + lo] = acc[2 * i + t][r];
     __syncthreads();
     const int rows = min(BM, M - tc.m0);
     float* op = reinterpret_cast<float*>(G.out) + tc.s * G.sstride + (int64_t)tc.m0 * G.ldo + tc.n0;
