@@ -307,7 +307,11 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   constexpr int A_BYTES = BM * 128;
   constexpr int STAGE_BYTES = A_BYTES + 128 * 128;  // activations, then the 128 weight rows
   constexpr int PER_IT = 4 + MT;  // DMA instructions per wave per k-block: 4 weight, MT activation
-  __shared__ __attribute__((aligned(1024))) uint8_t ring[STAGES * STAGE_BYTES];
+  // epilogue staging reuses the ring: dual hand-over + bf16 tile, or the fp32 tile (pitch 132)
+  constexpr int EPI_BYTES = DUAL ? 4 * (MT / 2) * 64 * 16 * 4 + BM * 72 * 2 : BM * 132 * 4;
+  constexpr int RING_BYTES = STAGES * STAGE_BYTES > EPI_BYTES ? STAGES * STAGE_BYTES : EPI_BYTES;
+  static_assert(RING_BYTES <= 160 * 1024, "LDS of one CU");
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[RING_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hi = lane >> 5, lo = lane & 31;
@@ -433,7 +437,7 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
     // 128-byte line per row.
     constexpr int OPITCH = 72;
     constexpr int XFER_BYTES = 4 * MH * 64 * 16 * 4;
-    static_assert(XFER_BYTES + BM * OPITCH * 2 <= STAGES * STAGE_BYTES, "dual epilogue fits");
+    static_assert(XFER_BYTES + BM * OPITCH * 2 <= RING_BYTES, "dual epilogue fits");
     __syncthreads();  // ring free
     float* xfer = reinterpret_cast<float*>(ring);
     uint16_t* ot = reinterpret_cast<uint16_t*>(ring + XFER_BYTES);
@@ -484,7 +488,7 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
     constexpr int PITCH = 132;
     constexpr int TPR = BM <= 64 ? 4 : (BM <= 128 ? 2 : 1);
     constexpr int CPT = 128 / TPR;
-    static_assert(BM * PITCH * 4 <= STAGES * STAGE_BYTES, "lens tile fits the ring");
+    static_assert(BM * PITCH * 4 <= RING_BYTES, "lens tile fits the ring");
     __syncthreads();
     float* sm = reinterpret_cast<float*>(ring);
 #pragma unroll
@@ -531,7 +535,7 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
     // fp32 partial sums go through LDS (row pitch 132 floats) so that every
     // thread stores 16-byte pieces: 32 threads cover a 512-byte row segment
     constexpr int PITCH = 132;
-    static_assert(BM * PITCH * 4 <= STAGES * STAGE_BYTES, "partial tile fits the ring");
+    static_assert(BM * PITCH * 4 <= RING_BYTES, "partial tile fits the ring");
     __syncthreads();
     float* sm = reinterpret_cast<float*>(ring);
 #pragma unroll
