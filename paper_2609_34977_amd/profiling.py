@@ -1,7 +1,13 @@
-"""Profiling helpers: HBM traffic of a kernel class from rocprofv3 counters.
+"""Profiling helpers: kernel statistics and HBM traffic from rocprofv3 output.
 
+    python -m paper_2609_34977_amd.profiling stats --csv S_kernel_stats.csv \
+        --bench-log bench.log --out profiles/NAME.md --command "..."
     python -m paper_2609_34977_amd.profiling traffic --fetch F.csv --write W.csv \
         --copy-mib 256 --kernel-class gemm_gateup --out profiles/gemm_gateup_traffic
+
+`stats` turns a `rocprofv3 --kernel-trace --stats` kernel-statistics CSV into
+a markdown table of this library's kernels (namespace spider::), sorted by
+total time, with the bench line of the same run.
 
 F.csv / W.csv are rocprofv3 counter-collection CSVs of two runs of
 `bench.py --copy-probe-mib 256` (one with `--pmc FETCH_SIZE`, one with
@@ -109,9 +115,62 @@ def traffic(args):
     print("\n".join(lines))
 
 
+def _short_name(name: str) -> str:
+    # drop the namespace and the argument list, keep template arguments
+    name = name.replace("void ", "", 1) if name.startswith("void ") else name
+    name = re.sub(r"^spider::(\(anonymous namespace\)::)?", "", name)
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return name[:i]
+    return name
+
+
+def stats(args):
+    rows = []
+    with open(args.csv) as f:
+        for r in csv.DictReader(f):
+            name = r["Name"]
+            if "spider::" not in name:
+                continue
+            rows.append((_short_name(name), int(r["Calls"]), float(r["AverageNs"]) / 1e3,
+                         float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["TotalDurationNs"]) / 1e6))
+    rows.sort(key=lambda t: -t[5])
+    lines = [f"# {args.title}", "", "Command (run from the repository root on one MI355X):", "", "```"]
+    lines += (args.command or []) + ["```", "",
+                                      "Kernels of this library (spider::), sorted by total time; the torch kernels that "
+                                      "generate the synthetic inputs once at start-up are omitted (not part of the "
+                                      "timed step).", "",
+                                      "| kernel | calls | avg us | min us | max us | total ms |",
+                                      "|---|---|---|---|---|---|"]
+    for n, c, a, mn, mx, t in rows:
+        lines.append(f"| `{n}` | {c} | {a:.2f} | {mn:.2f} | {mx:.2f} | {t:.3f} |")
+    if args.bench_log:
+        with open(args.bench_log) as f:
+            js = [ln for ln in f if ln.startswith("{")]
+        if js:
+            rec = json.loads(js[-1])
+            lines += ["", "Bench line of the profiled run:", "",
+                      f"- ms_per_step {rec['ms_per_step']:.3f}, value {rec['value']:.0f} {rec['unit']}",
+                      f"- roofline: {json.dumps(rec.get('roofline'))}"]
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     p = argparse.ArgumentParser()
     sub = p.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("--csv", required=True)
+    s.add_argument("--bench-log")
+    s.add_argument("--out", required=True)
+    s.add_argument("--title", default="rocprofv3 kernel statistics")
+    s.add_argument("--command", action="append")
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
@@ -122,6 +181,8 @@ def main():
     args = p.parse_args()
     if args.cmd == "traffic":
         traffic(args)
+    elif args.cmd == "stats":
+        stats(args)
 
 
 if __name__ == "__main__":
