@@ -555,6 +555,213 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   }
 }
 
+// ------------------------------------------------------------------ large row counts
+// gemm_tile_kernel: the compute-bound regime (more than 256 rows).  A block
+// computes BM = 64*MH rows against 256 weight rows (non-dual: 256 output
+// columns; dual: the gate and up rows of 128 output columns) over its k range,
+// in k-blocks of 64.  4 waves in 2 x 2, wave (mh, nh) owning rows
+// [32 MH mh, 32 MH (mh + 1)) and 128 weight rows: non-dual LDS weight rows
+// [128 nh, 128 nh + 128); dual output columns [64 nh, 64 nh + 64), i.e. gate
+// rows [64 nh, +64) and up rows [128 + 64 nh, +64) of the stage, so every wave
+// holds the gate and up sums of the same outputs and the SwiGLU epilogue needs
+// no exchange.  Per k-step a wave reads MH + 4 fragments from LDS for 4 MH
+// v_mfma_f32_32x32x16_bf16 (acc[i][t]: row tile i, weight tile t).
+//
+// Operands go global -> LDS by global_load_lds into two stages (BM + 256 rows
+// of 128 B each); chunk c of row r sits in slot c ^ (r & 7) as in the
+// streaming kernel.  The DMA of k-block kb+1 is issued before the MMAs of kb,
+// then the wave waits for all its loads and the block passes one barrier.
+// Row tiles entirely past M skip their MMAs; their rows read row M-1.
+//
+// Tile order: per group, split-major, then GM = 8 row tiles x all column
+// tiles in column-major groups, so that the 32 blocks one XCD runs at a time
+// (after the XCD remap) share 4 weight tiles and 8 activation tiles in its L2.
+template <int MH, bool DUAL>
+__global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
+  constexpr int KB = 64;
+  constexpr int BM = 64 * MH;
+  constexpr int A_BYTES = BM * 128;
+  constexpr int STAGE_BYTES = A_BYTES + 256 * 128;
+  constexpr int OPITCH = 136;  // dual epilogue: bf16 tile BM x 128, padded rows
+  constexpr int RING_BYTES = 2 * STAGE_BYTES > BM * OPITCH * 2 ? 2 * STAGE_BYTES : BM * OPITCH * 2;
+  static_assert(RING_BYTES <= 160 * 1024, "LDS of one CU");
+  constexpr int A_PER_WAVE = BM / 32;  // DMA instructions (8 rows each) per wave and k-block
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[RING_BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int hi = lane >> 5, lo = lane & 31;
+  const int mh = wave >> 1, nh = wave & 1;
+
+  // logical tile -> (group, split, row tile, column tile)
+  const int t = xcd_remap(blockIdx.x, a.total_tiles);
+  int gi = 0;
+  if (a.ngroups > 1 && t >= a.g[1].tile_begin) gi = 1;
+  if (a.ngroups > 2 && t >= a.g[2].tile_begin) gi = 2;
+  const GroupView G = group_view(a, gi);
+  const int tm = sel3(gi, a.g[0].tiles_m, a.g[1].tiles_m, a.g[2].tiles_m);
+  const int tn = sel3(gi, a.g[0].tiles_n, a.g[1].tiles_n, a.g[2].tiles_n);
+  int local = t - sel3(gi, a.g[0].tile_begin, a.g[1].tile_begin, a.g[2].tile_begin);
+  const int s = local / (tm * tn);
+  local -= s * tm * tn;
+  constexpr int GM = 8;
+  const int grp = local / (GM * tn);
+  const int first_m = grp * GM;
+  const int gm = min(tm - first_m, GM);
+  const int within = local - grp * GM * tn;
+  const int m0 = (first_m + within % gm) * BM;
+  const int n0 = (within / gm) * (DUAL ? 128 : 256);  // first output column
+
+  const int M = G.M;
+  const int kbeg = s * a.k_per_split;
+  const int kend = min(a.K, kbeg + a.k_per_split);
+  const int nkb = kend > kbeg ? (kend - kbeg) / KB : 0;
+  const int chunk = 8 * ((lane & 7) ^ (lane >> 3));
+
+  // activation DMA: instruction j of this wave fills tile rows 8g..8g+7,
+  // g = wave*A_PER_WAVE + j; lane l takes row 8g + l/8, chunk (l%8) ^ (l/8)
+  const uint16_t* pa[A_PER_WAVE];
+#pragma unroll
+  for (int j = 0; j < A_PER_WAVE; ++j) {
+    const int r = min(m0 + 8 * (wave * A_PER_WAVE + j) + (lane >> 3), M - 1);
+    const int src = G.rows ? G.rows[r] : r;
+    pa[j] = reinterpret_cast<const uint16_t*>(G.A) + (int64_t)src * a.lda + kbeg + chunk;
+  }
+  // weight DMA: instruction j of this wave fills stage weight rows 8g..8g+7, g = 8*wave + j
+  const uint16_t* pw[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int wr = 8 * (8 * wave + j) + (lane >> 3);  // 0..255
+    const uint16_t* W;
+    int row;
+    if constexpr (DUAL) {
+      W = reinterpret_cast<const uint16_t*>(wr < 128 ? G.W : G.W2);
+      row = n0 + (wr & 127);
+    } else {
+      W = reinterpret_cast<const uint16_t*>(G.W);
+      row = n0 + wr;
+    }
+    pw[j] = W + (int64_t)row * a.K + kbeg + chunk;
+  }
+
+  // row tiles of this wave that hold rows < M (the rest skip their MMAs)
+  const int live = min(MH, max(0, (M - m0 - 32 * MH * mh + 31) / 32));
+
+  floatx16 acc[MH][4];
+#pragma unroll
+  for (int i = 0; i < MH; ++i)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc[i][u] = floatx16{};
+
+  auto issue = [&](int kb, auto S) {
+    constexpr int st = decltype(S)::value;
+    uint8_t* base = ring + st * STAGE_BYTES;
+#pragma unroll
+    for (int j = 0; j < A_PER_WAVE; ++j)
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(pa[j] + kb * KB),
+                                       (__attribute__((address_space(3))) void*)(base + (wave * A_PER_WAVE + j) * 1024),
+                                       16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(pw[j] + kb * KB),
+                                       (__attribute__((address_space(3))) void*)(base + A_BYTES + (8 * wave + j) * 1024),
+                                       16, 0, 0);
+  };
+
+  // weight tile u of the wave: LDS weight rows wrow(u) .. +31
+  auto wrow = [&](int u) {
+    if constexpr (DUAL) return (u < 2 ? 64 * nh + 32 * u : 128 + 64 * nh + 32 * (u - 2));
+    else return 128 * nh + 32 * u;
+  };
+
+  auto compute = [&](auto S) {
+    constexpr int st = decltype(S)::value;
+    const uint8_t* tile = ring + st * STAGE_BYTES;
+    const uint8_t* at = tile + (32 * MH * mh + lo) * 128;
+    const uint8_t* wt = tile + A_BYTES + lo * 128;
+    bf16x8 wf[2][4], af[2][MH];
+    auto frags = [&](int q, bf16x8 (&w)[4], bf16x8 (&x)[MH]) {
+      const int c = 16 * ((4 * hi + q) ^ (lo & 7));
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        w[u] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wt + wrow(u) * 128 + c));
+#pragma unroll
+      for (int i = 0; i < MH; ++i)
+        x[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(at + i * 32 * 128 + c));
+    };
+    frags(0, wf[0], af[0]);
+    static_for<0, 4>([&](auto Q) {
+      constexpr int q = Q.value;
+      if constexpr (q + 1 < 4) frags(q + 1, wf[(q + 1) & 1], af[(q + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < MH; ++i) {
+        if (i < live) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            acc[i][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][i], wf[q & 1][u], acc[i][u], 0, 0, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+
+  if (nkb > 0) {
+    issue(0, std::integral_constant<int, 0>{});
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    auto body = [&](int kb, auto J) {
+      constexpr int j = decltype(J)::value;
+      // the next k-block (the last one again at the end) into the other stage
+      issue(min(kb + 1, nkb - 1), std::integral_constant<int, j ^ 1>{});
+      compute(J);
+      wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+    };
+    int kb = 0;
+    for (; kb + 2 <= nkb; kb += 2) {
+      body(kb, std::integral_constant<int, 0>{});
+      body(kb + 1, std::integral_constant<int, 1>{});
+    }
+    if (kb < nkb) body(kb, std::integral_constant<int, 0>{});
+  }
+
+  // D layout of the 32x32 MMA: column lane % 32, row 8 (r / 4) + 4 (lane / 32) + r % 4
+  auto acc_row = [&](int i, int r) { return 32 * (MH * mh + i) + 8 * (r >> 2) + 4 * hi + (r & 3); };
+  if constexpr (DUAL) {
+    // bf16 silu(g) * u staged as a BM x 128 tile, written as 16-byte row pieces
+    __syncthreads();
+    uint16_t* ot = reinterpret_cast<uint16_t*>(ring);
+#pragma unroll
+    for (int i = 0; i < MH; ++i)
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          ot[acc_row(i, r) * OPITCH + 64 * nh + 32 * u + lo] =
+              f32_to_bf16_bits(silu(acc[i][u][r]) * acc[i][u + 2][r]);
+    __syncthreads();
+    const int rows = min(BM, M - m0);
+    uint16_t* op = reinterpret_cast<uint16_t*>(G.out) + (int64_t)m0 * G.ldo + n0;
+    for (int c = tid; c < rows * 16; c += 256) {
+      const int row = c >> 4, ch = c & 15;
+      *reinterpret_cast<u32x4*>(op + (int64_t)row * G.ldo + 8 * ch) =
+          *reinterpret_cast<const u32x4*>(ot + row * OPITCH + 8 * ch);
+    }
+  } else {
+    // fp32 partial sums: each store instruction writes two whole 128-byte row segments
+    float* op = reinterpret_cast<float*>(G.out) + s * G.sstride;
+#pragma unroll
+    for (int i = 0; i < MH; ++i)
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + acc_row(i, r);
+          if (m < M) op[(int64_t)m * G.ldo + n0 + wrow(u) + lo] = acc[i][u][r];
+        }
+  }
+}
+
 // ------------------------------------------------------------------ fp32
 template <bool DUAL>
 __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
@@ -659,6 +866,51 @@ void launch_stream(const GemmArgs& a, hipStream_t st) {
   gemm_stream_kernel<MT, LEAD, DUAL, LENS><<<a.total_tiles, 256, 0, st>>>(a);
 }
 
+// More than 256 rows: gemm_tile_kernel when the shapes fit it (N a multiple of
+// the block's output columns, K of 64, 16-byte aligned bf16 output rows for
+// the SwiGLU epilogue).  The row tile (256, 192 or 128) minimises the number
+// of waves of blocks (one block per CU) times the cost of a block; split-K
+// only fills a grid that would leave CUs idle.
+bool tile_path_fits(const GemmArgs& a, bool dual) {
+  if (a.K % 64) return false;
+  for (int i = 0; i < a.ngroups; ++i) {
+    const GemmGroup& g = a.g[i];
+    if (g.N % (dual ? 128 : 256)) return false;
+    if (dual && (reinterpret_cast<uintptr_t>(g.out) % 16 || g.ldo % 8)) return false;
+  }
+  return true;
+}
+
+hipError_t launch_tile(GemmArgs& a, int split_max, bool dual, hipStream_t st) {
+  const int bn = dual ? 128 : 256;
+  int best_mh = 4, best_split = 1;
+  double best = 1e300;
+  for (int mh : {4, 3, 2}) {
+    const int bm = 64 * mh;
+    const int tiles = tiles_for(a, bm, bn);
+    const int split = dual ? 1 : choose_split(tiles, a.K, split_max, 64, true);
+    const double cost = (double)ceil_div(tiles * split, kTargetBlocks) * (bm + 64) / split;
+    if (cost < best) {
+      best = cost;
+      best_mh = mh;
+      best_split = split;
+    }
+  }
+  a.split = best_split;
+  a.k_per_split = ceil_div(a.K / 64, a.split) * 64;
+  fill_tiles(a, 64 * best_mh, bn);
+  if (a.total_tiles == 0) return hipSuccess;
+  switch (best_mh * 2 + (dual ? 1 : 0)) {
+    case 8: gemm_tile_kernel<4, false><<<a.total_tiles, 256, 0, st>>>(a); break;
+    case 9: gemm_tile_kernel<4, true><<<a.total_tiles, 256, 0, st>>>(a); break;
+    case 6: gemm_tile_kernel<3, false><<<a.total_tiles, 256, 0, st>>>(a); break;
+    case 7: gemm_tile_kernel<3, true><<<a.total_tiles, 256, 0, st>>>(a); break;
+    case 4: gemm_tile_kernel<2, false><<<a.total_tiles, 256, 0, st>>>(a); break;
+    default: gemm_tile_kernel<2, true><<<a.total_tiles, 256, 0, st>>>(a); break;
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
 
 int gemm_split_for(int M, int N, int K, bool dual, bool bf16, int split_max) {
@@ -688,6 +940,7 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
     return hipGetLastError();
   }
   const bool dual = a.epilogue == EPI_SWIGLU;
+  if (maxM > 256 && tile_path_fits(a, dual)) return launch_tile(a, split_max, dual, st);
   TileCfg tc = pick_bf16_tile(maxM, dual);
   // the streaming kernel's epilogue stores 16-byte pieces of output rows
   auto vec_out = [&](const GemmGroup& g) {
