@@ -27,6 +27,15 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+typedef float float2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
   constexpr int DH = 128;
   constexpr int NW = 4;
@@ -206,6 +215,252 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
     }
 }
 
+// bf16, dh = 128, many queries (attention_wide_kernel): one block of 4 waves
+// per (128 QT compacted queries, head); wave w owns QT tiles of 32 queries.
+// The 32-key blocks of K and V^T are staged once per block in LDS by DMA
+// (two stages) and shared by the four waves, so every key read serves 128 QT
+// queries (the per-query-block kernel above re-reads them per 32 queries).
+// K rows enter the tile in the order sigma(i) = i with bits 2 and 3 swapped:
+// then the S^T registers of a lane hold, for MFMA k-block u of P V, the 8
+// consecutive keys 16u + 8 hi + [0, 8), and the V^T operand is one 16-byte
+// read.  LDS chunks are swizzled (K: chunk c of row r at c ^ (r & 7), rows of
+// 256 B; V^T: c ^ ((r >> 1) & 3), rows of 64 B) so fragment reads are free of
+// bank conflicts.  Key rows past the last row read the last row (masked).  A
+// wave skips the MMAs of a key block that none of its queries can see.
+template <int QT>
+__global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(AttnArgs a) {
+  constexpr int DH = 128;
+  constexpr int KT_BYTES = 32 * 256, STAGE = KT_BYTES + 128 * 64;
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[2 * STAGE];
+  __shared__ int red[2][4];
+  const int tid = threadIdx.x, lane = tid & 63, hi = lane >> 5, lo = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = blockIdx.y;
+  const uint16_t* Q = reinterpret_cast<const uint16_t*>(a.q);
+  const uint16_t* Kp = reinterpret_cast<const uint16_t*>(a.k);
+  const uint16_t* VT = reinterpret_cast<const uint16_t*>(a.v);
+
+  int qrow[QT], qst[QT], qa[QT];
+  bool qok[QT];
+  bf16x8 qf[QT][DH / 16];
+  int wlo = 0x7FFFFFFF, whi = -1;
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    qa[t] = blockIdx.x * (128 * QT) + wave * (32 * QT) + 32 * t + lo;
+    qok[t] = qa[t] < a.nq;
+    qrow[t] = qok[t] ? a.q_rows[qa[t]] : -1;
+    qst[t] = qok[t] ? a.row_start[qrow[t]] : 0x7FFFFFFF;
+    wlo = min(wlo, qst[t]);
+    whi = max(whi, qrow[t]);
+#pragma unroll
+    for (int s = 0; s < DH / 16; ++s) {
+      u32x4 u = {0, 0, 0, 0};
+      if (qok[t]) u = *reinterpret_cast<const u32x4*>(Q + (int64_t)qa[t] * a.d + h * DH + 16 * s + 8 * hi);
+      qf[t][s] = __builtin_bit_cast(bf16x8, u);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    wlo = min(wlo, __shfl_xor(wlo, o, 64));
+    whi = max(whi, __shfl_xor(whi, o, 64));
+  }
+  wlo = __builtin_amdgcn_readfirstlane(wlo);
+  whi = __builtin_amdgcn_readfirstlane(whi);
+  // a key block [j0, j0 + 31] is fully visible to every valid query of the wave
+  // iff j0 >= wst_max and j0 + 31 <= wq_min (invalid lanes store nothing)
+  int wst_max = -1, wq_min = 0x7FFFFFFF;
+#pragma unroll
+  for (int t = 0; t < QT; ++t)
+    if (qok[t]) {
+      wst_max = max(wst_max, qst[t]);
+      wq_min = min(wq_min, qrow[t]);
+    }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    wst_max = max(wst_max, __shfl_xor(wst_max, o, 64));
+    wq_min = min(wq_min, __shfl_xor(wq_min, o, 64));
+  }
+  wst_max = __builtin_amdgcn_readfirstlane(wst_max);
+  wq_min = __builtin_amdgcn_readfirstlane(wq_min);
+  if (lane == 0) {
+    red[0][wave] = wlo;
+    red[1][wave] = whi;
+  }
+  __syncthreads();
+  const int blo = min(min(red[0][0], red[0][1]), min(red[0][2], red[0][3]));
+  const int bhi = max(max(red[1][0], red[1][1]), max(red[1][2], red[1][3]));
+  const int jb0 = blo & ~31;
+  const int nblk = (bhi - jb0) / 32 + 1;  // every block holds at least one query
+
+  // DMA of the key block at j0 into stage S: K tile rows 4i..4i+3 and V^T rows
+  // 16i..16i+15 for i = 2 wave + e (e = 0, 1); lane l writes 16 bytes at l*16
+  auto issue = [&](int j0, auto S) {
+    constexpr int st = decltype(S)::value;
+    uint8_t* base = ring + st * STAGE;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int i = 2 * wave + e;
+      const int row = 4 * i + (lane >> 4);
+      const int sig = (row & ~12) | ((row & 4) << 1) | ((row & 8) >> 1);
+      const int key = min(j0 + sig, a.rows - 1);
+      const int c = (lane & 15) ^ (row & 7);
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(Kp + (int64_t)key * a.d + h * DH + 8 * c),
+                                       (__attribute__((address_space(3))) void*)(base + i * 1024), 16, 0, 0);
+    }
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int i = 2 * wave + e;
+      const int row = 16 * i + (lane >> 2);
+      const int c = (lane & 3) ^ ((row >> 1) & 3);
+      __builtin_amdgcn_global_load_lds(
+          reinterpret_cast<const void*>(VT + (int64_t)(h * DH + row) * a.ldvt + j0 + 8 * c),
+          (__attribute__((address_space(3))) void*)(base + KT_BYTES + i * 1024), 16, 0, 0);
+    }
+  };
+
+  const float sc = a.scale * kLog2e;
+  float m_run[QT], l_run[QT];
+  floatx16 o[QT][DH / 32];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c) o[t][c] = floatx16{};
+  }
+
+  auto compute = [&](int j0, auto S) {
+    constexpr int st = decltype(S)::value;
+    if (j0 > whi || j0 + 31 < wlo) return;
+    const uint8_t* kt = ring + st * STAGE;
+    const uint8_t* vt = kt + KT_BYTES;
+    // S^T = K Q^T: lane (query lo) holds keys j0 + 16 (r >> 3) + 8 hi + (r & 7)
+    floatx16 s[QT];
+#pragma unroll
+    for (int t = 0; t < QT; ++t) s[t] = floatx16{};
+#pragma unroll
+    for (int k = 0; k < DH / 16; ++k) {
+      const bf16x8 kf = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(kt + lo * 256 + 16 * ((2 * k + hi) ^ (lo & 7))));
+#pragma unroll
+      for (int t = 0; t < QT; ++t) s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t][k], s[t], 0, 0, 0);
+    }
+    // Online softmax on the raw scores: the scale enters the exponent through
+    // one FMA, exp2 is the hardware instruction, keys are masked only in key
+    // blocks some query of the wave cannot fully see, and the accumulators
+    // are rescaled only when some lane's running max moved.
+    const bool full = j0 >= wst_max && j0 + 31 <= wq_min;
+    bf16x8 pf[QT][2][2];
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      float mx = -INFINITY;
+      if (full) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][r]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = j0 + 16 * (r >> 3) + 8 * hi + (r & 7);
+          const bool vis = qok[t] && key >= qst[t] && key <= qrow[t];
+          s[t][r] = vis ? s[t][r] : -INFINITY;
+          mx = fmaxf(mx, s[t][r]);
+        }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run[t], mx);
+      float alpha = 1.f, sum = 0.f;
+      float p[16];
+      if (m_new == -INFINITY) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) p[r] = 0.f;
+      } else {
+        const float msc = m_new * sc;
+        alpha = __builtin_amdgcn_exp2f(fmaf(m_run[t], sc, -msc));
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          p[r] = __builtin_amdgcn_exp2f(fmaf(s[t][r], sc, -msc));
+          sum += p[r];
+        }
+      }
+      sum += __shfl_xor(sum, 32, 64);
+      l_run[t] = l_run[t] * alpha + sum;
+      m_run[t] = m_new;
+      if (__any(alpha != 1.f)) {
+#pragma unroll
+        for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[t][c][r] *= alpha;
+      }
+      // hi + lo bf16 parts of the fp32 weights (hardware round to nearest even)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        uint32_t wh[4], wl[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float a0 = p[8 * u + 2 * e], a1 = p[8 * u + 2 * e + 1];
+          wh[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(float2v{a0, a1}, bf16x2v));
+          const float2v rest{a0 - __uint_as_float(wh[e] << 16), a1 - __uint_as_float(wh[e] & 0xFFFF0000u)};
+          wl[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(rest, bf16x2v));
+        }
+        pf[t][u][0] = __builtin_bit_cast(bf16x8, u32x4{wh[0], wh[1], wh[2], wh[3]});
+        pf[t][u][1] = __builtin_bit_cast(bf16x8, u32x4{wl[0], wl[1], wl[2], wl[3]});
+      }
+    }
+    // O^T += V^T P^T: V^T operand = dh row 32c + lo, keys 16u + 8 hi + [0, 8)
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c) {
+      const int row = 32 * c + lo;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const bf16x8 vf = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(vt + row * 64 + 16 * ((2 * u + hi) ^ ((row >> 1) & 3))));
+#pragma unroll
+        for (int t = 0; t < QT; ++t) {
+          o[t][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t][u][0], o[t][c], 0, 0, 0);
+          o[t][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t][u][1], o[t][c], 0, 0, 0);
+        }
+      }
+    }
+  };
+
+  issue(jb0, std::integral_constant<int, 0>{});
+  wait_vm<0>();
+  __syncthreads();
+  auto body = [&](int bi, auto J) {
+    constexpr int j = decltype(J)::value;
+    const int nb = min(bi + 1, nblk - 1);
+    issue(jb0 + 32 * nb, std::integral_constant<int, j ^ 1>{});
+    compute(jb0 + 32 * bi, J);
+    wait_vm<0>();
+    __syncthreads();
+  };
+  int bi = 0;
+  for (; bi + 2 <= nblk; bi += 2) {
+    body(bi, std::integral_constant<int, 0>{});
+    body(bi + 1, std::integral_constant<int, 1>{});
+  }
+  if (bi < nblk) body(bi, std::integral_constant<int, 0>{});
+
+  // D layout: lane holds query lo, dh rows 32c + 8 (r / 4) + 4 hi + r % 4
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    if (!qok[t]) continue;
+    const float inv = l_run[t] > 0.f ? 1.0f / l_run[t] : 0.f;
+    uint16_t* O = reinterpret_cast<uint16_t*>(a.o) + (int64_t)qa[t] * a.d + h * DH;
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int dh0 = c * 32 + 8 * r4 + 4 * hi;
+        uint32_t w0 = (uint32_t)f32_to_bf16_bits(o[t][c][4 * r4] * inv) |
+                      ((uint32_t)f32_to_bf16_bits(o[t][c][4 * r4 + 1] * inv) << 16);
+        uint32_t w1 = (uint32_t)f32_to_bf16_bits(o[t][c][4 * r4 + 2] * inv) |
+                      ((uint32_t)f32_to_bf16_bits(o[t][c][4 * r4 + 3] * inv) << 16);
+        *reinterpret_cast<uint2*>(O + dh0) = make_uint2(w0, w1);
+      }
+  }
+}
+
 __global__ void __launch_bounds__(64) attention_f32_kernel(AttnArgs a) {
   extern __shared__ float sc[];  // [max_seq]
   const int lane = threadIdx.x;
@@ -267,8 +522,15 @@ __global__ void __launch_bounds__(64) attention_f32_kernel(AttnArgs a) {
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t st) {
   if (a.nq == 0) return hipSuccess;
   if (a.dh != 128 || a.ldvt < ((a.rows + 31) / 32) * 32 || a.ldvt % 32) return hipErrorInvalidValue;
-  dim3 grid(ceil_div(a.nq, 32), a.H);
-  attention_bf16_kernel<<<grid, 256, 0, st>>>(a);
+  // At least 128 blocks of 128 queries: the shared-tile kernel (one query tile
+  // per wave: two waves per SIMD overlap one's softmax with the other's MMAs;
+  // two tiles per wave measured 1.7x slower at one wave per SIMD).  Fewer
+  // queries: the per-32-query kernel, whose waves split the keys.
+  if ((int64_t)ceil_div(a.nq, 128) * a.H >= 128) {
+    attention_wide_kernel<1><<<dim3(ceil_div(a.nq, 128), a.H), 256, 0, st>>>(a);
+  } else {
+    attention_bf16_kernel<<<dim3(ceil_div(a.nq, 32), a.H), 256, 0, st>>>(a);
+  }
   return hipGetLastError();
 }
 

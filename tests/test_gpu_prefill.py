@@ -71,6 +71,10 @@ PARITY = {
     "7b_256_rows": ("llava15_7b", 1, [0, 256], 64, 0.3, 0.3, True),
     "7b_97_rows_dense": ("llava15_7b", 1, [0, 97], 64, 0.0, 0.0, False),
     "13b_two_samples": ("llava15_13b", 1, [0, 256, 512], 128, 0.4, 0.2, True),
+    # three ragged samples (the middle one text only) with a third of the visual
+    # rows bypassing attention: query blocks of the shared-tile attention kernel
+    # and row tiles of the large-row GEMM straddle sample boundaries
+    "7b_three_ragged_1537_rows": ("llava15_7b", 1, [0, 1000, 1037, 1537], 64, 0.35, 0.2, True),
 }
 
 
