@@ -5,6 +5,8 @@
     python -m paper_2609_34977_amd.profiling traffic --fetch F.csv --write W.csv \
         --copy-mib 256 --kernel-class gemm_gateup --out profiles/gemm_gateup_traffic
 
+`bench-table` turns bench.py JSON lines (one per workload) into a markdown
+table of step time, throughput and the dominant kernel's roofline fraction.
 `stats` turns a `rocprofv3 --kernel-trace --stats` kernel-statistics CSV into
 a markdown table of this library's kernels (namespace spider::), sorted by
 total time, with the bench line of the same run.
@@ -162,9 +164,37 @@ def stats(args):
     print("\n".join(lines))
 
 
+def bench_table(args):
+    lines = [f"# {args.title}", "", "Commands (repository root, one MI355X), one per row:", "", "```"]
+    lines += (args.command or []) + ["```", "",
+                                      "| workload | skip p | decoder rows | ms / step | prefill TFLOP / step | "
+                                      "TFLOP/s (whole step) | dominant kernel | its avg us / launch | "
+                                      "achieved | frac of peak | GEMM ms (qkv/o/gateup/down) | attention ms |",
+                                      "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    with open(args.jsonl) as f:
+        for ln in f:
+            if not ln.startswith("{"):
+                continue
+            r = json.loads(ln)
+            ro, km, c = r["roofline"], r["kernel_ms_per_step"], r["config"]
+            g = "/".join(f"{km.get(k, 0):.2f}" for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down"))
+            lines.append(f"| {c['workload']} | {c.get('skip_p')} | {c['decoder_rows']} | {r['ms_per_step']:.2f} | "
+                         f"{r['prefill_tflop_per_step']:.2f} | {r['prefill_tflop_per_step'] / r['ms_per_step'] * 1e3:.0f} | "
+                         f"{ro['kernel']} ({ro['bound']}) | {ro['avg_launch_us']:.1f} | {ro['achieved']:.0f} {ro['unit']} | "
+                         f"{ro['frac']:.3f} | {g} | {km.get('attention', 0):.2f} |")
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     p = argparse.ArgumentParser()
     sub = p.add_subparsers(dest="cmd", required=True)
+    b = sub.add_parser("bench-table")
+    b.add_argument("--jsonl", required=True)
+    b.add_argument("--out", required=True)
+    b.add_argument("--title", default="bench.py over workloads")
+    b.add_argument("--command", action="append")
     s = sub.add_parser("stats")
     s.add_argument("--csv", required=True)
     s.add_argument("--bench-log")
@@ -183,6 +213,8 @@ def main():
         traffic(args)
     elif args.cmd == "stats":
         stats(args)
+    elif args.cmd == "bench-table":
+        bench_table(args)
 
 
 if __name__ == "__main__":
