@@ -579,6 +579,17 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
 // Tile order: per group, split-major, then GM = 8 row tiles x all column
 // tiles in column-major groups, so that the 32 blocks one XCD runs at a time
 // (after the XCD remap) share 4 weight tiles and 8 activation tiles in its L2.
+// Origin (first row, first output column) of logical tile `local` of a group
+// with tm x tn tiles: groups of GM = 8 row tiles, column-major inside a group.
+__device__ __forceinline__ int2 tile_origin(int local, int tm, int tn, int BM, int BN) {
+  constexpr int GM = 8;
+  const int grp = local / (GM * tn);
+  const int first_m = grp * GM;
+  const int gm = min(tm - first_m, GM);
+  const int within = local - grp * GM * tn;
+  return make_int2((first_m + within % gm) * BM, (within / gm) * BN);
+}
+
 template <int MH, bool DUAL>
 __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
   constexpr int KB = 64;
@@ -596,28 +607,36 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
   const int hi = lane >> 5, lo = lane & 31;
   const int mh = wave >> 1, nh = wave & 1;
 
-  // logical tile -> (group, split, row tile, column tile)
-  const int t = xcd_remap(blockIdx.x, a.total_tiles);
-  int gi = 0;
-  if (a.ngroups > 1 && t >= a.g[1].tile_begin) gi = 1;
-  if (a.ngroups > 2 && t >= a.g[2].tile_begin) gi = 2;
+  // Block -> (group, split, row tile, column tile).  SwiGLU launches may
+  // start with tail pieces: blocks [0, tail_tiles * tail_split) compute piece
+  // b % tail_split of the k range of tile (total_tiles + b / tail_split), the
+  // rest the whole tiles [0, total_tiles).
+  const int n_tail = a.tail_tiles * a.tail_split;
+  const bool tail = (int)blockIdx.x < n_tail;
+  int gi = 0, s, local, kps;
+  if (tail) {
+    s = blockIdx.x % a.tail_split;
+    local = a.total_tiles + blockIdx.x / a.tail_split;
+    kps = a.tail_kps;
+  } else {
+    const int t = xcd_remap(blockIdx.x - n_tail, a.total_tiles);
+    if (a.ngroups > 1 && t >= a.g[1].tile_begin) gi = 1;
+    if (a.ngroups > 2 && t >= a.g[2].tile_begin) gi = 2;
+    const int tm = sel3(gi, a.g[0].tiles_m, a.g[1].tiles_m, a.g[2].tiles_m);
+    const int tn = sel3(gi, a.g[0].tiles_n, a.g[1].tiles_n, a.g[2].tiles_n);
+    local = t - sel3(gi, a.g[0].tile_begin, a.g[1].tile_begin, a.g[2].tile_begin);
+    s = local / (tm * tn);
+    local -= s * tm * tn;
+    kps = a.k_per_split;
+  }
   const GroupView G = group_view(a, gi);
-  const int tm = sel3(gi, a.g[0].tiles_m, a.g[1].tiles_m, a.g[2].tiles_m);
-  const int tn = sel3(gi, a.g[0].tiles_n, a.g[1].tiles_n, a.g[2].tiles_n);
-  int local = t - sel3(gi, a.g[0].tile_begin, a.g[1].tile_begin, a.g[2].tile_begin);
-  const int s = local / (tm * tn);
-  local -= s * tm * tn;
-  constexpr int GM = 8;
-  const int grp = local / (GM * tn);
-  const int first_m = grp * GM;
-  const int gm = min(tm - first_m, GM);
-  const int within = local - grp * GM * tn;
-  const int m0 = (first_m + within % gm) * BM;
-  const int n0 = (within / gm) * (DUAL ? 128 : 256);  // first output column
+  const int2 mn = tile_origin(local, sel3(gi, a.g[0].tiles_m, a.g[1].tiles_m, a.g[2].tiles_m),
+                              sel3(gi, a.g[0].tiles_n, a.g[1].tiles_n, a.g[2].tiles_n), BM, DUAL ? 128 : 256);
+  const int m0 = mn.x, n0 = mn.y;  // first row, first output column
 
   const int M = G.M;
-  const int kbeg = s * a.k_per_split;
-  const int kend = min(a.K, kbeg + a.k_per_split);
+  const int kbeg = s * kps;
+  const int kend = min(a.K, kbeg + kps);
   const int nkb = kend > kbeg ? (kend - kbeg) / KB : 0;
   const int chunk = 8 * ((lane & 7) ^ (lane >> 3));
 
@@ -742,6 +761,22 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
   // D layout of the 32x32 MMA: column lane % 32, row 8 (r / 4) + 4 (lane / 32) + r % 4
   auto acc_row = [&](int i, int r) { return 32 * (MH * mh + i) + 8 * (r >> 2) + 4 * hi + (r & 3); };
   if constexpr (DUAL) {
+    if (tail) {
+      // fp32 partial sums of piece s: scratch[s][tail tile][BM][256], gate
+      // columns 0..127 then up columns 128..255 of the tile's 128 outputs
+      float* sp = reinterpret_cast<float*>(a.scratch) +
+                  ((int64_t)s * a.tail_tiles + (local - a.total_tiles)) * BM * 256;
+#pragma unroll
+      for (int i = 0; i < MH; ++i)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = acc_row(i, r);
+            if (m0 + row < M) sp[row * 256 + (u >> 1) * 128 + 64 * nh + 32 * (u & 1) + lo] = acc[i][u][r];
+          }
+      return;
+    }
     // bf16 silu(g) * u staged as a BM x 128 tile, written as 16-byte row pieces
     __syncthreads();
     uint16_t* ot = reinterpret_cast<uint16_t*>(ring);
@@ -774,6 +809,23 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
           if (m < M) op[(int64_t)m * G.ldo + n0 + wrow(u) + lo] = acc[i][u][r];
         }
   }
+}
+
+// Tail pieces of a SwiGLU launch: gate and up summed over the pieces in
+// piece order, out = bf16(silu(g) * u).  Grid (rows of a tile, tail tiles) x 128.
+__global__ void __launch_bounds__(128) swiglu_tail_reduce_kernel(GemmArgs a, int BM) {
+  const int row = blockIdx.x, tt = blockIdx.y, c = threadIdx.x;
+  const int2 mn = tile_origin(a.total_tiles + tt, a.g[0].tiles_m, a.g[0].tiles_n, BM, 128);
+  const int m = mn.x + row;
+  if (m >= a.g[0].M) return;
+  const float* sp = reinterpret_cast<const float*>(a.scratch) + ((int64_t)tt * BM + row) * 256;
+  const int64_t piece = (int64_t)a.tail_tiles * BM * 256;
+  float g = 0.f, u = 0.f;
+  for (int s = 0; s < a.tail_split; ++s) {
+    g += sp[s * piece + c];
+    u += sp[s * piece + 128 + c];
+  }
+  reinterpret_cast<uint16_t*>(a.g[0].out)[(int64_t)m * a.g[0].ldo + mn.y + c] = f32_to_bf16_bits(silu(g) * u);
 }
 
 // ------------------------------------------------------------------ fp32
@@ -897,30 +949,59 @@ bool tile_path_fits(const GemmArgs& a, bool dual) {
 
 hipError_t launch_tile(GemmArgs& a, int split_max, bool dual, hipStream_t st) {
   const int bn = dual ? 128 : 256;
-  int best_mh = 4, best_split = 1;
+  int best_mh = 4, best_split = 1, best_tail = 0, best_ts = 0;
   double best = 1e300;
   for (int mh : {4, 3, 2}) {
     const int bm = 64 * mh;
     const int tiles = tiles_for(a, bm, bn);
     const int split = dual ? 1 : choose_split(tiles, a.K, split_max, 64, true);
-    const double cost = (double)ceil_div(tiles * split, kTargetBlocks) * (bm + 64) / split;
+    double cost = (double)ceil_div(tiles * split, kTargetBlocks) * (bm + 64) / split;
+    int tail = 0, ts = 0;
+    // SwiGLU, one group: a last wave at most a quarter full is split along k
+    // into pieces that run beside the first wave (fp32 partials in scratch)
+    const int r = tiles % kTargetBlocks;
+    if (dual && a.ngroups == 1 && tiles > kTargetBlocks && r > 0 && r <= kTargetBlocks / 4 && a.scratch) {
+      const int nkb = a.K / 64;
+      int s = std::min(16, std::min(nkb / 2, kTargetBlocks / r));
+      while (s >= 2 && (size_t)r * s * bm * 256 * 4 > a.scratch_bytes) --s;
+      if (s >= 2) {
+        const double c2 = (double)(tiles / kTargetBlocks) * (bm + 64) + (bm + 64) * (1.0 / s + 0.1);
+        if (c2 < cost) {
+          cost = c2;
+          tail = r;
+          ts = s;
+        }
+      }
+    }
     if (cost < best) {
       best = cost;
       best_mh = mh;
       best_split = split;
+      best_tail = tail;
+      best_ts = ts;
     }
   }
   a.split = best_split;
   a.k_per_split = ceil_div(a.K / 64, a.split) * 64;
   fill_tiles(a, 64 * best_mh, bn);
-  if (a.total_tiles == 0) return hipSuccess;
+  a.tail_tiles = best_tail;
+  a.tail_split = best_ts;
+  a.tail_kps = best_ts ? ceil_div(a.K / 64, best_ts) * 64 : 0;
+  a.total_tiles -= best_tail;  // whole tiles; the tail tiles follow them in logical order
+  const int blocks = a.total_tiles + best_tail * best_ts;
+  if (blocks == 0) return hipSuccess;
   switch (best_mh * 2 + (dual ? 1 : 0)) {
-    case 8: gemm_tile_kernel<4, false><<<a.total_tiles, 256, 0, st>>>(a); break;
-    case 9: gemm_tile_kernel<4, true><<<a.total_tiles, 256, 0, st>>>(a); break;
-    case 6: gemm_tile_kernel<3, false><<<a.total_tiles, 256, 0, st>>>(a); break;
-    case 7: gemm_tile_kernel<3, true><<<a.total_tiles, 256, 0, st>>>(a); break;
-    case 4: gemm_tile_kernel<2, false><<<a.total_tiles, 256, 0, st>>>(a); break;
-    default: gemm_tile_kernel<2, true><<<a.total_tiles, 256, 0, st>>>(a); break;
+    case 8: gemm_tile_kernel<4, false><<<blocks, 256, 0, st>>>(a); break;
+    case 9: gemm_tile_kernel<4, true><<<blocks, 256, 0, st>>>(a); break;
+    case 6: gemm_tile_kernel<3, false><<<blocks, 256, 0, st>>>(a); break;
+    case 7: gemm_tile_kernel<3, true><<<blocks, 256, 0, st>>>(a); break;
+    case 4: gemm_tile_kernel<2, false><<<blocks, 256, 0, st>>>(a); break;
+    default: gemm_tile_kernel<2, true><<<blocks, 256, 0, st>>>(a); break;
+  }
+  if (best_tail) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    swiglu_tail_reduce_kernel<<<dim3(64 * best_mh, best_tail), 128, 0, st>>>(a, 64 * best_mh);
   }
   return hipGetLastError();
 }

@@ -37,6 +37,13 @@ struct GemmArgs {
   int k_per_split;
   int epilogue;
   int total_tiles;
+  // Optional fp32 scratch the launcher may use (SwiGLU with more than 256 rows:
+  // the tiles of a nearly empty last wave of blocks are split along k, their
+  // gate and up partial sums go here and a reduction applies the epilogue).
+  void* scratch;
+  size_t scratch_bytes;
+  // filled by the launcher for those split tiles
+  int tail_tiles, tail_split, tail_kps;
 };
 
 // Chooses tiles and split-K for the groups (all with the same K) and launches.

@@ -887,6 +887,10 @@ struct PrefillRun {
       gu.lda = d;
       gu.epilogue = EPI_SWIGLU;
       gu.g[0] = GemmGroup{xn, nullptr, T.nF, w.wg, w.wu, c.d_ff, act, c.d_ff, 0, 0, 0, 0};
+      // the QKV partials are consumed before attention: free scratch for the
+      // GEMM's split tail tiles until the next layer's QKV GEMM
+      gu.scratch = ws.Pq;
+      gu.scratch_bytes = (size_t)split_max_for_rows(R) * R * c.d * 4;
       {
         ProfScope ps(KC_GEMM_GATEUP, st);
         hipError_t e = gemm(gu, 1);
