@@ -828,6 +828,107 @@ __global__ void __launch_bounds__(128) swiglu_tail_reduce_kernel(GemmArgs a, int
   reinterpret_cast<uint16_t*>(a.g[0].out)[(int64_t)m * a.g[0].ldo + mn.y + c] = f32_to_bf16_bits(silu(g) * u);
 }
 
+// ------------------------------------------------------------------ decode rows
+// gemv_kernel: at most 4 rows (greedy decoding, one row per sample).  The
+// GEMM is then a stream of weight rows against a few activation rows: one
+// block of 4 waves, the MB activation rows staged in LDS once (bf16), each
+// wave owning NR weight rows (SwiGLU: NR/2 outputs, their gate and up rows)
+// for the whole K.  Lane l takes the 16-byte chunks l, l + 64, ... of every
+// row (1 KB per wave instruction, non-temporal: weights are read once), four
+// chunks of each row in flight; fp32 FMAs, then one fixed-order wave sum per
+// (row, activation row).  No split-K: the fp32 output is the finished sum.
+template <int MB, bool DUAL>
+__global__ void __launch_bounds__(256) gemv_kernel(GemmArgs a) {
+  constexpr int NR = 4;                       // weight rows per wave
+  constexpr int NO = DUAL ? NR / 2 : NR;      // outputs per wave
+  constexpr int U = 4;                        // chunks of each row in flight
+  extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [MB][K]
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  int gi = 0;
+  if (a.ngroups > 1 && (int)blockIdx.x >= a.g[1].tile_begin) gi = 1;
+  if (a.ngroups > 2 && (int)blockIdx.x >= a.g[2].tile_begin) gi = 2;
+  const GroupView G = group_view(a, gi);
+  const int blk = blockIdx.x - sel3(gi, a.g[0].tile_begin, a.g[1].tile_begin, a.g[2].tile_begin);
+  const int K = a.K, K8 = K / 8;
+  // activation rows (rows past M are zero)
+  for (int c = threadIdx.x; c < MB * K8; c += 256) {
+    const int m = c / K8, k8 = c - m * K8;
+    u32x4 v = {0, 0, 0, 0};
+    if (m < G.M) {
+      const int src = G.rows ? G.rows[m] : m;
+      v = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(G.A) + (int64_t)src * a.lda + 8 * k8);
+    }
+    *reinterpret_cast<u32x4*>(xs + (int64_t)m * K + 8 * k8) = v;
+  }
+  __syncthreads();
+  const int o0 = (blk * 4 + wave) * NO;  // first output column of this wave
+  if (o0 >= G.N) return;
+  const uint16_t* wrow[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int o = min(o0 + (DUAL ? r % NO : r), G.N - 1);
+    const uint16_t* W = reinterpret_cast<const uint16_t*>(DUAL && r >= NO ? G.W2 : G.W);
+    wrow[r] = W + (int64_t)o * K;
+  }
+  float acc[NR][MB];
+#pragma unroll
+  for (int r = 0; r < NR; ++r)
+#pragma unroll
+    for (int m = 0; m < MB; ++m) acc[r][m] = 0.f;
+  for (int c0 = lane; c0 < K8; c0 += 64 * U) {
+    u32x4 wv[U][NR];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        const int c = c0 + 64 * u;
+        wv[u][r] = c < K8 ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow[r] + 8 * c))
+                          : u32x4{0, 0, 0, 0};
+      }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + 64 * u;
+      if (c >= K8) break;
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        const u32x4 xv = *reinterpret_cast<const u32x4*>(xs + (int64_t)m * K + 8 * c);
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          x[2 * e] = __uint_as_float(xv[e] << 16);
+          x[2 * e + 1] = __uint_as_float(xv[e] & 0xFFFF0000u);
+        }
+#pragma unroll
+        for (int r = 0; r < NR; ++r)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[r][m] = fmaf(__uint_as_float(wv[u][r][e] << 16), x[2 * e], acc[r][m]);
+            acc[r][m] = fmaf(__uint_as_float(wv[u][r][e] & 0xFFFF0000u), x[2 * e + 1], acc[r][m]);
+          }
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < NR; ++r)
+#pragma unroll
+    for (int m = 0; m < MB; ++m) acc[r][m] = wave_sum(acc[r][m]);
+  if (lane != 0) return;
+#pragma unroll
+  for (int q = 0; q < NO; ++q) {
+    const int o = o0 + q;
+    if (o >= G.N) break;
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      if (m >= G.M) break;
+      if constexpr (DUAL)
+        reinterpret_cast<uint16_t*>(G.out)[(int64_t)m * G.ldo + o] =
+            f32_to_bf16_bits(silu(acc[q][m]) * acc[q + NO][m]);
+      else
+        reinterpret_cast<float*>(G.out)[(int64_t)m * G.ldo + o] = acc[q][m];
+    }
+  }
+}
+
 // ------------------------------------------------------------------ fp32
 template <bool DUAL>
 __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
@@ -1006,6 +1107,31 @@ hipError_t launch_tile(GemmArgs& a, int split_max, bool dual, hipStream_t st) {
   return hipGetLastError();
 }
 
+// At most 4 rows: gemv_kernel, no split (the output holds the finished sums).
+hipError_t launch_gemv(GemmArgs& a, int maxM, bool dual, hipStream_t st) {
+  a.split = 1;
+  a.k_per_split = a.K;
+  const int per_block = 4 * (dual ? 2 : 4);  // outputs per block
+  int t = 0;
+  for (int i = 0; i < a.ngroups; ++i) {
+    a.g[i].tile_begin = t;
+    t += ceil_div(a.g[i].N, per_block);
+  }
+  a.total_tiles = t;
+  if (t == 0 || maxM == 0) return hipSuccess;
+  const int mb = maxM <= 1 ? 1 : (maxM <= 2 ? 2 : 4);
+  const size_t sh = (size_t)mb * a.K * 2;
+  switch (mb * 2 + (dual ? 1 : 0)) {
+    case 2: gemv_kernel<1, false><<<t, 256, sh, st>>>(a); break;
+    case 3: gemv_kernel<1, true><<<t, 256, sh, st>>>(a); break;
+    case 4: gemv_kernel<2, false><<<t, 256, sh, st>>>(a); break;
+    case 5: gemv_kernel<2, true><<<t, 256, sh, st>>>(a); break;
+    case 8: gemv_kernel<4, false><<<t, 256, sh, st>>>(a); break;
+    default: gemv_kernel<4, true><<<t, 256, sh, st>>>(a); break;
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
 
 int gemm_split_for(int M, int N, int K, bool dual, bool bf16, int split_max) {
@@ -1035,6 +1161,7 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
     return hipGetLastError();
   }
   const bool dual = a.epilogue == EPI_SWIGLU;
+  if (maxM <= 4 && a.K % 8 == 0 && (size_t)4 * a.K * 2 <= 160 * 1024) return launch_gemv(a, maxM, dual, st);
   if (maxM > 256 && tile_path_fits(a, dual)) return launch_tile(a, split_max, dual, st);
   TileCfg tc = pick_bf16_tile(maxM, dual);
   // the streaming kernel's epilogue stores 16-byte pieces of output rows

@@ -358,6 +358,22 @@ __device__ __forceinline__ float act_load(const AT* p) {
   else return bf16_bits_to_f32(*p);
 }
 
+// A 16-byte vector of activations as floats (8 bf16 or 4 fp32).
+template <typename AT>
+__device__ __forceinline__ void unpack16(const uint4& v, float* x) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  if constexpr (sizeof(AT) == 2) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = __uint_as_float(w[i]);
+  }
+}
+
 // grid (H, B): one query (the new token) against the cache rows 0..lens[b].
 // Logits fp32 (dot products over c ascending), softmax with the block max,
 // exponentials summed per thread in key order then in a fixed tree; P.V in
@@ -368,22 +384,40 @@ __global__ void __launch_bounds__(256) decode_attention_kernel(const AT* __restr
                                                                const AT* __restrict__ cv, int64_t layer_off, int cap,
                                                                const int32_t* __restrict__ lens, int d, int dh,
                                                                float scale, AT* __restrict__ O) {
+  // One block per (head, sample).  Scores: a thread per cached key, its row
+  // read as 16-byte vectors all in flight (dh <= 256).  P V: a thread per
+  // (group of VE columns, key group), its keys strided by the number of key
+  // groups; the key groups are combined in fixed order through LDS.
+  constexpr int VE = 16 / sizeof(AT);  // elements per 16-byte vector
   __shared__ float qs[kDecodeMaxDh];
   __shared__ float z[kDecodeMaxKeys];
   __shared__ float red[4];
-  __shared__ float part[256];
+  __shared__ float part[256 * VE];
   const int h = blockIdx.x, b = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lens[b] + 1;
+  const int nv = dh / VE;  // vectors per row
   for (int c = tid; c < dh; c += 256) qs[c] = act_load<AT>(Q + (int64_t)b * d + h * dh + c);
   __syncthreads();
   const AT* kb = ck + layer_off + (int64_t)b * cap * d + h * dh;
   const AT* vb = cv + layer_off + (int64_t)b * cap * d + h * dh;
   float mx = -INFINITY;
   for (int j = tid; j < n; j += 256) {
-    const AT* kr = kb + (int64_t)j * d;
+    const uint4* kr = reinterpret_cast<const uint4*>(kb + (int64_t)j * d);
     float acc = 0.f;
-    for (int c = 0; c < dh; ++c) acc = fmaf(qs[c], act_load<AT>(kr + c), acc);
+    for (int q0 = 0; q0 < nv; q0 += 8) {  // 8 vectors (128 B) of the row in flight
+      uint4 kv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) kv[u] = q0 + u < nv ? kr[q0 + u] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (q0 + u >= nv) break;
+        float x[VE];
+        unpack16<AT>(kv[u], x);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) acc = fmaf(qs[(q0 + u) * VE + e], x[e], acc);
+      }
+    }
     const float v = acc * scale;
     z[j] = v;
     mx = fmaxf(mx, v);
@@ -403,17 +437,40 @@ __global__ void __launch_bounds__(256) decode_attention_kernel(const AT* __restr
   if (lane == 0) red[wave] = s;
   __syncthreads();
   s = (red[0] + red[1]) + (red[2] + red[3]);
-  const int G = 256 / dh;
-  const int col = tid % dh, g = tid / dh;
-  float acc = 0.f;
-  if (g < G)
-    for (int j = g; j < n; j += G) acc = fmaf(z[j], act_load<AT>(vb + (int64_t)j * d + col), acc);
-  part[tid] = acc;
+  const int ng = 256 / nv;  // key groups
+  const int cg = tid % nv, kg = tid / nv;
+  float acc[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) acc[e] = 0.f;
+  if (kg < ng) {
+    for (int j0 = kg; j0 < n; j0 += 4 * ng) {
+      uint4 vv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = j0 + u * ng;
+        if (j < n) vv[u] = reinterpret_cast<const uint4*>(vb + (int64_t)j * d)[cg];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = j0 + u * ng;
+        if (j >= n) break;
+        float x[VE];
+        unpack16<AT>(vv[u], x);
+        const float p = z[j];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) acc[e] = fmaf(p, x[e], acc[e]);
+      }
+    }
+  }
+  if (kg < ng) {
+#pragma unroll
+    for (int e = 0; e < VE; ++e) part[kg * dh + cg * VE + e] = acc[e];
+  }
   __syncthreads();
-  if (tid < dh) {
-    float o = part[tid];
-    for (int q = 1; q < G; ++q) o += part[q * dh + tid];
-    Act<AT>::store(O + (int64_t)b * d + h * dh + tid, __fdiv_rn(o, s));
+  for (int c = tid; c < dh; c += 256) {
+    float o = part[c];
+    for (int g = 1; g < ng; ++g) o += part[g * dh + c];
+    Act<AT>::store(O + (int64_t)b * d + h * dh + c, __fdiv_rn(o, s));
   }
 }
 
@@ -427,13 +484,38 @@ __global__ void __launch_bounds__(256) logits_argmax_kernel(const float* __restr
   const int b = blockIdx.x, tid = threadIdx.x;
   float best = -INFINITY;
   int arg = 0x7fffffff;
-  for (int v = tid; v < V; v += 256) {
-    float x = 0.f;
-    for (int s = 0; s < split; ++s) x += P[s * pstride + (int64_t)b * V + v];
-    if (logits) logits[(int64_t)b * V + v] = x;
-    if (x > best) {
-      best = x;
-      arg = v;
+  if (split == 1 && V % 4 == 0) {
+    // float4 pieces 4t, 4t + 1024, ...: four in flight, ids still ascending per thread
+    const float4* P4 = reinterpret_cast<const float4*>(P + (int64_t)b * V);
+    const int V4 = V / 4;
+    for (int v0 = tid; v0 < V4; v0 += 1024) {
+      float4 x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (v0 + 256 * u < V4) x[u] = P4[v0 + 256 * u];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int v4 = v0 + 256 * u;
+        if (v4 >= V4) break;
+        if (logits) reinterpret_cast<float4*>(logits + (int64_t)b * V)[v4] = x[u];
+        const float e[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (e[k] > best) {
+            best = e[k];
+            arg = 4 * v4 + k;
+          }
+      }
+    }
+  } else {
+    for (int v = tid; v < V; v += 256) {
+      float x = 0.f;
+      for (int s = 0; s < split; ++s) x += P[s * pstride + (int64_t)b * V + v];
+      if (logits) logits[(int64_t)b * V + v] = x;
+      if (x > best) {
+        best = x;
+        arg = v;
+      }
     }
   }
   bv[tid] = best;
@@ -1405,6 +1487,11 @@ extern "C" spider_status spider_decode_step(const spider_decoder_cfg* cfg, const
   SPIDER_REQUIRE(kv && kv->k && kv->v && kv->cap >= 1, SPIDER_ERR_INVALID_ARG,
                  "spider_decode_step: kv cache with k, v and cap >= 1 required");
   SPIDER_REQUIRE(cfg->d / cfg->H <= kDecodeMaxDh, SPIDER_ERR_UNSUPPORTED, "spider_decode_step: dh must be <= 256");
+  // decode attention reads cached rows as 16-byte vectors
+  SPIDER_REQUIRE((cfg->d / cfg->H) % (cfg->dtype == SPIDER_BF16 ? 8 : 4) == 0, SPIDER_ERR_UNSUPPORTED,
+                 "spider_decode_step: dh must be a multiple of 16 bytes");
+  SPIDER_REQUIRE(((uintptr_t)kv->k % 16) == 0 && ((uintptr_t)kv->v % 16) == 0, SPIDER_ERR_UNSUPPORTED,
+                 "spider_decode_step: cache must be 16-byte aligned");
   for (int b = 0; b < B; ++b)
     SPIDER_REQUIRE(lens[b] >= 0 && lens[b] < kv->cap && lens[b] + 1 <= kDecodeMaxKeys, SPIDER_ERR_SHAPE,
                    "spider_decode_step: lens[%d] = %d outside [0, min(cap, 8192) - 1]", b, lens[b]);
