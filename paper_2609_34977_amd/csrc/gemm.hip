@@ -850,17 +850,56 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemmArgs a) {
   const GroupView G = group_view(a, gi);
   const int blk = blockIdx.x - sel3(gi, a.g[0].tile_begin, a.g[1].tile_begin, a.g[2].tile_begin);
   const int K = a.K, K8 = K / 8;
-  // activation rows (rows past M are zero)
-  for (int c = threadIdx.x; c < MB * K8; c += 256) {
-    const int m = c / K8, k8 = c - m * K8;
-    u32x4 v = {0, 0, 0, 0};
-    if (m < G.M) {
-      const int src = G.rows ? G.rows[m] : m;
-      v = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(G.A) + (int64_t)src * a.lda + 8 * k8);
+  if (a.norm_h) {
+    // rows = bf16(h * rsqrt(mean(h^2) + eps) * w), summed in the order of the
+    // RMSNorm kernel (float4 pieces tid + 256 j, wave sums, waves (0+1)+(2+3))
+    __shared__ float red[4];
+    const int K4 = K / 4;
+    for (int m = 0; m < MB; ++m) {
+      float4 v[8];
+      const float4* hr = reinterpret_cast<const float4*>(a.norm_h + (int64_t)(m < G.M ? (G.rows ? G.rows[m] : m) : 0) * K);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int c = threadIdx.x + 256 * j;
+        v[j] = (m < G.M && c < K4) ? hr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      float ss = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        ss = fmaf(v[j].x, v[j].x, fmaf(v[j].y, v[j].y, fmaf(v[j].z, v[j].z, fmaf(v[j].w, v[j].w, ss))));
+      ss = wave_sum(ss);
+      if (lane == 0) red[wave] = ss;
+      __syncthreads();
+      const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+      const float inv = 1.0f / sqrtf(tot / (float)K + a.norm_eps);
+      const float4* w4 = reinterpret_cast<const float4*>(a.norm_w);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int c = threadIdx.x + 256 * j;
+        if (c < K4) {
+          const float4 ww = w4[c];
+          uint16_t* o = xs + (int64_t)m * K + 4 * c;
+          o[0] = f32_to_bf16_bits(v[j].x * inv * ww.x);
+          o[1] = f32_to_bf16_bits(v[j].y * inv * ww.y);
+          o[2] = f32_to_bf16_bits(v[j].z * inv * ww.z);
+          o[3] = f32_to_bf16_bits(v[j].w * inv * ww.w);
+        }
+      }
+      __syncthreads();  // red is reused by the next row
     }
-    *reinterpret_cast<u32x4*>(xs + (int64_t)m * K + 8 * k8) = v;
+  } else {
+    // activation rows (rows past M are zero)
+    for (int c = threadIdx.x; c < MB * K8; c += 256) {
+      const int m = c / K8, k8 = c - m * K8;
+      u32x4 v = {0, 0, 0, 0};
+      if (m < G.M) {
+        const int src = G.rows ? G.rows[m] : m;
+        v = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(G.A) + (int64_t)src * a.lda + 8 * k8);
+      }
+      *reinterpret_cast<u32x4*>(xs + (int64_t)m * K + 8 * k8) = v;
+    }
+    __syncthreads();
   }
-  __syncthreads();
   const int o0 = (blk * 4 + wave) * NO;  // first output column of this wave
   if (o0 >= G.N) return;
   const uint16_t* wrow[NR];
@@ -923,6 +962,8 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemmArgs a) {
       if constexpr (DUAL)
         reinterpret_cast<uint16_t*>(G.out)[(int64_t)m * G.ldo + o] =
             f32_to_bf16_bits(silu(acc[q][m]) * acc[q + NO][m]);
+      else if (a.epilogue == EPI_RESIDUAL_F32)
+        reinterpret_cast<float*>(G.out)[(int64_t)m * G.ldo + o] += acc[q][m];
       else
         reinterpret_cast<float*>(G.out)[(int64_t)m * G.ldo + o] = acc[q][m];
     }
@@ -1161,7 +1202,13 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
     return hipGetLastError();
   }
   const bool dual = a.epilogue == EPI_SWIGLU;
-  if (maxM <= 4 && a.K % 8 == 0 && (size_t)4 * a.K * 2 <= 160 * 1024) return launch_gemv(a, maxM, dual, st);
+  const bool gemv_ok = maxM <= 4 && a.K % 8 == 0 && (size_t)4 * a.K * 2 <= 160 * 1024;
+  if (a.epilogue == EPI_RESIDUAL_F32 || a.norm_h) {
+    // only the decode-row kernel applies a residual epilogue or a fused norm
+    // (the norm holds a row of at most 8192 floats in registers)
+    if (!gemv_ok || (a.norm_h && (!a.norm_w || a.K > 8192))) return hipErrorInvalidValue;
+  }
+  if (gemv_ok) return launch_gemv(a, maxM, dual, st);
   if (maxM > 256 && tile_path_fits(a, dual)) return launch_tile(a, split_max, dual, st);
   TileCfg tc = pick_bf16_tile(maxM, dual);
   // the streaming kernel's epilogue stores 16-byte pieces of output rows

@@ -23,9 +23,10 @@ struct GemmGroup {
 enum GemmEpilogue {
   EPI_PARTIAL_F32 = 0,  // out fp32 [split][M][N]: this split's partial sums
   EPI_SWIGLU = 1,       // out act dtype [M][N] = silu(A W^T) * (A W2^T); split must be 1
-  EPI_LENS_STATS = 2    // out fp32 [M][N/128][4]: per row and 128-column tile of z = A W^T,
+  EPI_LENS_STATS = 2,   // out fp32 [M][N/128][4]: per row and 128-column tile of z = A W^T,
                         // (max z, sum e^(z-max), sum e^(z-max) (z-max), 0); bf16 only,
                         // M <= 256, N % 128 == 0, K % 64 == 0, no split
+  EPI_RESIDUAL_F32 = 3  // out fp32 [M][N] += A W^T; bf16, M <= 4 only (decode), no split
 };
 
 struct GemmArgs {
@@ -44,6 +45,11 @@ struct GemmArgs {
   size_t scratch_bytes;
   // filled by the launcher for those split tiles
   int tail_tiles, tail_split, tail_kps;
+  // Optional (bf16, M <= 4): A rows are RMSNorm(norm_h rows) * norm_w rounded
+  // to bf16, computed by the GEMM itself (norm_h fp32 [*, K], same row gather)
+  const float* norm_h;
+  const float* norm_w;
+  float norm_eps;
 };
 
 // Chooses tiles and split-K for the groups (all with the same K) and launches.

@@ -1239,11 +1239,15 @@ spider_status run_decode(const spider_decoder_cfg& c, const spider_layer_weights
     return bf16 ? launch_gemm_bf16(ga, s2, st) : launch_gemm_f32(ga, s2, st);
   };
   const float scale = (float)(1.0 / std::sqrt((double)dh));
+  // At most 4 bf16 rows the GEMMs run as GEMVs that normalise their own input
+  // rows (RMSNorm fused) and add O and down results straight into h: five
+  // launches per layer instead of eight, no split partials.
+  const bool fused = bf16 && B <= 4 && d <= 8192;
   int pend = 0;
   for (int l = 0; l < c.L; ++l) {
     const spider_layer_weights& w = W[l];
     const int64_t loff = (int64_t)l * B * kv.cap * d;
-    {
+    if (!fused) {
       ProfScope ps(KC_RMSNORM, st);
       launch_norm<AT>(B, h, d, p.Pres, pend, ps_, pend ? ident : nullptr, w.attn_norm, c.eps, nullptr, 1, xn, st);
       SPIDER_LAUNCHED("rmsnorm(attn)");
@@ -1257,6 +1261,11 @@ spider_status run_decode(const spider_decoder_cfg& c, const spider_layer_weights
     ga.g[0] = GemmGroup{xn, nullptr, B, w.wq, nullptr, d, p.Pq, d, ps_, 0, 0, 0};
     ga.g[1] = GemmGroup{xn, nullptr, B, w.wk, nullptr, d, p.Pk, d, ps_, 0, 0, 0};
     ga.g[2] = GemmGroup{xn, nullptr, B, w.wv, nullptr, d, p.Pv, d, ps_, 0, 0, 0};
+    if (fused) {
+      ga.norm_h = h;
+      ga.norm_w = w.attn_norm;
+      ga.norm_eps = c.eps;
+    }
     {
       ProfScope ps(KC_GEMM_QKV, st);
       hipError_t e = gemm(ga, 2);
@@ -1278,15 +1287,15 @@ spider_status run_decode(const spider_decoder_cfg& c, const spider_layer_weights
     go.ngroups = 1;
     go.K = d;
     go.lda = d;
-    go.epilogue = EPI_PARTIAL_F32;
-    go.g[0] = GemmGroup{ob, nullptr, B, w.wo, nullptr, d, p.Pres, d, ps_, 0, 0, 0};
+    go.epilogue = fused ? EPI_RESIDUAL_F32 : EPI_PARTIAL_F32;
+    go.g[0] = GemmGroup{ob, nullptr, B, w.wo, nullptr, d, fused ? (void*)h : (void*)p.Pres, d, ps_, 0, 0, 0};
     {
       ProfScope ps(KC_GEMM_O, st);
       hipError_t e = gemm(go, 8);
       SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "decode gemm_o: %s", hipGetErrorString(e));
     }
-    pend = go.split;
-    {
+    if (!fused) {
+      pend = go.split;
       ProfScope ps(KC_RMSNORM, st);
       launch_norm<AT>(B, h, d, p.Pres, pend, ps_, ident, w.ffn_norm, c.eps, nullptr, 1, xn, st);
       SPIDER_LAUNCHED("rmsnorm(ffn)");
@@ -1298,6 +1307,11 @@ spider_status run_decode(const spider_decoder_cfg& c, const spider_layer_weights
     gu.lda = d;
     gu.epilogue = EPI_SWIGLU;
     gu.g[0] = GemmGroup{xn, nullptr, B, w.wg, w.wu, c.d_ff, act, c.d_ff, 0, 0, 0, 0};
+    if (fused) {
+      gu.norm_h = h;
+      gu.norm_w = w.ffn_norm;
+      gu.norm_eps = c.eps;
+    }
     {
       ProfScope ps(KC_GEMM_GATEUP, st);
       hipError_t e = gemm(gu, 1);
@@ -1307,30 +1321,36 @@ spider_status run_decode(const spider_decoder_cfg& c, const spider_layer_weights
     gd.ngroups = 1;
     gd.K = c.d_ff;
     gd.lda = c.d_ff;
-    gd.epilogue = EPI_PARTIAL_F32;
-    gd.g[0] = GemmGroup{act, nullptr, B, w.wd, nullptr, d, p.Pres, d, ps_, 0, 0, 0};
+    gd.epilogue = fused ? EPI_RESIDUAL_F32 : EPI_PARTIAL_F32;
+    gd.g[0] = GemmGroup{act, nullptr, B, w.wd, nullptr, d, fused ? (void*)h : (void*)p.Pres, d, ps_, 0, 0, 0};
     {
       ProfScope ps(KC_GEMM_DOWN, st);
       hipError_t e = gemm(gd, 8);
       SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "decode gemm_down: %s", hipGetErrorString(e));
     }
-    pend = gd.split;
+    pend = fused ? 0 : gd.split;
   }
-  {
+  if (pend) {
     ProfScope ps(KC_RESIDUAL, st);
     launch_norm<AT>(B, h, d, p.Pres, pend, ps_, ident, nullptr, 0.f, nullptr, 0, static_cast<AT*>(nullptr), st);
     SPIDER_LAUNCHED("residual_add");
   }
   if (wu) {
     ProfScope ps(KC_LM_HEAD, st);
-    launch_norm<AT>(B, h, d, nullptr, 0, 0, nullptr, final_norm, c.eps, nullptr, 1, xn, st);
-    SPIDER_LAUNCHED("final_norm");
     GemmArgs gh{};
     gh.ngroups = 1;
     gh.K = d;
     gh.lda = d;
     gh.epilogue = EPI_PARTIAL_F32;
     gh.g[0] = GemmGroup{xn, nullptr, B, wu, nullptr, V, ws.Plog, V, (int64_t)B * V, 0, 0, 0};
+    if (fused) {
+      gh.norm_h = h;
+      gh.norm_w = final_norm;
+      gh.norm_eps = c.eps;
+    } else {
+      launch_norm<AT>(B, h, d, nullptr, 0, 0, nullptr, final_norm, c.eps, nullptr, 1, xn, st);
+      SPIDER_LAUNCHED("final_norm");
+    }
     hipError_t e = bf16 ? launch_gemm_bf16(gh, kHeadSplit, st) : launch_gemm_f32(gh, kHeadSplit, st);
     SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lm head: %s", hipGetErrorString(e));
     logits_argmax_kernel<<<B, 256, 0, st>>>(ws.Plog, gh.split, (int64_t)B * V, V, logits, next);
