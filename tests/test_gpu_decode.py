@@ -28,6 +28,12 @@ CASES = {
     # name: (workload, layers, cu_seqlens, n_text, V, steps)
     "tiny_fp32": ("tiny", 2, [0, 40, 77], 32, 1000, 3),
     "7b_two_samples": ("llava15_7b", 2, [0, 150, 342], 64, 32000, 3),
+    # one sample: the 1-row GEMVs with the fused RMSNorm and residual adds
+    "7b_one_sample": ("llava15_7b", 2, [0, 192], 64, 32000, 3),
+    # three samples: the 4-row GEMVs with one zero-padded row
+    "7b_three_samples": ("llava15_7b", 2, [0, 100, 180, 290], 64, 32000, 2),
+    # five samples: more than 4 rows, split-K GEMMs with separate norm kernels
+    "7b_five_samples": ("llava15_7b", 1, [0, 70, 140, 210, 280, 350], 64, 32000, 2),
 }
 
 
