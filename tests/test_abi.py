@@ -311,6 +311,16 @@ def test_prefill_kv_and_decode_validation_before_any_hip_call(L):
     assert dcall(np.array([3], np.int32), V=32001) == UNSUPPORTED
     assert dcall(np.array([3], np.int32), fn=None) == INVALID
     assert dcall(np.array([3], np.int32), ws=100) == WORKSPACE
+    # the decode attention reads cached rows as 16-byte vectors
+    kv_odd = lib_mod.KVCache(0x10008, 0x20000, 16)
+    f32 = lib_mod.decoder_cfg(2, 4096, 32, 11008, lib_mod.F32)
+    assert L.spider_decode_step(ctypes.byref(f32), W, 1, np.array([3], np.int32).ctypes.data, 0x1000,
+                                ctypes.byref(kv_odd), None, None, 0, 0x5000, None, None, 0x100000, 1 << 40,
+                                None) == UNSUPPORTED
+    f32_dh30 = lib_mod.decoder_cfg(2, 120, 4, 344, lib_mod.F32)     # dh = 30: not a multiple of 4 floats
+    assert L.spider_decode_step(ctypes.byref(f32_dh30), W, 1, np.array([3], np.int32).ctypes.data, 0x1000,
+                                ctypes.byref(kv), None, None, 0, 0x5000, None, None, 0x100000, 1 << 40,
+                                None) == UNSUPPORTED
     assert L.spider_decode_workspace_size(ctypes.byref(bf), 2, 16, 32000) > \
         L.spider_decode_workspace_size(ctypes.byref(bf), 2, 16, 0) > 0
 
