@@ -126,6 +126,24 @@ def test_bypassed_rows_keep_input_bits_and_runs_are_deterministic():
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("wl,cu", [("llava_next_7b", [0, 705]), ("llava15_7b", [0, 1000, 1037, 1537])])
+def test_large_row_paths_are_deterministic(wl, cu):
+    """More than 256 rows: tile GEMMs (the 705-row SwiGLU launch splits its last wave's tiles along k)
+    and the shared-tile attention; two runs give the same bits."""
+    L = need_gpu()
+    dec = get_workload(wl).dec
+    cu = np.array(cu, np.int32)
+    rows = int(cu[-1])
+    log(f"[prefill] deterministic large rows: {wl} rows={rows}")
+    codes = _codes(2, cu, 64, 11, 0.3, 0.2, True)
+    x = _x(dec, rows, 4)
+    h1, W, cfg = _run(L, dec, 2, cu, codes, x)
+    h2 = L.prefill(cfg, W, cu, x.cuda(), codes).cpu().numpy()
+    assert np.array_equal(h1, h2)
+    assert np.all(np.isfinite(h1))
+
+
+@pytest.mark.gpu
 def test_all_rows_bypass_everything_is_identity():
     L = need_gpu()
     w = get_workload("llava15_7b")
