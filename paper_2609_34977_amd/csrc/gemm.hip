@@ -590,7 +590,7 @@ __device__ __forceinline__ int2 tile_origin(int local, int tm, int tn, int BM, i
   return make_int2((first_m + within % gm) * BM, (within / gm) * BN);
 }
 
-template <int MH, bool DUAL>
+template <int MH, bool DUAL, bool QKV = false>
 __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
   constexpr int KB = 64;
   constexpr int BM = 64 * MH;
@@ -598,9 +598,14 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
   constexpr int STAGE_BYTES = A_BYTES + 256 * 128;
   constexpr int OPITCH = 136;  // dual epilogue: bf16 tile BM x 128, padded rows
   constexpr int RING_BYTES = 2 * STAGE_BYTES > BM * OPITCH * 2 ? 2 * STAGE_BYTES : BM * OPITCH * 2;
-  static_assert(RING_BYTES <= 160 * 1024, "LDS of one CU");
+  // QKV epilogue: RoPE positions of the block's rows past the ring.  They
+  // share its LDS array on purpose: with a second __shared__ object the
+  // compiler can no longer tell the fragment reads from the in-flight
+  // global_load_lds writes and waits for all loads before them.
+  constexpr int POS_BYTES = QKV ? BM * 4 : 0;
+  static_assert(RING_BYTES + POS_BYTES <= 144 * 1024, "LDS of one block");
   constexpr int A_PER_WAVE = BM / 32;  // DMA instructions (8 rows each) per wave and k-block
-  __shared__ __attribute__((aligned(1024))) uint8_t ring[RING_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[RING_BYTES + POS_BYTES];
 
   // wave-derived values are uniform: keep them (and the branches on them) scalar
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -651,6 +656,15 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
   }
   // weight DMA: instruction j of this wave fills stage weight rows 8g..8g+7, g = 8*wave + j
   const uint16_t* pw[8];
+  // QKV epilogue: RoPE positions of the block's rows, read once at the start
+  int* spos = reinterpret_cast<int*>(ring + RING_BYTES);
+  const int kind = sel3(gi, a.g[0].kind, a.g[1].kind, a.g[2].kind);
+  if constexpr (QKV) {
+    if (kind == 1 && tid < BM) {
+      const int m = min(m0 + tid, M - 1);
+      spos[tid] = a.pos[G.rows ? G.rows[m] : m];
+    }
+  }
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int wr = 8 * (8 * wave + j) + (lane >> 3);  // 0..255
@@ -795,6 +809,90 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
       const int row = c >> 4, ch = c & 15;
       *reinterpret_cast<u32x4*>(op + (int64_t)row * G.ldo + 8 * ch) =
           *reinterpret_cast<const u32x4*>(ot + row * OPITCH + 8 * ch);
+    }
+  } else if constexpr (QKV) {
+    // bf16 Q, K or V^T.  The wave's 128 output columns are one head, so the
+    // rotate-half partner of column 32u + lo (u = 0, 1) is the same lane's
+    // column 32(u + 2) + lo.  First RoPE in place on the accumulators, then
+    // one 32-row tile at a time through the wave's own LDS area and out
+    // as 16-byte pieces: [row][column] rows of Q and K, or [column][row] for
+    // V^T whose rows M..ldvt-1 are written zero.  That loop and its barriers
+    // run the same number of times in every wave.
+    if (kind == 1) {
+      // cos/sin rows of the block's BM rows into the ring (512 B per row, row
+      // j at byte 512 j): one burst of global_load_lds, 2 rows per wave
+      // instruction, then one wait instead of one table latency per tile
+      static_assert(BM * 512 <= RING_BYTES, "RoPE rows fit in the ring");
+      __syncthreads();  // spos written, every wave done with the last stage
+#pragma unroll
+      for (int t = 0; t < BM / 8; ++t) {
+        const int row = 2 * (wave + 4 * t) + hi;
+        const int p = spos[row];
+        __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(a.rope + (int64_t)p * 64 + 2 * lo),
+                                         (__attribute__((address_space(3))) void*)(ring + 2 * (wave + 4 * t) * 512),
+                                         16, 0, 0);
+      }
+      wait_vmcnt<0>();
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < MH; ++i) {
+        if (i < live) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = 32 * (MH * mh + i) + 8 * (r >> 2) + 4 * hi + (r & 3);
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              const float2 c = *reinterpret_cast<const float2*>(ring + row * 512 + (32 * u + lo) * 8);
+              const float2 y = rope_rotate(acc[i][u][r], acc[i][u + 2][r], c.x, c.y);
+              acc[i][u][r] = y.x;
+              acc[i][u + 2][r] = y.y;
+            }
+          }
+        }
+      }
+    }
+    constexpr int QP = 136, VP = 40;  // pitches (bf16) of the two layouts
+    constexpr int WAREA = 32 * QP > 128 * VP ? 32 * QP : 128 * VP;
+    static_assert(4 * WAREA * 2 <= RING_BYTES, "epilogue staging fits");
+    uint16_t* sw = reinterpret_cast<uint16_t*>(ring) + wave * WAREA;
+    const int col0 = n0 + 128 * nh;
+    uint16_t* out = reinterpret_cast<uint16_t*>(G.out);
+#pragma unroll
+    for (int i = 0; i < MH; ++i) {
+      const int rb = m0 + 32 * (MH * mh + i);  // first row of the tile
+      __syncthreads();
+      if (i < live) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = 8 * (r >> 2) + 4 * hi + (r & 3);
+            if (kind == 1)
+              sw[row * QP + 32 * u + lo] = f32_to_bf16_bits(acc[i][u][r]);
+            else
+              sw[(32 * u + lo) * VP + row] = f32_to_bf16_bits(rb + row < M ? acc[i][u][r] : 0.f);
+          }
+      }
+      __syncthreads();
+      if (i < live) {
+        if (kind == 1) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int row = (lane >> 4) + 4 * j, ch = lane & 15;
+            if (rb + row < M)
+              *reinterpret_cast<u32x4*>(out + (int64_t)(rb + row) * G.ldo + col0 + 8 * ch) =
+                  *reinterpret_cast<const u32x4*>(sw + row * QP + 8 * ch);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int c = (lane >> 2) + 16 * j, ch = lane & 3;
+            if (rb + 8 * ch < a.ldvt)
+              *reinterpret_cast<u32x4*>(out + (int64_t)(col0 + c) * a.ldvt + rb + 8 * ch) =
+                  *reinterpret_cast<const u32x4*>(sw + c * VP + 8 * ch);
+          }
+        }
+      }
     }
   } else {
     // fp32 partial sums: each store instruction writes two whole 128-byte row segments
@@ -1089,10 +1187,14 @@ bool tile_path_fits(const GemmArgs& a, bool dual) {
   return true;
 }
 
-hipError_t launch_tile(GemmArgs& a, int split_max, bool dual, hipStream_t st) {
+struct TileChoice {
+  int mh, split, tail, tail_split;
+};
+
+TileChoice tile_choice(const GemmArgs& a, int split_max, bool dual) {
   const int bn = dual ? 128 : 256;
-  int best_mh = 4, best_split = 1, best_tail = 0, best_ts = 0;
-  double best = 1e300;
+  TileChoice best{4, 1, 0, 0};
+  double best_cost = 1e300;
   for (int mh : {4, 3, 2}) {
     const int bm = 64 * mh;
     const int tiles = tiles_for(a, bm, bn);
@@ -1115,14 +1217,20 @@ hipError_t launch_tile(GemmArgs& a, int split_max, bool dual, hipStream_t st) {
         }
       }
     }
-    if (cost < best) {
-      best = cost;
-      best_mh = mh;
-      best_split = split;
-      best_tail = tail;
-      best_ts = ts;
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = TileChoice{mh, split, tail, ts};
     }
   }
+  return best;
+}
+
+hipError_t launch_tile(GemmArgs& a, int split_max, bool dual, hipStream_t st) {
+  const int bn = dual ? 128 : 256;
+  const TileChoice tc = tile_choice(a, split_max, dual);
+  const int best_mh = tc.mh, best_split = tc.split, best_tail = tc.tail, best_ts = tc.tail_split;
+  const bool qkv = a.epilogue == EPI_QKV_BF16;
+  if (qkv && best_split != 1) return hipErrorInvalidValue;
   a.split = best_split;
   a.k_per_split = ceil_div(a.K / 64, a.split) * 64;
   fill_tiles(a, 64 * best_mh, bn);
@@ -1133,11 +1241,14 @@ hipError_t launch_tile(GemmArgs& a, int split_max, bool dual, hipStream_t st) {
   const int blocks = a.total_tiles + best_tail * best_ts;
   if (blocks == 0) return hipSuccess;
   switch (best_mh * 2 + (dual ? 1 : 0)) {
-    case 8: gemm_tile_kernel<4, false><<<blocks, 256, 0, st>>>(a); break;
+    case 8: qkv ? gemm_tile_kernel<4, false, true><<<blocks, 256, 0, st>>>(a)
+                : gemm_tile_kernel<4, false><<<blocks, 256, 0, st>>>(a); break;
     case 9: gemm_tile_kernel<4, true><<<blocks, 256, 0, st>>>(a); break;
-    case 6: gemm_tile_kernel<3, false><<<blocks, 256, 0, st>>>(a); break;
+    case 6: qkv ? gemm_tile_kernel<3, false, true><<<blocks, 256, 0, st>>>(a)
+                : gemm_tile_kernel<3, false><<<blocks, 256, 0, st>>>(a); break;
     case 7: gemm_tile_kernel<3, true><<<blocks, 256, 0, st>>>(a); break;
-    case 4: gemm_tile_kernel<2, false><<<blocks, 256, 0, st>>>(a); break;
+    case 4: qkv ? gemm_tile_kernel<2, false, true><<<blocks, 256, 0, st>>>(a)
+                : gemm_tile_kernel<2, false><<<blocks, 256, 0, st>>>(a); break;
     default: gemm_tile_kernel<2, true><<<blocks, 256, 0, st>>>(a); break;
   }
   if (best_tail) {
@@ -1175,6 +1286,22 @@ hipError_t launch_gemv(GemmArgs& a, int maxM, bool dual, hipStream_t st) {
 
 }  // namespace
 
+namespace {
+bool gemv_fits(int maxM, int K) { return maxM <= 4 && K % 8 == 0 && (size_t)4 * K * 2 <= 160 * 1024; }
+int max_rows(const GemmArgs& a) {
+  int maxM = 0;
+  for (int i = 0; i < a.ngroups; ++i) maxM = std::max(maxM, a.g[i].M);
+  return maxM;
+}
+}  // namespace
+
+int gemm_tile_unsplit_blocks(const GemmArgs& a, int split_max) {
+  const int maxM = max_rows(a);
+  if (gemv_fits(maxM, a.K) || maxM <= 256 || !tile_path_fits(a, false)) return 0;
+  const TileChoice tc = tile_choice(a, split_max, false);
+  return tc.split == 1 ? tiles_for(a, 64 * tc.mh, 256) : 0;
+}
+
 int gemm_split_for(int M, int N, int K, bool dual, bool bf16, int split_max) {
   if (dual || !bf16) return 1;
   TileCfg tc = pick_bf16_tile(M, false);
@@ -1182,8 +1309,7 @@ int gemm_split_for(int M, int N, int K, bool dual, bool bf16, int split_max) {
 }
 
 hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
-  int maxM = 0;
-  for (int i = 0; i < a.ngroups; ++i) maxM = std::max(maxM, a.g[i].M);
+  const int maxM = max_rows(a);
   if (a.epilogue == EPI_LENS_STATS) {
     if (maxM > 256 || a.K % 64) return hipErrorInvalidValue;
     for (int i = 0; i < a.ngroups; ++i)
@@ -1202,7 +1328,17 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
     return hipGetLastError();
   }
   const bool dual = a.epilogue == EPI_SWIGLU;
-  const bool gemv_ok = maxM <= 4 && a.K % 8 == 0 && (size_t)4 * a.K * 2 <= 160 * 1024;
+  const bool gemv_ok = gemv_fits(maxM, a.K);
+  if (a.epilogue == EPI_QKV_BF16) {
+    // the tile kernel without split, one head of 128 columns per wave, 16-byte stores
+    if (gemm_tile_unsplit_blocks(a, split_max) == 0 || !a.rope || !a.pos) return hipErrorInvalidValue;
+    for (int i = 0; i < a.ngroups; ++i) {
+      const GemmGroup& g = a.g[i];
+      if (reinterpret_cast<uintptr_t>(g.out) % 16) return hipErrorInvalidValue;
+      if (g.kind == 1 ? g.ldo % 8 != 0 : (g.kind != 2 || a.ldvt % 32 || a.ldvt < g.M)) return hipErrorInvalidValue;
+    }
+    return launch_tile(a, split_max, false, st);
+  }
   if (a.epilogue == EPI_RESIDUAL_F32 || a.norm_h) {
     // only the decode-row kernel applies a residual epilogue or a fused norm
     // (the norm holds a row of at most 8192 floats in registers)
@@ -1259,6 +1395,7 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
 
 hipError_t launch_gemm_f32(GemmArgs& a, int split_max, hipStream_t st) {
   (void)split_max;
+  if (a.epilogue != EPI_PARTIAL_F32 && a.epilogue != EPI_SWIGLU) return hipErrorInvalidValue;
   a.split = 1;
   a.k_per_split = a.K;
   int t = 0;

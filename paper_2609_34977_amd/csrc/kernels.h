@@ -18,6 +18,7 @@ struct GemmGroup {
   int64_t split_stride;   // elements between split-K slabs of out
   int tiles_m, tiles_n;   // filled by the launcher
   int tile_begin;         // filled by the launcher
+  int kind;               // EPI_QKV_BF16 only: 1 = RoPE'd rows (Q, K), 2 = transposed rows (V^T)
 };
 
 enum GemmEpilogue {
@@ -26,7 +27,10 @@ enum GemmEpilogue {
   EPI_LENS_STATS = 2,   // out fp32 [M][N/128][4]: per row and 128-column tile of z = A W^T,
                         // (max z, sum e^(z-max), sum e^(z-max) (z-max), 0); bf16 only,
                         // M <= 256, N % 128 == 0, K % 64 == 0, no split
-  EPI_RESIDUAL_F32 = 3  // out fp32 [M][N] += A W^T; bf16, M <= 4 only (decode), no split
+  EPI_RESIDUAL_F32 = 3,  // out fp32 [M][N] += A W^T; bf16, M <= 4 only (decode), no split
+  EPI_QKV_BF16 = 4       // bf16 out per group kind: 1 = rotate-half RoPE at pos[row] (row = a_rows[m]
+                         // or m) then out [M][ldo]; 2 = out^T [N][ldvt]; head size 128, more than
+                         // 256 rows, the tile kernel without split only (gemm_tile_unsplit_blocks)
 };
 
 struct GemmArgs {
@@ -50,7 +54,21 @@ struct GemmArgs {
   const float* norm_h;
   const float* norm_w;
   float norm_eps;
+  // EPI_QKV_BF16: RoPE table [positions][64] (cos, sin), packed-row positions, V^T row stride
+  const float2* rope;
+  const int32_t* pos;
+  int64_t ldvt;
 };
+
+// Blocks of the launch when launch_gemm_bf16 would run these groups through
+// the tile kernel without split-K (the condition of EPI_QKV_BF16), else 0.
+int gemm_tile_unsplit_blocks(const GemmArgs& a, int split_max);
+
+// The rotate-half RoPE of the pair (x0, x1) with (cos, sin): one rounding
+// order shared by every kernel that applies it.
+__device__ __forceinline__ float2 rope_rotate(float x0, float x1, float c, float s) {
+  return make_float2(fmaf(x0, c, -(x1 * s)), fmaf(x1, c, x0 * s));
+}
 
 // Chooses tiles and split-K for the groups (all with the same K) and launches.
 // `split_max` bounds split-K (partial buffers are sized for it).

@@ -256,10 +256,9 @@ __global__ void __launch_bounds__(256) qkv_finalize_kernel(
         const float sy[4] = {cs[q][0].y, cs[q][0].w, cs[q][1].y, cs[q][1].w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float y0 = a[e] * cx[e] - b[e] * sy[e];
-          const float y1 = b[e] * cx[e] + a[e] * sy[e];
-          a[e] = y0;
-          b[e] = y1;
+          const float2 y = rope_rotate(a[e], b[e], cx[e], sy[e]);
+          a[e] = y.x;
+          b[e] = y.y;
         }
       }
 #pragma unroll
@@ -280,10 +279,9 @@ __global__ void __launch_bounds__(256) qkv_finalize_kernel(
     }
     if (p >= 0) {
       const float2 cs = rope[(int64_t)p * half + i];
-      const float y0 = x0 * cs.x - x1 * cs.y;
-      const float y1 = x1 * cs.x + x0 * cs.y;
-      x0 = y0;
-      x1 = y1;
+      const float2 y = rope_rotate(x0, x1, cs.x, cs.y);
+      x0 = y.x;
+      x1 = y.y;
     }
     Act<AT>::store(dst + c0, x0);
     Act<AT>::store(dst + c1, x1);
@@ -339,10 +337,9 @@ __global__ void __launch_bounds__(256) decode_qkv_kernel(const float* __restrict
     }
     if (kind < 2) {
       const float2 cs = rope[(int64_t)p * half + i];
-      const float y0 = x0 * cs.x - x1 * cs.y;
-      const float y1 = x1 * cs.x + x0 * cs.y;
-      x0 = y0;
-      x1 = y1;
+      const float2 y = rope_rotate(x0, x1, cs.x, cs.y);
+      x0 = y.x;
+      x1 = y.y;
     }
     Act<AT>::store(dst + c0, x0);
     Act<AT>::store(dst + c1, x1);
@@ -838,8 +835,9 @@ struct PrefillRun {
   bool bf16() const { return c.dtype == SPIDER_BF16; }
   int64_t pstride() const { return (int64_t)R * c.d; }
 
+  int split_cap(int cap) const { return std::min(split_max_for_rows(R), cap); }
   hipError_t gemm(GemmArgs& ga, int cap) {
-    const int sm = std::min(split_max_for_rows(R), cap);
+    const int sm = split_cap(cap);
     return bf16() ? launch_gemm_bf16(ga, sm, st) : launch_gemm_f32(ga, sm, st);
   }
 
@@ -912,12 +910,29 @@ struct PrefillRun {
         ga.g[0] = gk;
         ga.g[1] = gv;
       }
+      // Without a cache and with the tile kernel unsplit (many rows), the
+      // GEMM's epilogue applies RoPE and writes bf16 Q, K and V^T itself:
+      // no fp32 round trip and no finalize launch.
+      const bool fused = bf16() && !ck && dh == 128 && gemm_tile_unsplit_blocks(ga, split_cap(2)) > 0;
+      if (fused) {
+        ga.epilogue = EPI_QKV_BF16;
+        ga.rope = ws.rope;
+        ga.pos = dpos;
+        ga.ldvt = vt_rows(R);
+        void* outs[3] = {qb, kb, vb};
+        const int kinds[3] = {1, 1, 2};
+        const int first = ga.ngroups == 3 ? 0 : 1;
+        for (int i = 0; i < ga.ngroups; ++i) {
+          ga.g[i].out = outs[first + i];
+          ga.g[i].kind = kinds[first + i];
+        }
+      }
       {
         ProfScope ps(KC_GEMM_QKV, st);
         hipError_t e = gemm(ga, 2);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_qkv: %s", hipGetErrorString(e));
       }
-      {
+      if (!fused) {
         ProfScope ps(KC_QKV_FINALIZE, st);
         const int64_t ldvt = bf16() ? vt_rows(R) : 0;
         const int vblocks = bf16() ? (vt_rows(R) / 32) * (d / 64) : R;

@@ -75,6 +75,9 @@ PARITY = {
     # rows bypassing attention: query blocks of the shared-tile attention kernel
     # and row tiles of the large-row GEMM straddle sample boundaries
     "7b_three_ragged_1537_rows": ("llava15_7b", 1, [0, 1000, 1037, 1537], 64, 0.35, 0.2, True),
+    # 3000 rows: the unsplit QKV GEMM applies RoPE and stores bf16 Q, K and V^T in its own
+    # epilogue, here with 256-row tiles (the 1537-row case above takes 192-row tiles)
+    "7b_three_ragged_3000_rows": ("llava15_7b", 1, [0, 1500, 1560, 3000], 64, 0.4, 0.2, True),
 }
 
 
@@ -126,10 +129,13 @@ def test_bypassed_rows_keep_input_bits_and_runs_are_deterministic():
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("wl,cu", [("llava_next_7b", [0, 705]), ("llava15_7b", [0, 1000, 1037, 1537])])
+@pytest.mark.parametrize("wl,cu", [("llava_next_7b", [0, 705]), ("llava15_7b", [0, 1000, 1037, 1537]),
+                                   ("llava15_7b", [0, 1500, 1560, 3000])])
 def test_large_row_paths_are_deterministic(wl, cu):
     """More than 256 rows: tile GEMMs (the 705-row SwiGLU launch splits its last wave's tiles along k)
-    and the shared-tile attention; two runs give the same bits."""
+    and the shared-tile attention; two runs give the same bits.  Without a KV cache the unsplit QKV
+    GEMM applies RoPE and stores bf16 Q, K and V^T in its epilogue; with one it writes fp32 sums and
+    a separate kernel does that: both must give the same bits."""
     L = need_gpu()
     dec = get_workload(wl).dec
     cu = np.array(cu, np.int32)
@@ -141,6 +147,9 @@ def test_large_row_paths_are_deterministic(wl, cu):
     h2 = L.prefill(cfg, W, cu, x.cuda(), codes).cpu().numpy()
     assert np.array_equal(h1, h2)
     assert np.all(np.isfinite(h1))
+    kv = L.kv_cache(cfg, len(cu) - 1, int(max(cu[1:] - cu[:-1])), "cuda")
+    h3 = L.prefill_kv(cfg, W, cu, x.cuda(), codes, kv).cpu().numpy()
+    assert np.array_equal(h1, h3)
 
 
 @pytest.mark.gpu
