@@ -420,10 +420,11 @@ __global__ void __launch_bounds__(256) kmeans_assign_kernel(int n, int d, int n_
                                                             int first, FeatArgs fa, int last,
                                                             const int32_t* __restrict__ rest_list,
                                                             ClusterWs cw, int32_t* __restrict__ cluster_out) {
-  extern __shared__ float smem[];
+  extern __shared__ __attribute__((aligned(16))) float smem[];  // 16-byte centroid reads
   float* cs = smem;                 // [K*d] centroids
   float* red = cs + K * d;          // [4*512]
   __shared__ int lab[kMaxRowsPerBlock];
+  __shared__ int sidx[kMaxRowsPerBlock];  // U[j0..j1): one dependent load less per row
   __shared__ int chg;
   const int g = blockIdx.y, b = blockIdx.x;
   const int m = n - n_anchor;
@@ -431,6 +432,7 @@ __global__ void __launch_bounds__(256) kmeans_assign_kernel(int n, int d, int n_
   if (j0 >= j1 || cw.conv[g]) return;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int32_t* U = rest_list + (int64_t)g * n;
+  for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) sidx[j - j0] = U[j];
   float* cent = cw.cent + (int64_t)g * K * d;
   if (first) {
     // centroids at rows floor(k*m/K) of the non-anchor list
@@ -453,18 +455,40 @@ __global__ void __launch_bounds__(256) kmeans_assign_kernel(int n, int d, int n_
   for (int k = 0; k < kFusedClusters; ++k)
 #pragma unroll
     for (int v = 0; v < VPL; ++v) acc[k][v] = 0.f;
+  // d % 8 == 0: every 8-dimension chunk of a lane is whole, and its centroid
+  // values are read as two 16-byte LDS vectors (lane l reads bytes 32 l ..,
+  // no bank conflicts; scalar reads at 8-float lane strides conflict 8 ways).
+  // Same terms in the same order as the scalar loop, so the same bits.
+  const bool d8 = (d & 7) == 0;
   for (int j = j0 + wave; j < j1; j += 4) {
     float x[VPL];
-    load_slice<FT, VPL>(feat_row<FT>(fa, last, g, U[j]), d, lane, x);
+    load_slice<FT, VPL>(feat_row<FT>(fa, last, g, sidx[j - j0]), d, lane, x);
     int best = 0;
     float bd = 0.f;
     for (int k = 0; k < K; ++k) {
       float s = 0.f;
+      if (d8) {
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) {
-        const int dim = slice_dim(v, lane);
-        const float t = dim < d ? x[v] - cs[k * d + dim] : 0.f;
-        s = fmaf(t, t, s);
+        for (int c = 0; c < VPL / 8; ++c) {
+          const int base = c * 512 + lane * 8;
+          if (base < d) {
+            const float4 c0 = *reinterpret_cast<const float4*>(cs + k * d + base);
+            const float4 c1 = *reinterpret_cast<const float4*>(cs + k * d + base + 4);
+            const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float t = x[8 * c + e] - cc[e];
+              s = fmaf(t, t, s);
+            }
+          }
+        }
+      } else {
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          const int dim = slice_dim(v, lane);
+          const float t = dim < d ? x[v] - cs[k * d + dim] : 0.f;
+          s = fmaf(t, t, s);
+        }
       }
       s = wave_sum(s);
       if (k == 0 || s < bd) {
@@ -477,7 +501,7 @@ __global__ void __launch_bounds__(256) kmeans_assign_kernel(int n, int d, int n_
       if (!first && asg[j] != best) chg = 1;
       asg[j] = best;
       lab[j - j0] = best;
-      cluster_out[(int64_t)g * n + U[j]] = best;
+      cluster_out[(int64_t)g * n + sidx[j - j0]] = best;
     }
   }
   __syncthreads();
@@ -526,13 +550,20 @@ __global__ void __launch_bounds__(256) cluster_sum_kernel(int n, int d, int n_an
                                                           const float* __restrict__ mvec, ClusterWs cw) {
   __shared__ float red[4 * 512];
   __shared__ int lab[kMaxRowsPerBlock];
+  __shared__ int sidx[kMaxRowsPerBlock];  // U[j0..j1), then m of those rows: no dependent
+  __shared__ float sm_m[kMaxRowsPerBlock];  // index loads inside the row loops
   const int g = blockIdx.y, b = blockIdx.x;
   const int m = n - n_anchor;
   const int j0 = b * cw.RB, j1 = min(m, j0 + cw.RB);
   if (j0 >= j1) return;
   const int32_t* U = rest_list + (int64_t)g * n;
   const int32_t* asg = cw.assign + (int64_t)g * n;
-  for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) lab[j - j0] = asg[j];
+  for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
+    lab[j - j0] = asg[j];
+    const int i = U[j];
+    sidx[j - j0] = i;
+    sm_m[j - j0] = mvec[(int64_t)g * n + i];
+  }
   __syncthreads();
   const int64_t slot = (int64_t)g * cw.NB + b;
   for (int l = 0; l < n_layers; ++l) {
@@ -547,7 +578,7 @@ __global__ void __launch_bounds__(256) cluster_sum_kernel(int n, int d, int n_an
 #pragma unroll
         for (int v = 0; v < VPL; ++v) acc[k][v] = 0.f;
       for (int j = j0 + wave; j < j1; j += 4) {
-        const int i = U[j];
+        const int i = sidx[j - j0];
         float x[VPL];
         load_slice<FT, VPL>(feat_row<FT>(fa, l, g, i), d, lane, x);
         add_to_cluster<kFusedClusters, VPL>(acc, lab[j - j0], x, nul[i]);
@@ -563,7 +594,7 @@ __global__ void __launch_bounds__(256) cluster_sum_kernel(int n, int d, int n_an
     for (int j = j0; j < j1; ++j)
       if (lab[j - j0] == (int)threadIdx.x) {
         ++c;
-        sm += mvec[(int64_t)g * n + U[j]];
+        sm += sm_m[j - j0];
       }
     cw.pcnt[slot * K + threadIdx.x] = c;
     cw.pm[slot * K + threadIdx.x] = sm;
