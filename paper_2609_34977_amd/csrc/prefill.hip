@@ -36,11 +36,18 @@ template <>
 struct Act<float> {
   __device__ static inline void store(float* p, float v) { *p = v; }
   __device__ static inline float load(const float* p) { return *p; }
+  // 4 consecutive values, p 16-byte aligned
+  __device__ static inline void store4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
 };
 template <>
 struct Act<uint16_t> {
   __device__ static inline void store(uint16_t* p, float v) { *p = f32_to_bf16_bits(v); }
   __device__ static inline float load(const uint16_t* p) { return bf16_bits_to_f32(*p); }
+  // 4 consecutive values, p 8-byte aligned
+  __device__ static inline void store4(uint16_t* p, float4 v) {
+    *reinterpret_cast<uint2*>(p) = make_uint2((uint32_t)f32_to_bf16_bits(v.x) | ((uint32_t)f32_to_bf16_bits(v.y) << 16),
+                                              (uint32_t)f32_to_bf16_bits(v.z) | ((uint32_t)f32_to_bf16_bits(v.w) << 16));
+  }
 };
 
 // h = float(x)
@@ -75,17 +82,22 @@ __global__ void __launch_bounds__(256) norm_kernel(float* __restrict__ h, int d,
                                                    AT* __restrict__ out) {
   __shared__ float red[4];
   const int r = blockIdx.x;
-  const int ps = (P && pslot) ? pslot[r] : -1;
-  const int ns = all_rows ? r : (nslot ? nslot[r] : -1);
-  if (ps < 0 && ns < 0) return;
   const int d4 = d >> 2;
+  // the row of h and the norm weights first: neither depends on the slot
+  // lookups, so their latency overlaps those and the partial sums' (w is
+  // null for a residual-only pass, which never reaches the normalisation)
   float4* hr = reinterpret_cast<float4*>(h + (int64_t)r * d);
-  float4 v[MAXV];
+  const float4* w4 = reinterpret_cast<const float4*>(w);
+  float4 v[MAXV], ww[MAXV];
 #pragma unroll
   for (int k = 0; k < MAXV; ++k) {
     const int c = threadIdx.x + k * 256;
     v[k] = c < d4 ? hr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    ww[k] = (w && c < d4) ? w4[c] : make_float4(0.f, 0.f, 0.f, 0.f);  // no weights: residual only
   }
+  const int ps = (P && pslot) ? pslot[r] : -1;
+  const int ns = all_rows ? r : (nslot ? nslot[r] : -1);
+  if (ps < 0 && ns < 0) return;
   if (ps >= 0) {
     const float4* pr = reinterpret_cast<const float4*>(P + (int64_t)ps * d);
     const int64_t ps4 = pstride >> 2;
@@ -128,17 +140,12 @@ __global__ void __launch_bounds__(256) norm_kernel(float* __restrict__ h, int d,
   const float tot = (red[0] + red[1]) + (red[2] + red[3]);
   const float inv = 1.0f / sqrtf(tot / (float)d + eps);
   AT* o = out + (int64_t)ns * d;
-  const float4* w4 = reinterpret_cast<const float4*>(w);
 #pragma unroll
   for (int k = 0; k < MAXV; ++k) {
     const int c = threadIdx.x + k * 256;
-    if (c < d4) {
-      const float4 ww = w4[c];
-      Act<AT>::store(o + 4 * c + 0, v[k].x * inv * ww.x);
-      Act<AT>::store(o + 4 * c + 1, v[k].y * inv * ww.y);
-      Act<AT>::store(o + 4 * c + 2, v[k].z * inv * ww.z);
-      Act<AT>::store(o + 4 * c + 3, v[k].w * inv * ww.w);
-    }
+    if (c < d4)
+      Act<AT>::store4(o + 4 * c, make_float4(v[k].x * inv * ww[k].x, v[k].y * inv * ww[k].y,
+                                             v[k].z * inv * ww[k].z, v[k].w * inv * ww[k].w));
   }
 }
 
