@@ -932,12 +932,12 @@ __global__ void __launch_bounds__(128) swiglu_tail_reduce_kernel(GemmArgs a, int
 // block of 4 waves, the MB activation rows staged in LDS once (bf16), each
 // wave owning NR weight rows (SwiGLU: NR/2 outputs, their gate and up rows)
 // for the whole K.  Lane l takes the 16-byte chunks l, l + 64, ... of every
-// row (1 KB per wave instruction, non-temporal: weights are read once), four
-// chunks of each row in flight; fp32 FMAs, then one fixed-order wave sum per
-// (row, activation row).  No split-K: the fp32 output is the finished sum.
-// NR weight rows per wave, U chunks of each in flight per iteration; a
-// lane adds its chunks in ascending order whatever NR and U are (same bits).
-template <int MB, bool DUAL, int NR = 4, int U = 4>
+// row (1 KB per wave instruction, non-temporal: weights are read once), U
+// chunks of each row in flight per iteration; fp32 FMAs, then one fixed-order
+// wave sum per (row, activation row).  No split-K: the fp32 output is the
+// finished sum.  A lane adds its chunks in ascending order whatever NR and U
+// are, so they change the speed, not the bits.
+template <int MB, bool DUAL, int NR, int U>
 __global__ void __launch_bounds__(256) gemv_kernel(GemmArgs a) {
   constexpr int NO = DUAL ? NR / 2 : NR;      // outputs per wave
   extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [MB][K]
@@ -1260,19 +1260,16 @@ hipError_t launch_tile(GemmArgs& a, int split_max, bool dual, hipStream_t st) {
 }
 
 // At most 4 rows: gemv_kernel, no split (the output holds the finished sums).
-// A launch of fewer than 1024 blocks of 16 rows (the QKV, O and down
-// projections of a decode step: 768 / 256 blocks, one wave per SIMD, each
-// wave's row chunks fetched in several dependent rounds) runs one weight row
-// per wave with 16 chunks in flight instead: four times the blocks, a third
-// of the rounds (measured 3.40 -> 3.25 ms per decode step; the fused norm that
-// every block then recomputes for its rows costs less than it gains).
+// Decode rows: one weight row per wave with 16 chunks in flight (SwiGLU: the
+// gate and up rows of one output, 8 chunks each), four waves per block.  With
+// 4 rows (2 outputs) and 4 chunks per wave, a wave fetched its rows in several
+// dependent rounds and the O and down projections filled only 256 blocks:
+// 3.40 ms per decode step then, 3.13 now; 32 / 16 chunks (more registers,
+// fewer waves per SIMD) measured 3.55 ms.
 hipError_t launch_gemv(GemmArgs& a, int maxM, bool dual, hipStream_t st) {
   a.split = 1;
   a.k_per_split = a.K;
-  int t16 = 0;
-  for (int i = 0; i < a.ngroups; ++i) t16 += ceil_div(a.g[i].N, 16);
-  const bool narrow = !dual && t16 < 1024;
-  const int per_block = narrow ? 4 : 4 * (dual ? 2 : 4);  // outputs per block
+  const int per_block = 4;  // outputs per block
   int t = 0;
   for (int i = 0; i < a.ngroups; ++i) {
     a.g[i].tile_begin = t;
@@ -1282,7 +1279,7 @@ hipError_t launch_gemv(GemmArgs& a, int maxM, bool dual, hipStream_t st) {
   if (t == 0 || maxM == 0) return hipSuccess;
   const int mb = maxM <= 1 ? 1 : (maxM <= 2 ? 2 : 4);
   const size_t sh = (size_t)mb * a.K * 2;
-  if (narrow) {
+  if (!dual) {
     switch (mb) {
       case 1: gemv_kernel<1, false, 1, 16><<<t, 256, sh, st>>>(a); break;
       case 2: gemv_kernel<2, false, 1, 16><<<t, 256, sh, st>>>(a); break;
@@ -1290,13 +1287,10 @@ hipError_t launch_gemv(GemmArgs& a, int maxM, bool dual, hipStream_t st) {
     }
     return hipGetLastError();
   }
-  switch (mb * 2 + (dual ? 1 : 0)) {
-    case 2: gemv_kernel<1, false><<<t, 256, sh, st>>>(a); break;
-    case 3: gemv_kernel<1, true><<<t, 256, sh, st>>>(a); break;
-    case 4: gemv_kernel<2, false><<<t, 256, sh, st>>>(a); break;
-    case 5: gemv_kernel<2, true><<<t, 256, sh, st>>>(a); break;
-    case 8: gemv_kernel<4, false><<<t, 256, sh, st>>>(a); break;
-    default: gemv_kernel<4, true><<<t, 256, sh, st>>>(a); break;
+  switch (mb) {
+    case 1: gemv_kernel<1, true, 2, 8><<<t, 256, sh, st>>>(a); break;
+    case 2: gemv_kernel<2, true, 2, 8><<<t, 256, sh, st>>>(a); break;
+    default: gemv_kernel<4, true, 2, 8><<<t, 256, sh, st>>>(a); break;
   }
   return hipGetLastError();
 }
