@@ -937,8 +937,11 @@ __global__ void __launch_bounds__(128) swiglu_tail_reduce_kernel(GemmArgs a, int
 // wave sum per (row, activation row).  No split-K: the fp32 output is the
 // finished sum.  A lane adds its chunks in ascending order whatever NR and U
 // are, so they change the speed, not the bits.
-template <int MB, bool DUAL, int NR, int U>
+// QKV (EPI_DECODE_QKV): NR = 2, the wave's rows are the rotate-half pair
+// (c, c + 64) of one head, c = 128 (w / 64) + w % 64 for wave w of the launch.
+template <int MB, bool DUAL, int NR, int U, bool QKV = false>
 __global__ void __launch_bounds__(256) gemv_kernel(GemmArgs a) {
+  static_assert(!QKV || (NR == 2 && !DUAL), "QKV: one rotate-half pair per wave");
   constexpr int NO = DUAL ? NR / 2 : NR;      // outputs per wave
   extern __shared__ __attribute__((aligned(16))) uint16_t xs[];  // [MB][K]
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -998,12 +1001,13 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemmArgs a) {
     }
     __syncthreads();
   }
-  const int o0 = (blk * 4 + wave) * NO;  // first output column of this wave
+  const int gw = blk * 4 + wave;  // wave of the group
+  const int o0 = QKV ? 128 * (gw >> 6) + (gw & 63) : gw * NO;  // first output column of this wave
   if (o0 >= G.N) return;
   const uint16_t* wrow[NR];
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
-    const int o = min(o0 + (DUAL ? r % NO : r), G.N - 1);
+    const int o = QKV ? o0 + 64 * r : min(o0 + (DUAL ? r % NO : r), G.N - 1);
     const uint16_t* W = reinterpret_cast<const uint16_t*>(DUAL && r >= NO ? G.W2 : G.W);
     wrow[r] = W + (int64_t)o * K;
   }
@@ -1050,6 +1054,25 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemmArgs a) {
 #pragma unroll
     for (int m = 0; m < MB; ++m) acc[r][m] = wave_sum(acc[r][m]);
   if (lane != 0) return;
+  if constexpr (QKV) {
+    const int kind = sel3(gi, a.g[0].kind, a.g[1].kind, a.g[2].kind);
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      if (m >= G.M) break;
+      const int p = a.pos[m];
+      float y0 = acc[0][m], y1 = acc[1][m];
+      if (kind & 1) {
+        const float2 cs = a.rope[(int64_t)p * 64 + (o0 & 63)];
+        const float2 y = rope_rotate(y0, y1, cs.x, cs.y);
+        y0 = y.x;
+        y1 = y.y;
+      }
+      uint16_t* dst = reinterpret_cast<uint16_t*>(G.out) + ((kind & 2) ? (int64_t)m * a.kv_cap + p : m) * G.ldo;
+      dst[o0] = f32_to_bf16_bits(y0);
+      dst[o0 + 64] = f32_to_bf16_bits(y1);
+    }
+    return;
+  }
 #pragma unroll
   for (int q = 0; q < NO; ++q) {
     const int o = o0 + q;
@@ -1269,7 +1292,8 @@ hipError_t launch_tile(GemmArgs& a, int split_max, bool dual, hipStream_t st) {
 hipError_t launch_gemv(GemmArgs& a, int maxM, bool dual, hipStream_t st) {
   a.split = 1;
   a.k_per_split = a.K;
-  const int per_block = 4;  // outputs per block
+  const bool qkv = a.epilogue == EPI_DECODE_QKV;
+  const int per_block = qkv ? 8 : 4;  // outputs per block
   int t = 0;
   for (int i = 0; i < a.ngroups; ++i) {
     a.g[i].tile_begin = t;
@@ -1279,6 +1303,14 @@ hipError_t launch_gemv(GemmArgs& a, int maxM, bool dual, hipStream_t st) {
   if (t == 0 || maxM == 0) return hipSuccess;
   const int mb = maxM <= 1 ? 1 : (maxM <= 2 ? 2 : 4);
   const size_t sh = (size_t)mb * a.K * 2;
+  if (qkv) {
+    switch (mb) {
+      case 1: gemv_kernel<1, false, 2, 8, true><<<t, 256, sh, st>>>(a); break;
+      case 2: gemv_kernel<2, false, 2, 8, true><<<t, 256, sh, st>>>(a); break;
+      default: gemv_kernel<4, false, 2, 8, true><<<t, 256, sh, st>>>(a); break;
+    }
+    return hipGetLastError();
+  }
   if (!dual) {
     switch (mb) {
       case 1: gemv_kernel<1, false, 1, 16><<<t, 256, sh, st>>>(a); break;
@@ -1350,10 +1382,15 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
     }
     return launch_tile(a, split_max, false, st);
   }
-  if (a.epilogue == EPI_RESIDUAL_F32 || a.norm_h) {
-    // only the decode-row kernel applies a residual epilogue or a fused norm
-    // (the norm holds a row of at most 8192 floats in registers)
+  if (a.epilogue == EPI_RESIDUAL_F32 || a.epilogue == EPI_DECODE_QKV || a.norm_h) {
+    // only the decode-row kernel applies a residual or cache epilogue or a
+    // fused norm (the norm holds a row of at most 8192 floats in registers)
     if (!gemv_ok || (a.norm_h && (!a.norm_w || a.K > 8192))) return hipErrorInvalidValue;
+  }
+  if (a.epilogue == EPI_DECODE_QKV) {
+    if (!a.rope || !a.pos || a.kv_cap < 1) return hipErrorInvalidValue;
+    for (int i = 0; i < a.ngroups; ++i)
+      if (a.g[i].N % 128 || a.g[i].a_rows) return hipErrorInvalidValue;
   }
   if (gemv_ok) return launch_gemv(a, maxM, dual, st);
   if (maxM > 256 && tile_path_fits(a, dual)) return launch_tile(a, split_max, dual, st);

@@ -28,9 +28,12 @@ enum GemmEpilogue {
                         // (max z, sum e^(z-max), sum e^(z-max) (z-max), 0); bf16 only,
                         // M <= 256, N % 128 == 0, K % 64 == 0, no split
   EPI_RESIDUAL_F32 = 3,  // out fp32 [M][N] += A W^T; bf16, M <= 4 only (decode), no split
-  EPI_QKV_BF16 = 4       // bf16 out per group kind: 1 = rotate-half RoPE at pos[row] (row = a_rows[m]
+  EPI_QKV_BF16 = 4,      // bf16 out per group kind: 1 = rotate-half RoPE at pos[row] (row = a_rows[m]
                          // or m) then out [M][ldo]; 2 = out^T [N][ldvt]; head size 128, more than
                          // 256 rows, the tile kernel without split only (gemm_tile_unsplit_blocks)
+  EPI_DECODE_QKV = 5     // bf16, M <= 4 (decode rows, row m = sample m), head size 128: kind bit 0 =
+                         // rotate-half RoPE at pos[m], bit 1 = row m goes to the cache slot
+                         // out + (m * kv_cap + pos[m]) * ldo instead of out + m * ldo
 };
 
 struct GemmArgs {
@@ -58,6 +61,7 @@ struct GemmArgs {
   const float2* rope;
   const int32_t* pos;
   int64_t ldvt;
+  int kv_cap;  // EPI_DECODE_QKV: cache slots per sample
 };
 
 // Blocks of the launch when launch_gemm_bf16 would run these groups through

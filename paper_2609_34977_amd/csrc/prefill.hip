@@ -1287,13 +1287,24 @@ spider_status run_decode(const spider_decoder_cfg& c, const spider_layer_weights
       ga.norm_h = h;
       ga.norm_w = w.attn_norm;
       ga.norm_eps = c.eps;
+      // the GEMV itself applies RoPE, stores Q and appends K and V to the cache
+      ga.epilogue = EPI_DECODE_QKV;
+      ga.rope = ws.rope;
+      ga.pos = dlens;
+      ga.kv_cap = kv.cap;
+      ga.g[0].out = qb;
+      ga.g[0].kind = 1;
+      ga.g[1].out = ck + loff;
+      ga.g[1].kind = 3;
+      ga.g[2].out = cv + loff;
+      ga.g[2].kind = 2;
     }
     {
       ProfScope ps(KC_GEMM_QKV, st);
       hipError_t e = gemm(ga, 2);
       SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "decode gemm_qkv: %s", hipGetErrorString(e));
     }
-    {
+    if (!fused) {
       ProfScope ps(KC_QKV_FINALIZE, st);
       decode_qkv_kernel<AT><<<dim3((unsigned)B, 3), 256, 0, st>>>(p.Pq, p.Pk, p.Pv, ga.split, ps_, d, dh, dlens,
                                                                    ws.rope, qb, ck, cv, loff, kv.cap);
