@@ -405,16 +405,27 @@ __global__ void __launch_bounds__(256) decode_attention_kernel(const AT* __restr
   __syncthreads();
   const AT* kb = ck + layer_off + (int64_t)b * cap * d + h * dh;
   const AT* vb = cv + layer_off + (int64_t)b * cap * d + h * dh;
+  // P V work split (below); this thread's first PF value vectors are loaded
+  // now, so their latency overlaps the scores and the softmax
+  constexpr int PF = 16;
+  const int ng = 256 / nv;  // key groups
+  const int cg = tid % nv, kg = tid / nv;
+  uint4 vpre[PF];
+#pragma unroll
+  for (int u = 0; u < PF; ++u) {
+    const int j = kg + u * ng;
+    vpre[u] = (kg < ng && j < n) ? reinterpret_cast<const uint4*>(vb + (int64_t)j * d)[cg] : make_uint4(0, 0, 0, 0);
+  }
   float mx = -INFINITY;
   for (int j = tid; j < n; j += 256) {
     const uint4* kr = reinterpret_cast<const uint4*>(kb + (int64_t)j * d);
     float acc = 0.f;
-    for (int q0 = 0; q0 < nv; q0 += 8) {  // 8 vectors (128 B) of the row in flight
-      uint4 kv[8];
+    for (int q0 = 0; q0 < nv; q0 += 16) {  // 16 vectors (256 B) of the row in flight
+      uint4 kv[16];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) kv[u] = q0 + u < nv ? kr[q0 + u] : make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < 16; ++u) kv[u] = q0 + u < nv ? kr[q0 + u] : make_uint4(0, 0, 0, 0);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 16; ++u) {
         if (q0 + u >= nv) break;
         float x[VE];
         unpack16<AT>(kv[u], x);
@@ -441,13 +452,22 @@ __global__ void __launch_bounds__(256) decode_attention_kernel(const AT* __restr
   if (lane == 0) red[wave] = s;
   __syncthreads();
   s = (red[0] + red[1]) + (red[2] + red[3]);
-  const int ng = 256 / nv;  // key groups
-  const int cg = tid % nv, kg = tid / nv;
   float acc[VE];
 #pragma unroll
   for (int e = 0; e < VE; ++e) acc[e] = 0.f;
   if (kg < ng) {
-    for (int j0 = kg; j0 < n; j0 += 4 * ng) {
+    // keys kg, kg + ng, ... in increasing order: the prefetched ones first
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int j = kg + u * ng;
+      if (j >= n) break;
+      float x[VE];
+      unpack16<AT>(vpre[u], x);
+      const float p = z[j];
+#pragma unroll
+      for (int e = 0; e < VE; ++e) acc[e] = fmaf(p, x[e], acc[e]);
+    }
+    for (int j0 = kg + PF * ng; j0 < n; j0 += 4 * ng) {
       uint4 vv[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
