@@ -1,6 +1,13 @@
 """Benchmark of the pruned-and-skipped multimodal prefill on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llava15_7b] [--keep 128]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload stress] [--keep 288] [--skip-p 0.25]
+
+With no workload flags the step is the largest single-GPU configuration
+that both prunes and skips: the high-resolution stress shape (batch 4 x 2880
+visual tokens in 5 AnyRes tiles of 576, keep 288 per tile, LLaVA-1.5-7B-shaped
+decoder, each of the 2 x 32 sub-layer slots bypassed by every visual row with
+probability 0.25); the same JSON line then carries the LLaVA-1.5-7B keep-128
+batch-1 step as an extra field (`llava15_7b_keep128`).
 
 One step = the whole hot path over one batch of synthetic LLaVA-shaped input
 already resident in HBM: multi-layer scoring of the vision tokens
@@ -39,12 +46,15 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--workload", default="llava15_7b")
+    p.add_argument("--workload", default=None,
+                   help="workload name (default: the stress shape at keep 288, skip 0.25)")
     p.add_argument("--keep", type=int, default=None)
     p.add_argument("--layers", type=int, default=None)
     p.add_argument("--skip-p", type=float, default=None)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-layers", type=int, default=8)
+    p.add_argument("--cpu-layers", type=int, default=2)
+    p.add_argument("--no-secondary", action="store_true",
+                   help="do not add the LLaVA-1.5-7B keep-128 step to the default line")
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="run one plain device copy of this size after warm-up (counter calibration)")
     p.add_argument("--score-sweep", action="store_true",
@@ -82,7 +92,7 @@ def online_policy(w, dev, V):
                       w_unembed=unembed(w.dec, V, w.seed, dev))
 
 
-def build_inputs(w, dev):
+def build_inputs(w, dev, weights=None):
     from synth.decoder_inputs import layer_weights, text_rows, visual_src
     from synth.skip_inputs import (adaptive_scores, layer_mask, policy_lists, slc_tables)
     from synth.vision import vision_inputs
@@ -92,7 +102,7 @@ def build_inputs(w, dev):
     attn, feats = vision_inputs(w.score, w.seed)
     attn, feats = attn.to(dev), [f.to(dev) for f in feats]
     src, text = visual_src(w, dev), text_rows(w, dev)
-    W = [layer_weights(w.dec, l, w.seed, dev) for l in range(w.dec.L)]
+    W = weights if weights is not None else [layer_weights(w.dec, l, w.seed, dev) for l in range(w.dec.L)]
     if w.skip["kind"] in ("random_layer", "mask"):
         pol = SkipPolicy(kind="layer_mask", layer_mask=layer_mask(w))
     else:
@@ -143,14 +153,17 @@ def algorithmic(w, cu, codes, admit=None, V=0):
 
 def cpu_baseline(w, n_layers: int, W_dev=None):
     """Oracle (as it is) on a bounded sample: scoring+selection of every tile and
-    n_layers of the decoder, scaled to one step.  Decoder weights are the
-    benchmark's own (copied to host memory) when given."""
+    n_layers of the decoder with the oracle's own skip plan for the workload (the
+    per-layer mask, or Algorithm 1's admission on the same S_sa and SLC tables),
+    decoder time scaled to all layers.  Decoder weights are the benchmark's own
+    (copied to host memory) when given."""
     import threadpoolctl
+    from oracle import asl_skip as ak
     from oracle import decoder as odec
     from oracle import msv_prune as mp
     from synth.decoder_inputs import layer_weights, text_rows, visual_src
     from synth.vision import vision_inputs
-    from synth.skip_inputs import layer_mask
+    from synth.skip_inputs import adaptive_scores, layer_mask, policy_lists, slc_tables
 
     cores = len(os.sched_getaffinity(0))
     attn, feats = vision_inputs(w.score, w.seed)
@@ -162,20 +175,30 @@ def cpu_baseline(w, n_layers: int, W_dev=None):
     else:
         Wl = [{k: v.float().numpy() for k, v in layer_weights(w.dec, l, w.seed).items()}
               for l in range(n_layers)]
+    mode = "exact" if w.quota_mode == 1 else "literal"
     with threadpoolctl.threadpool_limits(cores):
         torch.set_num_threads(cores)
         t0 = time.perf_counter()
         tiles = [mp.prune_tile(A[g], [f[g] for f in Fs], w.score.keep, w.score.r_num,
-                               w.score.r_den, w.score.K, w.score.kmeans_iter)
+                               w.score.r_den, w.score.K, w.score.kmeans_iter, mode)
                  for g in range(w.score.G)]
         x, cu = mp.assemble(src, [t["idx"] for t in tiles], text, w.tiles_per_sample)
+        n_vis = [int(cu[b + 1] - cu[b]) - w.n_text for b in range(w.B)]
+        if w.skip["kind"] in ("random_layer", "mask"):
+            m = layer_mask(w)
+            col = (m[:, 0].astype(np.uint8) | (m[:, 1].astype(np.uint8) << 1))
+            per_sample = [np.repeat(col[:, None], n_vis[b], axis=1) for b in range(w.B)]
+        else:
+            L = w.dec.L
+            cap = min(w.score.n, w.score.keep + w.score.K)
+            sa, sf = slc_tables(policy_lists(w.skip["policy"], L, w.seed), L)
+            na, nf = ak.slc_normalize(sa, sf)
+            tgt, sel = ak.skip_targets(na, nf)
+            s_sa = adaptive_scores(w, w.tiles_per_sample * cap)
+            per_sample = [ak.plan(s_sa[b][:, :n_vis[b]], sel, tgt, w.skip["w1"], w.skip["w2"],
+                                  w.skip["T_skip"], L)[0] for b in range(w.B)]
+        codes = ak.pack_codes(per_sample, n_vis, w.n_text, w.dec.L)
         t1 = time.perf_counter()
-        m = layer_mask(w) if w.skip["kind"] in ("random_layer", "mask") else np.zeros((w.dec.L, 2), bool)
-        col = (m[:, 0].astype(np.uint8) | (m[:, 1].astype(np.uint8) << 1))
-        codes = np.zeros((w.dec.L, int(cu[-1])), np.uint8)
-        for b in range(w.B):
-            n_vis = int(cu[b + 1] - cu[b]) - w.n_text
-            codes[:, cu[b]:cu[b] + n_vis] = col[:, None]
         odec.prefill(x.astype(np.float32), Wl, cu, codes, w.dec, recipe="bf16",
                      dtype=np.float32, n_layers=n_layers)
         t2 = time.perf_counter()
@@ -183,10 +206,11 @@ def cpu_baseline(w, n_layers: int, W_dev=None):
     rows = int(cu[-1])
     return {"value": rows / t_step, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "ms_per_step_extrapolated": t_step * 1e3,
-            "sample": (f"oracle scoring+selection of all {w.score.G} tile(s) "
+            "extrapolated": n_layers < w.dec.L,
+            "sample": (f"oracle scoring+selection+skip plan of all {w.score.G} tile(s) "
                        f"({(t1 - t0):.2f} s) plus decoder layers 0..{n_layers - 1} of {w.dec.L} "
-                       f"({(t2 - t1):.2f} s, float32 with the bf16 rounding recipe), decoder "
-                       f"time scaled by {w.dec.L}/{n_layers}; {rows} rows")}
+                       f"({(t2 - t1):.2f} s, float32 with the bf16 rounding recipe, the oracle's own "
+                       f"skip codes), decoder time extrapolated by {w.dec.L}/{n_layers}; {rows} rows")}
 
 
 def score_sweep(w, dev, args):
@@ -311,34 +335,27 @@ def colmean_sweep(dev):
             torch.cuda.empty_cache()
 
 
-def main():
-    args = parse()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(see the sharding notes in DESIGN.md); use --gpus 1", file=sys.stderr)
-        sys.exit(2)
-    from synth import get_workload
+HEADLINE = {"workload": "stress", "keep": 288, "skip_p": 0.25}
+
+
+def run_step(w, args, dev, weights=None, online=False, projector_on=False, decode=0,
+             cpu=True, copy_probe_mib=0):
+    """Times `args.steps` whole steps of workload `w` and returns its result record
+    (without the contract's top-level fields).  `weights` reuses device weights
+    already generated for the same decoder and seed."""
     from paper_2609_34977_amd import _lib
     from paper_2609_34977_amd.pipeline import Pipeline
+    from paper_2609_34977_amd.profiling import recorded_traffic
 
-    w = get_workload(args.workload, keep=args.keep, L=args.layers, skip_p=args.skip_p)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    if args.score_sweep:
-        score_sweep(w, dev, args)
-        return
-    if args.colmean_sweep:
-        colmean_sweep(dev)
-        return
     t_setup = time.perf_counter()
-    attn, feats, src, text, W, pol = build_inputs(w, dev)
-    if args.online:
+    attn, feats, src, text, W, pol = build_inputs(w, dev, weights)
+    if online:
         pol = online_policy(w, dev, args.vocab)
     sc, dec = w.score, w.dec
     cfg = _lib.decoder_cfg(dec.L, dec.d, dec.H, dec.d_ff,
                            _lib.BF16 if dec.dtype == "bf16" else _lib.F32, dec.eps, dec.theta)
     projector = None
-    if args.projector:
+    if projector_on:
         from synth.decoder_inputs import projector_inputs, projector_weights
         projector = projector_weights(w, dev)
         src = projector_inputs(w, dev)
@@ -347,15 +364,15 @@ def main():
                     n_text=w.n_text, quota_mode=w.quota_mode, dec=cfg, weights=W, device=dev,
                     projector=projector)
     torch.cuda.synchronize()
-    print(f"# setup {time.perf_counter() - t_setup:.1f} s", file=sys.stderr, flush=True)
+    print(f"# {w.name}: setup {time.perf_counter() - t_setup:.1f} s", file=sys.stderr, flush=True)
 
     out = None
     for i in range(args.warmup):
         out = pipe.step(attn, feats, src, text, pol)
     torch.cuda.synchronize()
-    print("# warmup done", file=sys.stderr, flush=True)
-    if args.copy_probe_mib > 0:
-        a = torch.empty(args.copy_probe_mib << 20, dtype=torch.uint8, device=dev)
+    print(f"# {w.name}: warmup done", file=sys.stderr, flush=True)
+    if copy_probe_mib > 0:
+        a = torch.empty(copy_probe_mib << 20, dtype=torch.uint8, device=dev)
         b = torch.empty_like(a)
         b.copy_(a)
         torch.cuda.synchronize()
@@ -384,7 +401,7 @@ def main():
     prof = _lib.profile_read()
     _lib.profile_enable(False)
     _lib.profile_mask(None)
-    print("# timed steps done", file=sys.stderr, flush=True)
+    print(f"# {w.name}: timed steps done", file=sys.stderr, flush=True)
 
     ms = (t1 - t0) * 1e3 / args.steps
     cu, codes = out["cu"], out["codes"]
@@ -410,28 +427,26 @@ def main():
             roof = {"bound": "mfma", "achieved": ach, "peak": pk, "unit": "TFLOP/s", "frac": ach / pk}
     else:
         roof = {"bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": None}
-    from paper_2609_34977_amd.profiling import recorded_traffic
+    workload = (f"{w.name}_keep{sc.keep}" + (f"_skip{w.skip['p']:g}" if w.skip.get("kind") == "random_layer"
+                                               and w.name == "stress" else "")
+                + ("_online" if online else "") + ("_projector" if projector_on else ""))
     roof.update({"kernel": dom, "launches_per_step": prof[dom][0] // args.steps,
                  "avg_launch_us": prof[dom][1] * 1e3 / max(prof[dom][0], 1),
-                 "traffic": recorded_traffic(os.path.join(ROOT, "profiles", f"{dom}_traffic.json"), dom)
-                 if dom in ("gemm_gateup",) else None})
+                 "traffic": recorded_traffic(os.path.join(ROOT, "profiles", f"{dom}_traffic_{workload}.json"),
+                                             dom, workload, rows)})
     prefill_flops = sum(v[1] for v in alg.values())
     res = {
-        "metric": METRIC,
         "value": rows / (ms * 1e-3),
         "unit": "tokens/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": dec.dtype, "data": "synthetic",
-        "config": {"workload": f"{w.name}_keep{sc.keep}" + ("_online" if args.online else "")
-                   + ("_projector" if args.projector else ""),
+        "dtype": dec.dtype,
+        "config": {"workload": workload,
                    "batch": B, "tiles": sc.G,
                    "visual_tokens_per_tile": sc.n, "keep_per_tile": sc.keep,
                    "text_tokens": w.n_text, "decoder_rows": rows, "decoder_layers": dec.L,
                    "d_model": dec.d, "heads": dec.H, "d_ff": dec.d_ff,
-                   "skip": "online" if args.online else w.skip.get("kind"),
-                   "skip_p": None if args.online else w.skip.get("p"),
+                   "skip": "online" if online else w.skip.get("kind"),
+                   "skip_p": None if online else w.skip.get("p"),
                    "skipped_sublayer_slots": float((codes[:, :rows] != 0).mean()),
                    "parallelism": "single GPU"},
         "ms_per_sample": ms / B,
@@ -445,12 +460,51 @@ def main():
         "kernel_ms_per_step": {k: round(v, 4) for k, v in kernel_ms.items()},
         "launches_per_step": launches,
     }
-    if args.decode > 0:
+    if decode > 0:
         res["decode"] = decode_latency(w, pipe, out, dev, args)
-    if not args.no_cpu_baseline and not args.online and not args.projector:
-        print("# cpu baseline", file=sys.stderr, flush=True)
+    if cpu:
+        print(f"# {w.name}: cpu baseline", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, min(args.cpu_layers, dec.L), W)
-    print(json.dumps(res), flush=True)
+    return res, W
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see the sharding notes in DESIGN.md); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    from synth import get_workload
+
+    headline = args.workload is None
+    name = HEADLINE["workload"] if headline else args.workload
+    keep = args.keep if args.keep is not None or not headline else HEADLINE["keep"]
+    skip_p = args.skip_p if args.skip_p is not None or not headline else HEADLINE["skip_p"]
+    w = get_workload(name, keep=keep, L=args.layers, skip_p=skip_p)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.score_sweep:
+        score_sweep(w, dev, args)
+        return
+    if args.colmean_sweep:
+        colmean_sweep(dev)
+        return
+    cpu = not args.no_cpu_baseline and not args.online and not args.projector
+    res, W = run_step(w, args, dev, online=args.online, projector_on=args.projector, decode=args.decode,
+                      cpu=cpu, copy_probe_mib=args.copy_probe_mib)
+    line = {"metric": METRIC, "value": res.pop("value"), "unit": res.pop("unit"), "n_gpus": 1,
+            "steps": args.steps, "warmup": args.warmup, "ms_per_step": res.pop("ms_per_step"),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": res.pop("dtype"),
+            "data": "synthetic", "config": res.pop("config")}
+    line.update(res)
+    if headline and not args.no_secondary and not args.online and not args.projector:
+        w2 = get_workload("llava15_7b", L=args.layers)
+        same = w2.dec == w.dec and w2.seed == w.seed
+        r2, _ = run_step(w2, args, dev, weights=W if same else None, cpu=False)
+        line[r2["config"]["workload"]] = {k: r2[k] for k in ("value", "unit", "ms_per_step", "ms_per_sample",
+                                                             "effective_tokens_per_s", "roofline",
+                                                             "kernel_ms_per_step", "config")}
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":

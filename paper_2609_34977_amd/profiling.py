@@ -3,7 +3,8 @@
     python -m paper_2609_34977_amd.profiling stats --csv S_kernel_stats.csv \
         --bench-log bench.log --out profiles/NAME.md --command "..."
     python -m paper_2609_34977_amd.profiling traffic --fetch F.csv --write W.csv \
-        --copy-mib 256 --kernel-class gemm_gateup --out profiles/gemm_gateup_traffic
+        --copy-mib 256 --kernel-class gemm_gateup --workload W --rows R \
+        --out profiles/gemm_gateup_traffic_W
 
 `bench-table` turns bench.py JSON lines (one per workload) into a markdown
 table of step time, throughput and the dominant kernel's roofline fraction.
@@ -13,7 +14,9 @@ total time, with the bench line of the same run.
 
 F.csv / W.csv are rocprofv3 counter-collection CSVs of two runs of
 `bench.py --copy-probe-mib 256` (one with `--pmc FETCH_SIZE`, one with
-`--pmc WRITE_SIZE`).  The plain copy of known size in the same runs calibrates
+`--pmc WRITE_SIZE`) on one workload; the record names that workload
+(config.workload of the bench line) and its decoder row count, and bench.py
+uses it only for the same workload and rows.  The plain copy of known size in the same runs calibrates
 both counters (bytes the copy must read / write divided by what the counter
 reports for it); the per-launch traffic of the kernel class is the mean over
 its dispatches, scaled by that factor.  Writes <out>.json (read by bench.py,
@@ -32,10 +35,15 @@ import statistics
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 
-# kernel class -> (source files whose text defines its kernels, dispatch-name pattern)
+# kernel class -> (source files whose text defines its kernels, pattern of the dispatches
+# that make one launch of the class, pattern of the one dispatch counted per launch)
+_GEMM_SRC = ("csrc/gemm.hip", "csrc/kernels.h", "csrc/common.h")
 CLASSES = {
-    "gemm_gateup": (("csrc/gemm.hip", "csrc/kernels.h", "csrc/common.h"),
-                    r"gemm_stream_kernel<\d+, \d+, true\b|gemm_bf16_kernel<\d+, \d+, \d+, \d+, \d+, true"),
+    "gemm_gateup": (_GEMM_SRC,
+                    r"gemm_stream_kernel<\d+, \d+, true\b|gemm_bf16_kernel<\d+, \d+, \d+, \d+, \d+, true"
+                    r"|gemm_tile_kernel<\d+, true\b|swiglu_tail_reduce_kernel",
+                    r"gemm_stream_kernel<\d+, \d+, true\b|gemm_bf16_kernel<\d+, \d+, \d+, \d+, \d+, true"
+                    r"|gemm_tile_kernel<\d+, true\b"),
 }
 
 
@@ -47,14 +55,17 @@ def kernel_source_hash(kernel_class: str) -> str:
     return h.hexdigest()
 
 
-def recorded_traffic(path: str, kernel_class: str):
-    """Bytes per launch recorded for the class, or None if absent or stale."""
+def recorded_traffic(path: str, kernel_class: str, workload: str, rows: int):
+    """Bytes per launch recorded for the class on this workload and decoder row count,
+    or None if there is no such record or the kernel sources changed since."""
     try:
         with open(path) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_class") != kernel_class:
+    if rec.get("kernel_class") != kernel_class or kernel_class not in CLASSES:
+        return None
+    if rec.get("workload") != workload or rec.get("rows") != rows:
         return None
     if rec.get("source_sha256") != kernel_source_hash(kernel_class):
         return None
@@ -82,29 +93,33 @@ def _calibration(rows, expect_kib: float):
 
 def traffic(args):
     pat = re.compile(CLASSES[args.kernel_class][1])
+    primary = re.compile(CLASSES[args.kernel_class][2])
     expect_kib = args.copy_mib * 1024.0
-    out = {"kernel_class": args.kernel_class,
+    out = {"kernel_class": args.kernel_class, "workload": args.workload, "rows": args.rows,
            "source_sha256": kernel_source_hash(args.kernel_class)}
     per = {}
     for counter, path in (("FETCH_SIZE", args.fetch), ("WRITE_SIZE", args.write)):
         rows = _dispatches(path, counter)
         factor, measured = _calibration(rows, expect_kib)
         vals = [v for name, v in rows if pat.search(name)]
-        if not vals:
+        launches = sum(1 for name, _ in rows if primary.search(name))
+        if not vals or not launches:
             raise SystemExit(f"no {args.kernel_class} dispatch in {path}")
-        per[counter] = {"mean_kib_per_dispatch": statistics.fmean(vals), "dispatches": len(vals),
+        # a launch of the class may be more than one dispatch (e.g. the SwiGLU tail reduction)
+        per[counter] = {"mean_kib_per_dispatch": sum(vals) / launches, "dispatches": launches,
                         "copy_kib_measured": measured, "copy_kib_expected": expect_kib,
                         "factor": factor,
-                        "bytes_per_launch": statistics.fmean(vals) * factor * 1024.0}
+                        "bytes_per_launch": sum(vals) / launches * factor * 1024.0}
     out["counters"] = per
     out["bytes_per_launch"] = per["FETCH_SIZE"]["bytes_per_launch"] + per["WRITE_SIZE"]["bytes_per_launch"]
     out["commands"] = args.command or []
     with open(args.out + ".json", "w") as f:
         json.dump(out, f, indent=1)
-    lines = [f"# HBM traffic of `{args.kernel_class}` (rocprofv3 counters)", "",
+    lines = [f"# HBM traffic of `{args.kernel_class}` on `{args.workload}` ({args.rows} decoder rows; "
+             "rocprofv3 counters)", "",
              "Commands (from the repository root, one MI355X):", "", "```"]
     lines += out["commands"] + ["```", "",
-                                "| counter | dispatches | mean KiB / dispatch | copy KiB measured | copy KiB expected | factor | bytes / launch |",
+                                "| counter | launches | mean KiB / launch | copy KiB measured | copy KiB expected | factor | bytes / launch |",
                                 "|---|---|---|---|---|---|---|"]
     for c, v in per.items():
         lines.append(f"| {c} | {v['dispatches']} | {v['mean_kib_per_dispatch']:.1f} | "
@@ -206,6 +221,8 @@ def main():
     t.add_argument("--write", required=True)
     t.add_argument("--copy-mib", type=float, required=True)
     t.add_argument("--kernel-class", default="gemm_gateup")
+    t.add_argument("--workload", required=True, help="config.workload of the bench line")
+    t.add_argument("--rows", type=int, required=True, help="decoder rows of the bench line")
     t.add_argument("--out", required=True)
     t.add_argument("--command", action="append")
     args = p.parse_args()

@@ -87,3 +87,42 @@ def test_score_large_tile_batch_matches_per_tile():
         one = L.score(attn[g:g + 1].contiguous().cuda(), [f[g:g + 1].contiguous().cuda() for f in feats], 89)
         for k in ("a", "cluster", "s", "m"):
             assert torch.equal(allr[k][g:g + 1], one[k]), (g, k)
+
+
+@pytest.mark.gpu
+def test_score_zero_norm_rows():
+    """Feature rows that are exactly zero (cosine with a zero row is 0): some only in the
+    middle layer, some only in the last, some in both, one of them an anchor's row; the
+    anchor set, clusters and selection inputs must still match the oracle."""
+    L = need_gpu()
+    w = get_workload("llava15_7b", keep=128)
+    attn, feats = vision_inputs(w.score, 11)
+    fm, fl = feats[0].clone(), feats[-1].clone()
+    a_host = attn[0, :, 1:].sum(0)
+    top = int(torch.argmax(a_host))            # the strongest anchor (patch index)
+    for i in (3, 40, 41, 200, 575):            # zero in the last layer only
+        fl[0, 1 + i] = 0
+    for i in (7, 41, 300):                     # zero in the middle layer (41: in both)
+        fm[0, 1 + i] = 0
+    fl[0, 1 + top] = 0                         # an anchor with a zero last-layer row
+    feats = [fm, fl]
+    n_anchor = (128 * 7) // 10
+    log(f"[score] zero-norm rows, anchor {top} zeroed")
+    out = L.score(attn.cuda(), [f.cuda() for f in feats], n_anchor, 4, w.score.kmeans_iter)
+    torch.cuda.synchronize()
+    cl = out["cluster"].cpu().numpy()[0]
+    s = out["s"].cpu().numpy()[0]
+    m = out["m"].cpu().numpy()[0]
+    o = oracle_tiles(attn, feats, 128, 7, 10, 4, w.score.kmeans_iter)[0]
+    assert np.array_equal(out["a"].cpu().numpy()[0], o["a"])
+    assert top in set(o["anchors"]) and cl[top] < 0
+    assert o["margin"].min() > 1e-4, "input too close to a K-means tie for an exact check"
+    assert np.array_equal(cl, o["cluster"])
+    na = o["cluster"] >= 0
+    err = np.abs(s[na] - o["s"][na]) / np.maximum(1.0, np.abs(o["s"][na]))
+    assert err.max() <= 1e-5, err.max()
+    merr = np.abs(m - o["mvec"]) / np.maximum(1.0, np.abs(o["mvec"]))
+    assert merr.max() <= 1e-5, merr.max()
+    # a row that is zero in the last layer has no similarity to any anchor
+    for i in (3, 40, 41, 200, 575):
+        assert m[i] == 0.0 and o["mvec"][i] == 0.0
