@@ -161,6 +161,33 @@ spider_status spider_score(int G, int n, int H, int d_v, int n_layers,
                            void* workspace, size_t workspace_bytes, spider_stream stream);
 
 /* ------------------------------------------------------------------------
+ * spider_score_noalloc - spider_score without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  Arguments, outputs,
+ * limits and results are those of spider_score (bit-identical outputs); the
+ * scratch space is a static device array of SPIDER_SCORE_SCRATCH_BYTES that
+ * every GPU the library runs on holds until the process ends.  Sizes whose
+ * spider_score_workspace_size exceeds it are rejected with
+ * SPIDER_ERR_WORKSPACE before any HIP call (e.g. 32 MiB holds about 50 tiles
+ * of 576 patches with two tapped layers of width 1024 and K = 4).  The call
+ * allocates nothing (no hipMalloc / hipFree); its first call on a device looks
+ * up that device's scratch address.  All calls on one GPU share its scratch:
+ * calls that overlap on one GPU (concurrent streams, or other host threads)
+ * race and must be serialised by the caller; a later call on the same stream
+ * is ordered after an earlier one and needs nothing.
+ * ------------------------------------------------------------------------ */
+#define SPIDER_SCORE_SCRATCH_BYTES (32u << 20)
+
+spider_status spider_score_noalloc(int G, int n, int H, int d_v, int n_layers,
+                                   const float* cls_attn, int64_t attn_stride_g,
+                                   int64_t attn_stride_h, int attn_col0,
+                                   const void* const* feats, spider_dtype feat_dtype,
+                                   int64_t feat_stride_g, int64_t feat_stride_row, int feat_row0,
+                                   int n_anchor, int K, int kmeans_max_iter,
+                                   float* a_out, int32_t* cluster_out, float* s_out, float* m_out,
+                                   spider_stream stream);
+
+/* ------------------------------------------------------------------------
  * spider_select - quotas, complementary selection, spatial-order union
  * (Sec. 4.1.2, Eq. 2; Sec. 4.1) and optional assembly of the decoder input.
  * Per tile g (cluster/s as written by spider_score, row stride n):

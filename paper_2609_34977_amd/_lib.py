@@ -58,6 +58,8 @@ _SIGS = {
     "spider_score_workspace_size": ([_I, _I, _I, _I, _I], _SZ),
     "spider_score": ([_I, _I, _I, _I, _I, _VP, _I64, _I64, _I, ctypes.POINTER(_VP), _I, _I64, _I64,
                       _I, _I, _I, _I, _VP, _VP, _VP, _VP, _VP, _SZ, _VP], _I),
+    "spider_score_noalloc": ([_I, _I, _I, _I, _I, _VP, _I64, _I64, _I, ctypes.POINTER(_VP), _I, _I64, _I64,
+                              _I, _I, _I, _I, _VP, _VP, _VP, _VP, _VP], _I),
     "spider_select": ([_I, _I, _VP, _VP, _I, _I, _I, _I, _VP, _VP, _I, _I, _VP, _I64, _I, _I, _VP,
                        _I, _VP, _VP, _VP], _I),
     "spider_slc_policy": ([_I, _VP, _VP, _D, _VP, _VP], _I),
@@ -207,9 +209,11 @@ def cls_attention(q: torch.Tensor, k: torch.Tensor, scale: float, out: Optional[
 
 def score(cls_attn: Optional[torch.Tensor], feats: Sequence[torch.Tensor], n_anchor: int, K: int = 4,
           max_iter: int = 10, attn_col0: int = 1, feat_row0: int = 1, n: Optional[int] = None,
-          a: Optional[torch.Tensor] = None):
+          a: Optional[torch.Tensor] = None, noalloc: bool = False):
     """MSV-Prune scoring of G tiles.  cls_attn [G,H,T] fp32, feats list of [G,T,d_v];
-    or cls_attn None and a [G, n] fp32 given anchor scores (encoders without [CLS])."""
+    or cls_attn None and a [G, n] fp32 given anchor scores (encoders without [CLS]).
+    With noalloc the call goes to spider_score_noalloc (the library's static scratch
+    instead of a workspace)."""
     f0 = feats[0]
     d_v = f0.shape[-1]
     if cls_attn is None:
@@ -232,9 +236,16 @@ def score(cls_attn: Optional[torch.Tensor], feats: Sequence[torch.Tensor], n_anc
     s = torch.empty(G, n, dtype=torch.float32, device=dev)
     m = torch.empty(G, n, dtype=torch.float32, device=dev)
     L = lib()
+    fptr = (ctypes.c_void_p * len(feats))(*[f.data_ptr() for f in feats])
+    if noalloc:
+        _check(L.spider_score_noalloc(G, n, H, d_v, len(feats), _ptr(cls_attn),
+                                      cls_attn.stride(0) if cls_attn is not None else 0,
+                                      cls_attn.stride(1) if cls_attn is not None else 0, attn_col0, fptr,
+                                      _dt(f0), f0.stride(0), f0.stride(1), feat_row0, n_anchor, K, max_iter,
+                                      _ptr(a), _ptr(cl), _ptr(s), _ptr(m), _stream(dev)))
+        return {"a": a, "cluster": cl, "s": s, "m": m}
     wsz = L.spider_score_workspace_size(G, n, d_v, len(feats), K)
     ws = _ws(wsz, dev)
-    fptr = (ctypes.c_void_p * len(feats))(*[f.data_ptr() for f in feats])
     _check(L.spider_score(G, n, H, d_v, len(feats), _ptr(cls_attn),
                           cls_attn.stride(0) if cls_attn is not None else 0,
                           cls_attn.stride(1) if cls_attn is not None else 0, attn_col0, fptr, _dt(f0),

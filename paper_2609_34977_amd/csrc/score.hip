@@ -27,6 +27,7 @@
 #include <algorithm>
 #include <cfloat>
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 
@@ -886,4 +887,64 @@ extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers
   SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "spider_score: cluster kernels failed: %s",
                  hipGetErrorString(e));
   return SPIDER_OK;
+}
+
+// ------------------------------------------------------------------ no-allocation variant
+// Scratch of spider_score_noalloc: a file-scope device array, so the call needs
+// no device allocation (for callers that cannot allocate, e.g. under graph
+// capture or in a serving loop).  Every GPU the library runs on holds its own
+// copy until the process ends.  Host code never uses the array's name as an
+// address: the device address is looked up once per device with
+// hipGetSymbolAddress and kept in g_scratch_ptr.
+static __device__ __align__(256) uint8_t scratch[SPIDER_SCORE_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's copy of the scratch array (looked up on the
+// first call made with that device current).
+spider_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  SPIDER_HIP(hipGetDevice(&dev));
+  SPIDER_REQUIRE(dev >= 0 && dev < kMaxDevices, SPIDER_ERR_UNSUPPORTED,
+                 "spider_score_noalloc: device %d beyond the %d the library tracks", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    SPIDER_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    SPIDER_REQUIRE(p != nullptr && ((uintptr_t)p % 256) == 0, SPIDER_ERR_HIP,
+                   "spider_score_noalloc: scratch address of device %d is not usable", dev);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SPIDER_OK;
+}
+}  // namespace
+
+extern "C" spider_status spider_score_noalloc(int G, int n, int H, int d_v, int n_layers,
+                                              const float* cls_attn, int64_t attn_stride_g,
+                                              int64_t attn_stride_h, int attn_col0,
+                                              const void* const* feats, spider_dtype feat_dtype,
+                                              int64_t feat_stride_g, int64_t feat_stride_row,
+                                              int feat_row0, int n_anchor, int K, int kmeans_max_iter,
+                                              float* a_out, int32_t* cluster_out, float* s_out,
+                                              float* m_out, spider_stream stream) {
+  clear_error();
+  SPIDER_REQUIRE(G >= 1 && n >= 1 && d_v >= 1 && n_layers >= 1 && K >= 1, SPIDER_ERR_INVALID_ARG,
+                 "spider_score_noalloc: G, n, d_v, n_layers and K must be >= 1");
+  const size_t need = score_ws_layout(G, n, d_v, n_layers, K, nullptr, nullptr);
+  SPIDER_REQUIRE(need <= (size_t)SPIDER_SCORE_SCRATCH_BYTES, SPIDER_ERR_WORKSPACE,
+                 "spider_score_noalloc: these sizes need %zu bytes of scratch, the static scratch "
+                 "holds %zu (use spider_score with a workspace)",
+                 need, (size_t)SPIDER_SCORE_SCRATCH_BYTES);
+  void* ws = nullptr;
+  const spider_status st = scratch_of_current_device(&ws);
+  if (st != SPIDER_OK) return st;
+  // the kernels write every scratch element they read: stale contents from an
+  // earlier call on this device need no clearing
+  return spider_score(G, n, H, d_v, n_layers, cls_attn, attn_stride_g, attn_stride_h, attn_col0, feats,
+                      feat_dtype, feat_stride_g, feat_stride_row, feat_row0, n_anchor, K, kmeans_max_iter,
+                      a_out, cluster_out, s_out, m_out, ws, SPIDER_SCORE_SCRATCH_BYTES, stream);
 }

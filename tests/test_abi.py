@@ -135,6 +135,20 @@ def test_score_validation_before_any_hip_call(L):
     assert L.spider_score_workspace_size(0, 576, 1024, 2, 4) == 0
 
 
+def test_score_noalloc_rejects_sizes_beyond_its_scratch_before_any_hip_call(L):
+    def call(G, n=576, d_v=1024, K=4):
+        feats = (ctypes.c_void_p * 2)(0x1000, 0x1000)
+        return L.spider_score_noalloc(G, n, 16, d_v, 2, 0x1000, 16 * (n + 1), n + 1, 1, feats, 1,
+                                      (n + 1) * d_v, d_v, 1, 89, K, 10, 0x1000, 0x1000, 0x1000, None, None)
+    limit = 32 << 20
+    per_tile = L.spider_score_workspace_size(1, 576, 1024, 2, 4)
+    too_many = limit // per_tile + 8
+    assert L.spider_score_workspace_size(too_many, 576, 1024, 2, 4) > limit
+    assert call(too_many) == WORKSPACE
+    assert b"static scratch" in L.spider_last_error()
+    assert call(0) == INVALID
+
+
 def _select_call(L, **kw):
     a = dict(G=1, n=576, cl=0x1000, s=0x1000, na=89, nc=39, K=4, qm=0, idx=0x1000, cnt=0x1000,
              cap=132, tps=1, src=None, ssg=0, dm=0, dt=1, text=None, nt=0, x=None, cu=None)
