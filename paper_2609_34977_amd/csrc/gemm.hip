@@ -295,12 +295,55 @@ __device__ __forceinline__ SoftStat soft_merge(SoftStat a, SoftStat b) {
   return {m, ea * a.s + eb * b.s, ea * fmaf(a.s, da, a.t) + eb * fmaf(b.s, db, b.t)};
 }
 
+// 16-byte-per-lane DMA from global memory into LDS at byte offset `lds` (+16
+// per lane), issued as inline assembly: the compiler does not track an LDS
+// DMA it cannot see, so its own LDS-read waits stay exact counts (with the
+// builtin, any DMA in flight turns every fragment wait into a wait for all
+// LDS reads).  Completion is the caller's business: dma_wait_barrier().
+// `lds` must be the same in every lane.  NT: non-temporal (data read once).
+// (m0 is declared clobbered on purpose: the compiler sets it before each of its
+// own LDS DMAs, and clang warns about clobbering a reserved register)
+#pragma clang diagnostic ignored "-Winline-asm"
+template <bool NT = false>
+__device__ __forceinline__ void dma16(const uint16_t* g, uint32_t lds) {
+  lds = __builtin_amdgcn_readfirstlane(lds);  // wave-uniform by construction
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(g), "s"(lds) : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+// At most N of this wave's DMAs still in flight, then the block barrier: the
+// older DMAs of every wave have landed and every wave is done reading what
+// the next DMAs overwrite.  One assembly statement with a memory clobber, so
+// no LDS access moves across it.
+template <int N = 0>
+__device__ __forceinline__ void dma_wait_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+// Every DMA of this wave complete (no barrier), as a compiler fence.
+__device__ __forceinline__ void dma_wait_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// LDS byte offset of a __shared__ address (the DMA's M0 operand).
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint8_t*)p;
+}
+
+// Tile layout shared by the GEMM kernels: 16-byte chunk c of a 128-byte tile
+// row r is stored in slot c ^ ((r >> 1) & 7).  An LDS pass of a 16-byte read
+// serves 16 lanes; a fragment read has those lanes on 16 consecutive rows, so
+// even and odd rows each cover the 8 slots and the 16 lanes hit 16 distinct
+// bank groups (with c ^ (r & 7), rows r and r + 8 collide).
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+
 template <int MT, int LEAD, bool DUAL, bool LENS = false>
 __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   constexpr int KB = 64;
   // weights are read once: the SwiGLU and lens launches (split 1, whole K per
   // block) load them non-temporal (measured 2-6 % faster there, no gain with split-K)
-  constexpr int kWeightPolicy = (DUAL || LENS) ? 2 : 0;
+  constexpr bool kWeightNT = DUAL || LENS;
   constexpr int BM = 32 * MT;
   constexpr int BN = DUAL ? 64 : 128;  // output columns per block
   constexpr int STAGES = LEAD + 1;
@@ -330,21 +373,21 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   const int wrow0 = tc.n0 + 32 * (DUAL ? (wave & 1) : wave);  // first weight row of this wave
   const uint16_t* W = reinterpret_cast<const uint16_t*>(DUAL && wave >= 2 ? G.W2 : G.W);
   // weight DMA: instruction q fills the wave's rows 8q..8q+7; lane l takes row
-  // 8q + l/8 and chunk (l%8) ^ (l/8)
+  // 8q + l/8, slot l%8
   const uint16_t* pw[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
-    pw[q] = W + (int64_t)(wrow0 + 8 * q + (lane >> 3)) * a.K + kbeg + 8 * ((lane & 7) ^ (lane >> 3));
+  for (int q = 0; q < 4; ++q)  // LDS weight row 32 wave + 8q + l/8
+    pw[q] = W + (int64_t)(wrow0 + 8 * q + (lane >> 3)) * a.K + kbeg + 8 * ((lane & 7) ^ swz(8 * q + (lane >> 3)));
 
   // activation DMA: instruction j of this wave fills tile rows 8g..8g+7,
-  // g = wave*MT + j; lane l takes row 8g + l/8 and chunk (l%8) ^ (l/8)
+  // g = wave*MT + j; lane l takes row 8g + l/8, slot l%8
   const uint16_t* pa[MT];
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
     const int g = wave * MT + j;
     const int r = min(tc.m0 + 8 * g + (lane >> 3), M - 1);
     const int src = G.rows ? G.rows[r] : r;
-    const int c = (lane & 7) ^ (lane >> 3);
+    const int c = (lane & 7) ^ swz(8 * g + (lane >> 3));
     pa[j] = reinterpret_cast<const uint16_t*>(G.A) + (int64_t)src * a.lda + kbeg + 8 * c;
   }
 
@@ -352,20 +395,14 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
 #pragma unroll
   for (int i = 0; i < MT; ++i) acc[i] = floatx16{};
 
+  const uint32_t ring_lds = lds_offset(ring);
   auto issue = [&](int kb, auto S) {
     constexpr int st = decltype(S)::value;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      __builtin_amdgcn_global_load_lds(
-          reinterpret_cast<const void*>(pw[q] + kb * KB),
-          (__attribute__((address_space(3))) void*)(ring + st * STAGE_BYTES + A_BYTES + (wave * 4 + q) * 1024),
-          16, 0, kWeightPolicy);
+      dma16<kWeightNT>(pw[q] + kb * KB, ring_lds + st * STAGE_BYTES + A_BYTES + (wave * 4 + q) * 1024);
 #pragma unroll
-    for (int j = 0; j < MT; ++j)
-      __builtin_amdgcn_global_load_lds(
-          reinterpret_cast<const void*>(pa[j] + kb * KB),
-          (__attribute__((address_space(3))) void*)(ring + st * STAGE_BYTES + (wave * MT + j) * 1024), 16,
-          0, 0);
+    for (int j = 0; j < MT; ++j) dma16(pa[j] + kb * KB, ring_lds + st * STAGE_BYTES + (wave * MT + j) * 1024);
   };
   // Wave tile (2 x 2 over the block): rows [32 MH mh, 32 MH (mh + 1)) against LDS
   // weight rows [64 nh, 64 nh + 64) -- output columns n0 + 64 nh.. (dual: nh 0
@@ -379,7 +416,7 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
     const uint8_t* at = tile + (32 * MH * mh + lo) * 128;
     bf16x8 wf[2][2], af[2][MH];
     auto frags = [&](int q, bf16x8 (&w)[2], bf16x8 (&x)[MH]) {
-      const int c = 16 * ((4 * hi + q) ^ (lo & 7));
+      const int c = 16 * ((4 * hi + q) ^ swz(lo));
 #pragma unroll
       for (int t = 0; t < 2; ++t)
         w[t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wt + t * 32 * 128 + c));
@@ -403,28 +440,25 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
 
   if (nkb > 0) {
     static_for<0, LEAD>([&](auto P) { issue(min((int)P.value, nkb - 1), P); });
-    wait_vmcnt<(LEAD - 1) * PER_IT>();
-    __builtin_amdgcn_s_barrier();
-    // EXACT: all loads issued here are consumed later, so the count holds; in
-    // the remainder the compiler may drop unused weight loads, so wait for all
+    dma_wait_barrier<(LEAD - 1) * PER_IT>();
     // k-block kb+LEAD goes to the slot that iteration kb-1 consumed (free since
-    // its barrier), before the MMAs of kb, so the loads overlap them
-    auto body = [&](int kb, auto J, auto EXACT) {
+    // its barrier), before the MMAs of kb, so the loads overlap them; every
+    // iteration issues the same DMAs (the last k-block again at the end), so
+    // the count of DMAs still in flight is exact
+    auto body = [&](int kb, auto J) {
       constexpr int j = decltype(J)::value;
       issue(min(kb + LEAD, nkb - 1), std::integral_constant<int, (j + LEAD) % STAGES>{});
       compute(J);
-      if constexpr (decltype(EXACT)::value) wait_vmcnt<(LEAD - 1) * PER_IT>();
-      else wait_vmcnt<0>();
-      __builtin_amdgcn_s_barrier();
+      dma_wait_barrier<(LEAD - 1) * PER_IT>();
     };
     int k0 = 0;
     for (; k0 + STAGES <= nkb; k0 += STAGES)
-      static_for<0, STAGES>([&](auto J) { body(k0 + J.value, J, std::true_type{}); });
+      static_for<0, STAGES>([&](auto J) { body(k0 + J.value, J); });
     const int rem = nkb - k0;
     static_for<0, STAGES>([&](auto J) {
-      if (J.value < rem) body(k0 + J.value, J, std::false_type{});
+      if (J.value < rem) body(k0 + J.value, J);
     });
-    wait_vmcnt<0>();
+    dma_wait_all();
   }
 
   // D layout of 32x32 MFMA: n = lane % 32, m = 8*(r/4) + 4*(lane/32) + r%4
@@ -643,16 +677,17 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
   const int kbeg = s * kps;
   const int kend = min(a.K, kbeg + kps);
   const int nkb = kend > kbeg ? (kend - kbeg) / KB : 0;
-  const int chunk = 8 * ((lane & 7) ^ (lane >> 3));
+  auto chunk_of = [&](int r) { return 8 * ((lane & 7) ^ swz(r)); };
 
   // activation DMA: instruction j of this wave fills tile rows 8g..8g+7,
-  // g = wave*A_PER_WAVE + j; lane l takes row 8g + l/8, chunk (l%8) ^ (l/8)
+  // g = wave*A_PER_WAVE + j; lane l takes row 8g + l/8, slot l%8
   const uint16_t* pa[A_PER_WAVE];
 #pragma unroll
   for (int j = 0; j < A_PER_WAVE; ++j) {
-    const int r = min(m0 + 8 * (wave * A_PER_WAVE + j) + (lane >> 3), M - 1);
+    const int tr = 8 * (wave * A_PER_WAVE + j) + (lane >> 3);
+    const int r = min(m0 + tr, M - 1);
     const int src = G.rows ? G.rows[r] : r;
-    pa[j] = reinterpret_cast<const uint16_t*>(G.A) + (int64_t)src * a.lda + kbeg + chunk;
+    pa[j] = reinterpret_cast<const uint16_t*>(G.A) + (int64_t)src * a.lda + kbeg + chunk_of(tr);
   }
   // weight DMA: instruction j of this wave fills stage weight rows 8g..8g+7, g = 8*wave + j
   const uint16_t* pw[8];
@@ -677,7 +712,7 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
       W = reinterpret_cast<const uint16_t*>(G.W);
       row = n0 + wr;
     }
-    pw[j] = W + (int64_t)row * a.K + kbeg + chunk;
+    pw[j] = W + (int64_t)row * a.K + kbeg + chunk_of(wr);
   }
 
   // row tiles of this wave that hold rows < M (the rest skip their MMAs)
@@ -691,18 +726,16 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
 
   // DMA instruction p (of NP per wave and k-block) of k-block kb into stage S
   constexpr int NP = A_PER_WAVE + 8;
+  // LDS offset of the ring (the DMA takes its LDS destination from M0)
+  const uint32_t ring_lds = lds_offset(ring);
   auto issue_piece = [&](int kb, auto S, auto Pc) {
     constexpr int st = decltype(S)::value;
     constexpr int p = decltype(Pc)::value;
-    uint8_t* base = ring + st * STAGE_BYTES;
+    const uint32_t base = ring_lds + st * STAGE_BYTES;
     if constexpr (p < A_PER_WAVE)
-      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(pa[p] + kb * KB),
-                                       (__attribute__((address_space(3))) void*)(base + (wave * A_PER_WAVE + p) * 1024),
-                                       16, 0, 0);
+      dma16(pa[p] + kb * KB, base + (wave * A_PER_WAVE + p) * 1024);
     else
-      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(pw[p - A_PER_WAVE] + kb * KB),
-                                       (__attribute__((address_space(3))) void*)(base + A_BYTES + (8 * wave + p - A_PER_WAVE) * 1024),
-                                       16, 0, 0);
+      dma16(pw[p - A_PER_WAVE] + kb * KB, base + A_BYTES + (8 * wave + p - A_PER_WAVE) * 1024);
   };
 
   // weight tile u of the wave: LDS weight rows wrow(u) .. +31
@@ -715,14 +748,14 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
   // issued between the MMA groups of the first two k-steps (a burst of all of
   // them at once stalls the wave before its MMAs; spread over all four k-steps
   // the last ones land too late), measured 10-15 % faster than either.
-  auto compute = [&](auto S, int kbn, auto SN) {
+  auto compute = [&](auto S, int kbn, auto SN, auto FULL) {
     constexpr int st = decltype(S)::value;
     const uint8_t* tile = ring + st * STAGE_BYTES;
     const uint8_t* at = tile + (32 * MH * mh + lo) * 128;
     const uint8_t* wt = tile + A_BYTES + lo * 128;
     bf16x8 wf[2][4], af[2][MH];
     auto frags = [&](int q, bf16x8 (&w)[4], bf16x8 (&x)[MH]) {
-      const int c = 16 * ((4 * hi + q) ^ (lo & 7));
+      const int c = 16 * ((4 * hi + q) ^ swz(lo));
 #pragma unroll
       for (int u = 0; u < 4; ++u)
         w[u] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wt + wrow(u) * 128 + c));
@@ -738,7 +771,7 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
       __builtin_amdgcn_sched_barrier(0);
       static_for<0, MH>([&](auto I) {
         constexpr int i = I.value;
-        if (i < live) {
+        if (decltype(FULL)::value || i < live) {
 #pragma unroll
           for (int u = 0; u < 4; ++u)
             acc[i][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][i], wf[q & 1][u], acc[i][u], 0, 0, 0);
@@ -755,21 +788,28 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
 
   if (nkb > 0) {
     static_for<0, NP>([&](auto P) { issue_piece(0, std::integral_constant<int, 0>{}, P); });
-    wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    auto body = [&](int kb, auto J) {
-      constexpr int j = decltype(J)::value;
-      // the next k-block (the last one again at the end) into the other stage
-      compute(J, min(kb + 1, nkb - 1), std::integral_constant<int, j ^ 1>{});
-      wait_vmcnt<0>();
-      __builtin_amdgcn_s_barrier();
+    dma_wait_barrier();
+    // Waves whose row tiles all hold rows < M (every block but the last row
+    // tile) run a copy of the loop without the per-tile guards: a branch
+    // inside the MMA groups splits the loop into basic blocks, across which
+    // the compiler can only wait for every outstanding LDS read, so each
+    // k-step would also wait for the next step's fragments.
+    auto run = [&](auto FULL) {
+      auto body = [&](int kb, auto J) {
+        constexpr int j = decltype(J)::value;
+        // the next k-block (the last one again at the end) into the other stage
+        compute(J, min(kb + 1, nkb - 1), std::integral_constant<int, j ^ 1>{}, FULL);
+        dma_wait_barrier();
+      };
+      int kb = 0;
+      for (; kb + 2 <= nkb; kb += 2) {
+        body(kb, std::integral_constant<int, 0>{});
+        body(kb + 1, std::integral_constant<int, 1>{});
+      }
+      if (kb < nkb) body(kb, std::integral_constant<int, 0>{});
     };
-    int kb = 0;
-    for (; kb + 2 <= nkb; kb += 2) {
-      body(kb, std::integral_constant<int, 0>{});
-      body(kb + 1, std::integral_constant<int, 1>{});
-    }
-    if (kb < nkb) body(kb, std::integral_constant<int, 0>{});
+    if (live == MH) run(std::true_type{});
+    else run(std::false_type{});
   }
 
   // D layout of the 32x32 MMA: column lane % 32, row 8 (r / 4) + 4 (lane / 32) + r % 4
