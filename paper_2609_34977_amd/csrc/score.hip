@@ -47,6 +47,15 @@ struct Feat<float> {
     o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
   }
   __device__ static inline float load1(const float* p) { return *p; }
+  // 8 consecutive elements kept raw while in flight
+  struct Raw {
+    floatx4 a, b;
+  };
+  __device__ static inline Raw load8_raw(const float* p) {
+    return {*reinterpret_cast<const floatx4*>(p), *reinterpret_cast<const floatx4*>(p + 4)};
+  }
+  __device__ static inline float raw_at(const Raw& v, int e) { return e < 4 ? v.a[e] : v.b[e - 4]; }
+  static constexpr int kPrepRowBatch = 4;
 };
 template <>
 struct Feat<uint16_t> {
@@ -61,6 +70,12 @@ struct Feat<uint16_t> {
     }
   }
   __device__ static inline float load1(const uint16_t* p) { return bf16_bits_to_f32(*p); }
+  typedef u32x4 Raw;
+  __device__ static inline Raw load8_raw(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+  __device__ static inline float raw_at(const Raw& v, int e) {
+    return __uint_as_float((e & 1) ? (v[e >> 1] & 0xFFFF0000u) : (v[e >> 1] << 16));
+  }
+  static constexpr int kPrepRowBatch = 8;
 };
 
 struct FeatArgs {
@@ -93,32 +108,85 @@ __device__ inline void load_slice(const FT* row, int d, int lane, float* x) {
 __device__ inline int slice_dim(int v, int lane) { return (v >> 3) * 512 + lane * 8 + (v & 7); }
 
 // ------------------------------------------------------------- score_prep
-template <typename FT>
+// Row norms of every tapped layer and the head-mean anchor scores, 32 patches
+// per block (the compulsory single read of the features and the CLS rows).
+// Each wave owns 8 patches; per tapped layer it issues the 16-byte loads of
+// a batch of rows (8 bf16 / 4 fp32 rows, NCH chunks of 512 elements each)
+// before reducing any of them.  Ordinary loads: the later passes re-read the
+// same rows, from the last-level cache while the tiles fit in it.  A lane
+// sums its chunks in ascending order and the wave sum is a fixed butterfly.
+// Threads 0..31 own one patch's head mean each: all head loads are issued
+// (8 at a time) before the sum, which runs over h = 0..H-1 in order, then one
+// IEEE division.
+constexpr int kPrepRows = 32;
+
+template <typename FT, int NCH>
 __global__ void __launch_bounds__(256) score_prep_kernel(
     int n, int H, int d, int n_layers, const float* __restrict__ attn, int64_t as_g,
     int64_t as_h, int col0, FeatArgs fa, float* __restrict__ a_out, float* __restrict__ nu) {
   const int g = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int i = blockIdx.x * 4 + wave;
-  if (i >= n) return;
-  for (int l = 0; l < n_layers; ++l) {
-    const FT* row = feat_row<FT>(fa, l, g, i);
-    float ss = 0.f;
-    for (int c = lane * 8; c < d; c += 512) {  // d is a multiple of 8
-      float x[8];
-      Feat<FT>::load8(row + c, x);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
-    }
-    ss = wave_sum(ss);
-    if (lane == 0) nu[((int64_t)g * n_layers + l) * n + i] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
-  }
-  if (lane == 0 && attn) {  // null: the anchor scores are given in a_out
+  const int i0 = blockIdx.x * kPrepRows;
+  if (attn && threadIdx.x < kPrepRows && i0 + (int)threadIdx.x < n) {  // null: scores given in a_out
+    const int i = i0 + threadIdx.x;
     const float* col = attn + (int64_t)g * as_g + col0 + i;
     float acc = 0.f;
-    for (int h = 0; h < H; ++h) acc = __fadd_rn(acc, col[(int64_t)h * as_h]);
+    for (int h0 = 0; h0 < H; h0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = h0 + t < H ? col[(int64_t)(h0 + t) * as_h] : 0.f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t)
+        if (h0 + t < H) acc = __fadd_rn(acc, v[t]);
+    }
     a_out[(int64_t)g * n + i] = __fdiv_rn(acc, (float)H);
   }
+  constexpr int RW = 8;  // rows per wave, in batches of RB
+  constexpr int RB = Feat<FT>::kPrepRowBatch;
+  const int r0 = i0 + RW * wave;
+  for (int l = 0; l < n_layers; ++l) {
+#pragma unroll
+    for (int rb = 0; rb < RW; rb += RB) {
+      typename Feat<FT>::Raw x[RB][NCH];
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        const FT* row = feat_row<FT>(fa, l, g, min(r0 + rb + r, n - 1));
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+          const int e0 = lane * 8 + 512 * c;
+          if (e0 < d) x[r][c] = Feat<FT>::load8_raw(row + e0);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        float ss = 0.f;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+          if (lane * 8 + 512 * c < d) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const float v = Feat<FT>::raw_at(x[r][c], e);
+              ss = fmaf(v, v, ss);
+            }
+          }
+        ss = wave_sum(ss);
+        const int i = r0 + rb + r;
+        if (lane == 0 && i < n) nu[((int64_t)g * n_layers + l) * n + i] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
+      }
+    }
+  }
+}
+
+template <typename FT>
+void launch_score_prep(int G, int n, int H, int d, int n_layers, const float* attn, int64_t as_g, int64_t as_h,
+                       int col0, const FeatArgs& fa, float* a_out, float* nu, hipStream_t st) {
+  const dim3 grid(ceil_div(n, kPrepRows), G);
+  if (d <= 512)
+    score_prep_kernel<FT, 1><<<grid, 256, 0, st>>>(n, H, d, n_layers, attn, as_g, as_h, col0, fa, a_out, nu);
+  else if (d <= 1024)
+    score_prep_kernel<FT, 2><<<grid, 256, 0, st>>>(n, H, d, n_layers, attn, as_g, as_h, col0, fa, a_out, nu);
+  else
+    score_prep_kernel<FT, 4><<<grid, 256, 0, st>>>(n, H, d, n_layers, attn, as_g, as_h, col0, fa, a_out, nu);
 }
 
 // ------------------------------------------------------------- anchor_topk
@@ -852,13 +920,12 @@ extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers
 
   {
     ProfScope ps(KC_SCORE_PREP, st);
-    dim3 grid(ceil_div(n, 4), G);
     if (feat_dtype == SPIDER_BF16)
-      score_prep_kernel<uint16_t><<<grid, 256, 0, st>>>(n, H, d_v, n_layers, cls_attn, attn_stride_g,
-                                                       attn_stride_h, attn_col0, fa, a_out, ws.nu);
+      launch_score_prep<uint16_t>(G, n, H, d_v, n_layers, cls_attn, attn_stride_g, attn_stride_h, attn_col0, fa,
+                                  a_out, ws.nu, st);
     else
-      score_prep_kernel<float><<<grid, 256, 0, st>>>(n, H, d_v, n_layers, cls_attn, attn_stride_g,
-                                                    attn_stride_h, attn_col0, fa, a_out, ws.nu);
+      launch_score_prep<float>(G, n, H, d_v, n_layers, cls_attn, attn_stride_g, attn_stride_h, attn_col0, fa,
+                               a_out, ws.nu, st);
     SPIDER_LAUNCHED("score_prep");
   }
   {
