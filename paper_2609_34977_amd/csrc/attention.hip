@@ -223,8 +223,9 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
 // K rows enter the tile in the order sigma(i) = i with bits 2 and 3 swapped:
 // then the S^T registers of a lane hold, for MFMA k-block u of P V, the 8
 // consecutive keys 16u + 8 hi + [0, 8), and the V^T operand is one 16-byte
-// read.  LDS chunks are swizzled (K: chunk c of row r at c ^ (r & 7), rows of
-// 256 B; V^T: c ^ ((r >> 1) & 3), rows of 64 B) so fragment reads are free of
+// read.  LDS chunks are swizzled (K: chunk c of row r at c ^ (r & 15), rows of
+// 256 B; V^T: c ^ ((r >> 2) & 3), rows of 64 B) so the 16 lanes an LDS pass of
+// a 16-byte read serves (16 consecutive rows) hit distinct banks: fragment reads are free of
 // bank conflicts.  Key rows past the last row read the last row (masked).  A
 // wave skips the MMAs of a key block that none of its queries can see.
 template <int QT>
@@ -294,27 +295,25 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
 
   // DMA of the key block at j0 into stage S: K tile rows 4i..4i+3 and V^T rows
   // 16i..16i+15 for i = 2 wave + e (e = 0, 1); lane l writes 16 bytes at l*16
+  const uint32_t ring_lds = lds_offset(ring);
   auto issue = [&](int j0, auto S) {
     constexpr int st = decltype(S)::value;
-    uint8_t* base = ring + st * STAGE;
+    const uint32_t base = ring_lds + st * STAGE;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int i = 2 * wave + e;
       const int row = 4 * i + (lane >> 4);
       const int sig = (row & ~12) | ((row & 4) << 1) | ((row & 8) >> 1);
       const int key = min(j0 + sig, a.rows - 1);
-      const int c = (lane & 15) ^ (row & 7);
-      __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(Kp + (int64_t)key * a.d + h * DH + 8 * c),
-                                       (__attribute__((address_space(3))) void*)(base + i * 1024), 16, 0, 0);
+      const int c = (lane & 15) ^ (row & 15);
+      dma16(Kp + (int64_t)key * a.d + h * DH + 8 * c, base + i * 1024);
     }
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int i = 2 * wave + e;
       const int row = 16 * i + (lane >> 2);
-      const int c = (lane & 3) ^ ((row >> 1) & 3);
-      __builtin_amdgcn_global_load_lds(
-          reinterpret_cast<const void*>(VT + (int64_t)(h * DH + row) * a.ldvt + j0 + 8 * c),
-          (__attribute__((address_space(3))) void*)(base + KT_BYTES + i * 1024), 16, 0, 0);
+      const int c = (lane & 3) ^ ((row >> 2) & 3);
+      dma16(VT + (int64_t)(h * DH + row) * a.ldvt + j0 + 8 * c, base + KT_BYTES + i * 1024);
     }
   };
 
@@ -338,13 +337,27 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
     floatx16 s[QT];
 #pragma unroll
     for (int t = 0; t < QT; ++t) s[t] = floatx16{};
+    // every K fragment of the block first (one LDS latency for all of them),
+    // then the V^T fragments, whose latency the softmax below covers
+    bf16x8 kf[DH / 16], vf[DH / 32][2];
 #pragma unroll
-    for (int k = 0; k < DH / 16; ++k) {
-      const bf16x8 kf = __builtin_bit_cast(
-          bf16x8, *reinterpret_cast<const u32x4*>(kt + lo * 256 + 16 * ((2 * k + hi) ^ (lo & 7))));
+    for (int k = 0; k < DH / 16; ++k)
+      kf[k] = __builtin_bit_cast(bf16x8,
+                                 *reinterpret_cast<const u32x4*>(kt + lo * 256 + 16 * ((2 * k + hi) ^ (lo & 15))));
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int t = 0; t < QT; ++t) s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[t][k], s[t], 0, 0, 0);
-    }
+    for (int k = 0; k < DH / 16; ++k)
+#pragma unroll
+      for (int t = 0; t < QT; ++t) s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[k], qf[t][k], s[t], 0, 0, 0);
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int row = 32 * c + lo;
+        vf[c][u] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(vt + row * 64 + 16 * ((2 * u + hi) ^ ((row >> 2) & 3))));
+      }
+    __builtin_amdgcn_sched_barrier(0);
     // Online softmax on the raw scores: the scale enters the exponent through
     // one FMA, exp2 is the hardware instruction, keys are masked only in key
     // blocks some query of the wave cannot fully see, and the accumulators
@@ -408,31 +421,24 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
     }
     // O^T += V^T P^T: V^T operand = dh row 32c + lo, keys 16u + 8 hi + [0, 8)
 #pragma unroll
-    for (int c = 0; c < DH / 32; ++c) {
-      const int row = 32 * c + lo;
+    for (int c = 0; c < DH / 32; ++c)
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const bf16x8 vf = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(vt + row * 64 + 16 * ((2 * u + hi) ^ ((row >> 1) & 3))));
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int t = 0; t < QT; ++t) {
-          o[t][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t][u][0], o[t][c], 0, 0, 0);
-          o[t][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t][u][1], o[t][c], 0, 0, 0);
+          o[t][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c][u], pf[t][u][0], o[t][c], 0, 0, 0);
+          o[t][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[c][u], pf[t][u][1], o[t][c], 0, 0, 0);
         }
-      }
-    }
   };
 
   issue(jb0, std::integral_constant<int, 0>{});
-  wait_vm<0>();
-  __syncthreads();
+  dma_wait_barrier();
   auto body = [&](int bi, auto J) {
     constexpr int j = decltype(J)::value;
     const int nb = min(bi + 1, nblk - 1);
     issue(jb0 + 32 * nb, std::integral_constant<int, j ^ 1>{});
     compute(jb0 + 32 * bi, J);
-    wait_vm<0>();
-    __syncthreads();
+    dma_wait_barrier();
   };
   int bi = 0;
   for (; bi + 2 <= nblk; bi += 2) {

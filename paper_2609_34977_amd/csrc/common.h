@@ -137,6 +137,46 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// ----------------------------------------------------------------- LDS DMA
+// 16-byte-per-lane DMA from global memory into LDS at byte offset `lds` (+16
+// per lane), issued as inline assembly: the compiler does not track an LDS
+// DMA it cannot see, so its own LDS-read waits stay exact counts (with the
+// builtin, any DMA in flight turns every fragment wait into a wait for all
+// LDS reads).  Completion is the caller's business: dma_wait_barrier().
+// `lds` must be the same in every lane.  NT: non-temporal (data read once).
+// (m0 is declared clobbered on purpose: the compiler sets it before each of its
+// own LDS DMAs, and clang warns about clobbering a reserved register)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+template <bool NT = false>
+__device__ __forceinline__ void dma16(const uint16_t* g, uint32_t lds) {
+  lds = __builtin_amdgcn_readfirstlane(lds);  // wave-uniform by construction
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(g), "s"(lds) : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+#pragma clang diagnostic pop
+
+// At most N of this wave's DMAs still in flight, then the block barrier: the
+// older DMAs of every wave have landed and every wave is done reading what
+// the next DMAs overwrite.  One assembly statement with a memory clobber, so
+// no LDS access moves across it.
+template <int N = 0>
+__device__ __forceinline__ void dma_wait_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+// Every DMA of this wave complete (no barrier), as a compiler fence.
+__device__ __forceinline__ void dma_wait_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// LDS byte offset of a __shared__ address (the DMA's M0 operand).
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint8_t*)p;
+}
+
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
