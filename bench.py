@@ -59,6 +59,12 @@ def parse():
                    help="run one plain device copy of this size after warm-up (counter calibration)")
     p.add_argument("--score-sweep", action="store_true",
                    help="instead of the step: time scoring over 20/64/256/512 tiles (one JSON line each)")
+    p.add_argument("--select-sweep", action="store_true",
+                   help="instead of the step: time quota/selection (spider_select) and the gather of the kept "
+                        "rows over 20/64/256/512 tiles at keep 128 and keep-all (one JSON line each)")
+    p.add_argument("--curve", action="store_true",
+                   help="instead of the headline step: the stress shape over keep {576, 288, 144, 64} per "
+                        "tile x skip {0, 0.25, 0.5} (one JSON line per point, weights shared)")
     p.add_argument("--colmean-sweep", action="store_true",
                    help="instead of the step: time the anchor scores of encoders without [CLS] "
                         "(column means of 16-head attention maps) over 1/8/64 tiles of 576 and 1024 patches")
@@ -254,6 +260,81 @@ def score_sweep(w, dev, args):
                           "kernel_ms_per_call": kms}), flush=True)
         del attn, feats
         torch.cuda.empty_cache()
+
+
+def select_sweep(w, dev, args):
+    """Quota/selection (select_kernel) and the gather of the kept rows into the packed
+    decoder input (assemble_kernel) over G tiles, from the workload's own score
+    outputs repeated up to G.  Algorithmic bytes: selection reads cluster ids and
+    scores and writes the kept indices and counts (12 n + 4 cap per tile); the
+    gather reads and writes every kept row once (2 x rows x d_model x 2 bytes)
+    plus the text rows."""
+    import dataclasses
+    from synth.decoder_inputs import text_rows, visual_src
+    from synth.vision import vision_inputs
+    from paper_2609_34977_amd import _lib
+
+    sc = w.score
+    for keep in (128, sc.n):
+        base = dataclasses.replace(sc, G=20, keep=keep)
+        attn0, feats0 = vision_inputs(base, w.seed)
+        n_anchor, n_cmp = _lib.budget(keep, sc.r_num, sc.r_den)
+        n_anchor = min(n_anchor, sc.n)
+        r0 = _lib.score(attn0.to(dev), [f.to(dev) for f in feats0], n_anchor, sc.K, sc.kmeans_iter)
+        wl = dataclasses.replace(w, score=dataclasses.replace(sc, G=20))
+        src0 = visual_src(wl, dev)
+        for G in (20, 64, 256, 512):  # multiples of the 4 tiles per sample
+            reps = (G + 19) // 20
+            cl = r0["cluster"].repeat(reps, 1)[:G].contiguous()
+            sv = r0["s"].repeat(reps, 1)[:G].contiguous()
+            src = src0.repeat(reps, 1, 1)[:G].contiguous()
+            tps = 4  # four tiles per sample (AnyRes-like): at most 255 samples per call
+            text = text_rows(dataclasses.replace(w, B=G // tps), dev)
+            cap = min(sc.n, n_anchor + n_cmp + sc.K)
+            for _ in range(2):
+                _lib.select(cl, sv, n_anchor, n_cmp, sc.K, w.quota_mode, cap, tps, src, text)
+            torch.cuda.synchronize()
+            _lib.profile_mask(["select", "assemble"])
+            _lib.profile_enable(True)
+            iters = 5
+            for _ in range(iters):
+                out = _lib.select(cl, sv, n_anchor, n_cmp, sc.K, w.quota_mode, cap, tps, src, text)
+            torch.cuda.synchronize()
+            prof = _lib.profile_read()
+            _lib.profile_enable(False)
+            _lib.profile_mask(None)
+            kept = int(out["count"].sum())
+            d = src.shape[-1]
+            sel_bytes = G * (12 * sc.n + 4 * cap)
+            gat_bytes = 2 * (kept + (G // tps) * w.n_text) * d * src.element_size()
+            t_sel = prof["select"][1] / iters
+            t_gat = prof["assemble"][1] / iters
+            print(json.dumps({"mode": "select_sweep", "tiles": G, "keep_per_tile": keep, "kept_rows": kept,
+                              "select_ms": t_sel, "select_bytes": sel_bytes,
+                              "select_frac_of_hbm_peak": sel_bytes / (t_sel * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                              "gather_ms": t_gat, "gather_bytes": gat_bytes,
+                              "gather_frac_of_hbm_peak": gat_bytes / (t_gat * 1e-3) / 1e9 / HBM_PEAK_GBS}),
+                  flush=True)
+            del cl, sv, src, text, out
+            torch.cuda.empty_cache()
+
+
+def curve(args, dev):
+    """The stress shape (batch 4 x 5 tiles of 576) over keep per tile {576, 288, 144, 64}
+    x skip fraction {0, 0.25, 0.5}: one JSON line per point with the step time and the
+    dominant kernel class against its roofline (weights generated once)."""
+    from synth import get_workload
+    W = None
+    for keep in (576, 288, 144, 64):
+        for p in (0.0, 0.25, 0.5):
+            w = get_workload("stress", keep=keep, L=args.layers, skip_p=p)
+            res, W = run_step(w, args, dev, weights=W, cpu=False)
+            r = {"mode": "curve", "keep_per_tile": keep, "skip_p": p, "ms_per_step": res["ms_per_step"],
+                 "tokens_per_s": res["value"], "decoder_rows": res["config"]["decoder_rows"],
+                 "skipped_sublayer_slots": res["config"]["skipped_sublayer_slots"],
+                 "prefill_tflop_per_step": res["prefill_tflop_per_step"], "roofline": res["roofline"],
+                 "kernel_ms_per_step": res["kernel_ms_per_step"]}
+            print(json.dumps(r), flush=True)
 
 
 def decode_latency(w, pipe, out, dev, args):
@@ -488,6 +569,12 @@ def main():
         return
     if args.colmean_sweep:
         colmean_sweep(dev)
+        return
+    if args.select_sweep:
+        select_sweep(w, dev, args)
+        return
+    if args.curve:
+        curve(args, dev)
         return
     cpu = not args.no_cpu_baseline and not args.online and not args.projector
     res, W = run_step(w, args, dev, online=args.online, projector_on=args.projector, decode=args.decode,

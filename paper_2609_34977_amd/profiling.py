@@ -157,6 +157,15 @@ def stats(args):
             rows.append((_short_name(name), int(r["Calls"]), float(r["AverageNs"]) / 1e3,
                          float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["TotalDurationNs"]) / 1e6))
     rows.sort(key=lambda t: -t[5])
+    cls_line = []
+    if getattr(args, "kernel_class", None):
+        pat, prim = re.compile(CLASSES[args.kernel_class][1]), re.compile(CLASSES[args.kernel_class][2])
+        tot_ms = sum(t for n, c, a, mn, mx, t in rows if pat.search(n))
+        launches = sum(c for n, c, a, mn, mx, t in rows if prim.search(n))
+        if launches:
+            cls_line = [f"Kernel class `{args.kernel_class}` (every dispatch of its kernels, the SwiGLU tail "
+                        f"reduction included): {launches} launches, {tot_ms * 1e3 / launches:.2f} us per launch "
+                        f"on average, {tot_ms:.3f} ms in total."]
     lines = [f"# {args.title}", "", "Command (run from the repository root on one MI355X):", "", "```"]
     lines += (args.command or []) + ["```", "",
                                       "Kernels of this library (spider::), sorted by total time; the torch kernels that "
@@ -166,6 +175,8 @@ def stats(args):
                                       "|---|---|---|---|---|---|"]
     for n, c, a, mn, mx, t in rows:
         lines.append(f"| `{n}` | {c} | {a:.2f} | {mn:.2f} | {mx:.2f} | {t:.3f} |")
+    if cls_line:
+        lines += [""] + cls_line
     if args.bench_log:
         with open(args.bench_log) as f:
             js = [ln for ln in f if ln.startswith("{")]
@@ -202,6 +213,96 @@ def bench_table(args):
     print("\n".join(lines))
 
 
+# kernels of the decoder step grouped for the counter table (name pattern, label)
+_MFMA_GROUPS = [
+    (r"gemm_tile_kernel<\d+, true\b", "tile GEMM, SwiGLU epilogue (gate/up, > 256 rows)"),
+    (r"gemm_tile_kernel<\d+, false, true>", "tile GEMM, RoPE/bf16 epilogue (QKV, > 256 rows)"),
+    (r"gemm_tile_kernel<\d+, false, false>", "tile GEMM, fp32 partials (O and down, > 256 rows)"),
+    (r"gemm_stream_kernel<\d+, \d+, true", "streaming GEMM, SwiGLU (<= 256 rows)"),
+    (r"gemm_stream_kernel<\d+, \d+, false", "streaming GEMM, fp32 partials (<= 256 rows)"),
+    (r"attention_wide_kernel", "attention, many queries"),
+    (r"attention_bf16_kernel", "attention, few queries"),
+]
+
+
+def mfma(args):
+    """MFMA counters per kernel group from a rocprofv3 counter CSV with SQ_BUSY_CYCLES,
+    SQ_VALU_MFMA_BUSY_CYCLES and SQ_INSTS_VALU_MFMA_MOPS_BF16 (one pass).  SQ_BUSY_CYCLES
+    sums the 32 shader engines (8 XCDs x 4), so a dispatch lasts SQ_BUSY_CYCLES / 32
+    cycles; MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x those cycles); one MOP
+    is 512 flops."""
+    per = {}
+    with open(args.csv) as f:
+        for r in csv.DictReader(f):
+            name = r["Kernel_Name"]
+            for pat, label in _MFMA_GROUPS:
+                if re.search(pat, name):
+                    d = per.setdefault(label, {}).setdefault(r["Dispatch_Id"], {})
+                    d[r["Counter_Name"]] = float(r["Counter_Value"])
+                    break
+    lines = [f"# {args.title}", "", "Command (repository root, one MI355X; `cd /tmp && export TMPDIR=/tmp` first):",
+             "", "```"] + (args.command or []) + ["```", "",
+             "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x SQ_BUSY_CYCLES / 32 shader engines), "
+             "summed over the group's dispatches; flops = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 (an exact "
+             "count of the MFMA work issued).  Counter runs serialise dispatches, so these fractions "
+             "describe the kernels themselves, not the step's overlap.", "",
+             "| kernel group | dispatches | MFMA busy | TFLOP issued (all dispatches) | TFLOP/s while running |",
+             "|---|---|---|---|---|"]
+    for _, label in _MFMA_GROUPS:
+        if label not in per:
+            continue
+        ds = per[label].values()
+        busy = sum(d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for d in ds)
+        cyc = sum(d.get("SQ_BUSY_CYCLES", 0) for d in ds) / 32.0
+        mops = sum(d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) for d in ds)
+        tf = mops * 512 / 1e12
+        secs = cyc / (args.clock_ghz * 1e9)
+        lines.append(f"| {label} | {len(per[label])} | {busy / max(1024 * cyc, 1):.3f} | {tf:.2f} | "
+                     f"{tf / max(secs, 1e-12):.0f} (at {args.clock_ghz} GHz) |")
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def sweep_table(args):
+    """Markdown table of bench.py JSON lines (score / select sweeps, the stress curve)."""
+    rows = []
+    with open(args.jsonl) as f:
+        for ln in f:
+            if ln.startswith("{"):
+                rows.append(json.loads(ln))
+    lines = [f"# {args.title}", "", "Command (repository root, one MI355X):", "", "```"] + \
+        (args.command or []) + ["```", ""] + (args.note or [])
+    if rows and rows[0].get("mode") == "curve":
+        lines += ["", "| keep / tile | skip p | decoder rows | ms / step | rows / s | prefill TFLOP | "
+                      "TFLOP/s (step) | dominant kernel | bound | achieved | frac of peak |",
+                  "|---|---|---|---|---|---|---|---|---|---|---|"]
+        for r in rows:
+            ro = r["roofline"]
+            lines.append(f"| {r['keep_per_tile']} | {r['skip_p']} | {r['decoder_rows']} | {r['ms_per_step']:.2f} | "
+                         f"{r['tokens_per_s']:.0f} | {r['prefill_tflop_per_step']:.1f} | "
+                         f"{r['prefill_tflop_per_step'] / r['ms_per_step'] * 1e3:.0f} | {ro['kernel']} | "
+                         f"{ro['bound']} | {ro['achieved']:.0f} {ro['unit']} | {ro['frac']:.3f} |")
+    elif rows and rows[0].get("mode") == "select_sweep":
+        lines += ["", "| keep / tile | tiles | kept rows | select ms | select frac of HBM | gather ms | "
+                      "gather MB | gather frac of HBM |", "|---|---|---|---|---|---|---|---|"]
+        for r in rows:
+            lines.append(f"| {r['keep_per_tile']} | {r['tiles']} | {r['kept_rows']} | {r['select_ms']:.4f} | "
+                         f"{r['select_frac_of_hbm_peak']:.3f} | {r['gather_ms']:.4f} | {r['gather_bytes'] / 1e6:.1f} | "
+                         f"{r['gather_frac_of_hbm_peak']:.3f} |")
+    elif rows and rows[0].get("mode") == "score_sweep":
+        ks = list(rows[0]["kernel_ms_per_call"])
+        lines += ["", "| tiles | ms / call | compulsory MB | frac of HBM (compulsory / call) | " +
+                  " | ".join(f"{k} ms" for k in ks) + " |", "|---|---|---|---|" + "---|" * len(ks)]
+        for r in rows:
+            lines.append(f"| {r['tiles']} | {r['ms_per_call']:.3f} | {r['compulsory_bytes'] / 1e6:.1f} | "
+                         f"{r['frac_of_hbm_peak']:.3f} | " +
+                         " | ".join(f"{r['kernel_ms_per_call'].get(k, 0):.4f}" for k in ks) + " |")
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     p = argparse.ArgumentParser()
     sub = p.add_subparsers(dest="cmd", required=True)
@@ -215,6 +316,7 @@ def main():
     s.add_argument("--bench-log")
     s.add_argument("--out", required=True)
     s.add_argument("--title", default="rocprofv3 kernel statistics")
+    s.add_argument("--kernel-class", default=None, help="also report this class's average per launch")
     s.add_argument("--command", action="append")
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
@@ -225,8 +327,24 @@ def main():
     t.add_argument("--rows", type=int, required=True, help="decoder rows of the bench line")
     t.add_argument("--out", required=True)
     t.add_argument("--command", action="append")
+    m = sub.add_parser("mfma")
+    m.add_argument("--csv", required=True)
+    m.add_argument("--out", required=True)
+    m.add_argument("--title", default="MFMA counters")
+    m.add_argument("--clock-ghz", type=float, default=2.4)
+    m.add_argument("--command", action="append")
+    w = sub.add_parser("sweep-table")
+    w.add_argument("--jsonl", required=True)
+    w.add_argument("--out", required=True)
+    w.add_argument("--title", default="bench.py sweep")
+    w.add_argument("--command", action="append")
+    w.add_argument("--note", action="append")
     args = p.parse_args()
-    if args.cmd == "traffic":
+    if args.cmd == "mfma":
+        mfma(args)
+    elif args.cmd == "sweep-table":
+        sweep_table(args)
+    elif args.cmd == "traffic":
         traffic(args)
     elif args.cmd == "stats":
         stats(args)
