@@ -712,27 +712,33 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
   // issued between the MMA groups of the first two k-steps (a burst of all of
   // them at once stalls the wave before its MMAs; spread over all four k-steps
   // the last ones land too late), measured 10-15 % faster than either.
-  auto compute = [&](auto S, int kbn, auto SN, auto FULL) {
+  // fragments of k-step q of the k-block in stage S
+  auto frags = [&](auto S, int q, bf16x8 (&w)[4], bf16x8 (&x)[MH]) __attribute__((always_inline)) {
     constexpr int st = decltype(S)::value;
     const uint8_t* tile = ring + st * STAGE_BYTES;
     const uint8_t* at = tile + (32 * MH * mh + lo) * 128;
     const uint8_t* wt = tile + A_BYTES + lo * 128;
-    bf16x8 wf[2][4], af[2][MH];
-    auto frags = [&](int q, bf16x8 (&w)[4], bf16x8 (&x)[MH]) {
-      const int c = 16 * ((4 * hi + q) ^ swz(lo));
+    const int c = 16 * ((4 * hi + q) ^ swz(lo));
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        w[u] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wt + wrow(u) * 128 + c));
+    for (int u = 0; u < 4; ++u)
+      w[u] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wt + wrow(u) * 128 + c));
 #pragma unroll
-      for (int i = 0; i < MH; ++i)
-        x[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(at + i * 32 * 128 + c));
-    };
-    constexpr int SLOTS = 2 * MH;  // MMA groups of k-steps 0 and 1
-    frags(0, wf[0], af[0]);
-    static_for<0, 4>([&](auto Q) {
-      constexpr int q = Q.value;
-      if constexpr (q + 1 < 4) frags(q + 1, wf[(q + 1) & 1], af[(q + 1) & 1]);
-      __builtin_amdgcn_sched_barrier(0);
+    for (int i = 0; i < MH; ++i)
+      x[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(at + i * 32 * 128 + c));
+  };
+  bf16x8 wf[2][4], af[2][MH];
+  constexpr int HALF = NP / 2;  // DMA pieces issued in step 3, the rest in the next step 0
+
+  // One k-block in stage S.  On entry buffer 0 holds its step-0 fragments and
+  // the first half of the DMA of the next k-block (stage SN) is in flight.
+  // Step 0 issues the other half; the barrier comes after step 2's MMAs, once
+  // step 3's fragments are in registers: then stage S is free (DMA of k-block
+  // kdma goes there, interleaved with step 3's MMAs) and stage SN has landed
+  // (the next k-block's step-0 fragments are read while step 3's MMAs run).
+  auto kblock = [&](auto S, auto SN, int knext, int kdma, auto FULL) __attribute__((always_inline)) {
+    auto mmas = [&](auto Q, auto P0, auto P1, auto SD, int kd) __attribute__((always_inline)) {
+      constexpr int q = decltype(Q)::value;
+      constexpr int p0 = decltype(P0)::value, p1 = decltype(P1)::value;
       static_for<0, MH>([&](auto I) {
         constexpr int i = I.value;
         if (decltype(FULL)::value || i < live) {
@@ -740,40 +746,49 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
           for (int u = 0; u < 4; ++u)
             acc[i][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][i], wf[q & 1][u], acc[i][u], 0, 0, 0);
         }
-        constexpr int slot = q * MH + i;
-        if constexpr (slot < SLOTS) {
-          constexpr int p0 = slot * NP / SLOTS, p1 = (slot + 1) * NP / SLOTS;
-          static_for<p0, p1>([&](auto P) { issue_piece(kbn, SN, P); });
-        }
+        constexpr int a0 = p0 + i * (p1 - p0) / MH, a1 = p0 + (i + 1) * (p1 - p0) / MH;
+        static_for<a0, a1>([&](auto P) { issue_piece(kd, SD, P); });
         __builtin_amdgcn_sched_barrier(0);
       });
-    });
+    };
+    using Z = std::integral_constant<int, 0>;
+    frags(S, 1, wf[1], af[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    mmas(std::integral_constant<int, 0>{}, std::integral_constant<int, HALF>{}, std::integral_constant<int, NP>{}, SN, knext);
+    frags(S, 2, wf[0], af[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    mmas(std::integral_constant<int, 1>{}, Z{}, Z{}, SN, knext);
+    frags(S, 3, wf[1], af[1]);
+    __builtin_amdgcn_sched_barrier(0);
+    mmas(std::integral_constant<int, 2>{}, Z{}, Z{}, SN, knext);
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    frags(SN, 0, wf[0], af[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    mmas(std::integral_constant<int, 3>{}, Z{}, std::integral_constant<int, HALF>{}, S, kdma);
   };
 
   if (nkb > 0) {
-    static_for<0, NP>([&](auto P) { issue_piece(0, std::integral_constant<int, 0>{}, P); });
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    static_for<0, NP>([&](auto P) { issue_piece(0, S0{}, P); });
     dma_wait_barrier();
+    frags(S0{}, 0, wf[0], af[0]);
+    static_for<0, HALF>([&](auto P) { issue_piece(min(1, nkb - 1), S1{}, P); });
     // Waves whose row tiles all hold rows < M (every block but the last row
     // tile) run a copy of the loop without the per-tile guards: a branch
     // inside the MMA groups splits the loop into basic blocks, across which
-    // the compiler can only wait for every outstanding LDS read, so each
-    // k-step would also wait for the next step's fragments.
-    auto run = [&](auto FULL) {
-      auto body = [&](int kb, auto J) {
-        constexpr int j = decltype(J)::value;
-        // the next k-block (the last one again at the end) into the other stage
-        compute(J, min(kb + 1, nkb - 1), std::integral_constant<int, j ^ 1>{}, FULL);
-        dma_wait_barrier();
-      };
+    // the compiler can only wait for every outstanding LDS read.
+    auto run = [&](auto FULL) __attribute__((always_inline)) {
       int kb = 0;
       for (; kb + 2 <= nkb; kb += 2) {
-        body(kb, std::integral_constant<int, 0>{});
-        body(kb + 1, std::integral_constant<int, 1>{});
+        kblock(S0{}, S1{}, min(kb + 1, nkb - 1), min(kb + 2, nkb - 1), FULL);
+        kblock(S1{}, S0{}, min(kb + 2, nkb - 1), min(kb + 3, nkb - 1), FULL);
       }
-      if (kb < nkb) body(kb, std::integral_constant<int, 0>{});
+      if (kb < nkb) kblock(S0{}, S1{}, min(kb + 1, nkb - 1), min(kb + 2, nkb - 1), FULL);
     };
     if (live == MH) run(std::true_type{});
     else run(std::false_type{});
+    dma_wait_all();
   }
 
   // D layout of the 32x32 MMA: column lane % 32, row 8 (r / 4) + 4 (lane / 32) + r % 4
