@@ -22,7 +22,8 @@
  *   - Calls on distinct workspaces are independent; the library keeps no
  *     per-call state except the thread-local error message, the optional
  *     profiler and the per-thread pinned staging buffers used by the
- *     prefill calls to upload row tables and read back admission flags.
+ *     prefill calls to upload row tables and read back admission flags
+ *     and codes.
  */
 #ifndef SPIDER_H
 #define SPIDER_H
@@ -422,9 +423,17 @@ spider_status spider_decode_step(const spider_decoder_cfg* cfg, const spider_lay
  *   NULL: admission layer, -1 if never; s_sa_out device fp32
  *   [floor(L/2), rows] or NULL: S_sa of each row at each window layer where it
  *   was scored, 0 elsewhere; h_out as spider_prefill.
- * Synchronisation: the admission flags are read back to the host once per
- *   window layer (the call waits for the stream there), so the call returns
- *   after the window has executed; the layers after it run asynchronously.
+ * Synchronisation: with rows <= 256, B * n_text >= 5 and (bf16) fewer than
+ *   128 heads x row blocks of 128 (ceil(rows / 128) * H < 128; with a bf16
+ *   lens over V not a multiple of 128 also no 1..4 visual rows), the
+ *   admissions, codes and row lists stay on the device and the launches of a
+ *   window layer read the live row counts there; codes_out and admit_out are
+ *   copied back once, after the last layer, and the call returns when the
+ *   whole prefill has executed.  Otherwise the admission flags are read back
+ *   to the host once per window layer (the call waits for the stream there)
+ *   and the host builds the row lists: the call returns after the window has
+ *   executed and the layers after it run asynchronously.  Both give the same
+ *   h as spider_prefill on the returned codes, bit for bit.
  * Workspace: spider_prefill_online_workspace_size(cfg, B, rows, V) bytes.
  * ------------------------------------------------------------------------ */
 size_t spider_prefill_online_workspace_size(const spider_decoder_cfg* cfg, int B, int rows, int V);

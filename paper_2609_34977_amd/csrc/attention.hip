@@ -43,8 +43,10 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) float xo[NW - 1][64 * 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hi = lane >> 5, lo = lane & 31;
   const int h = blockIdx.y;
+  const int nq = a.nq_dev ? min(a.nq, *a.nq_dev) : a.nq;
+  if ((int)blockIdx.x * 32 >= nq) return;
   const int qa = blockIdx.x * 32 + lo;
-  const bool qok = qa < a.nq;
+  const bool qok = qa < nq;
   const uint16_t* Q = reinterpret_cast<const uint16_t*>(a.q);
   const uint16_t* Kp = reinterpret_cast<const uint16_t*>(a.k);
   const uint16_t* VT = reinterpret_cast<const uint16_t*>(a.v);
@@ -471,6 +473,7 @@ __global__ void __launch_bounds__(64) attention_f32_kernel(AttnArgs a) {
   extern __shared__ float sc[];  // [max_seq]
   const int lane = threadIdx.x;
   const int qa = blockIdx.x, h = blockIdx.y;
+  if (a.nq_dev && qa >= *a.nq_dev) return;
   const int qrow = a.q_rows[qa];
   const int st = a.row_start[qrow];
   const int nk = qrow - st + 1;
@@ -528,11 +531,14 @@ __global__ void __launch_bounds__(64) attention_f32_kernel(AttnArgs a) {
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t st) {
   if (a.nq == 0) return hipSuccess;
   if (a.dh != 128 || a.ldvt < ((a.rows + 31) / 32) * 32 || a.ldvt % 32) return hipErrorInvalidValue;
+  // a device query count is honoured by the per-32-query kernel only
+  const bool wide = (int64_t)ceil_div(a.nq, 128) * a.H >= 128;
+  if (wide && a.nq_dev) return hipErrorInvalidValue;
   // At least 128 blocks of 128 queries: the shared-tile kernel (one query tile
   // per wave: two waves per SIMD overlap one's softmax with the other's MMAs;
   // two tiles per wave measured 1.7x slower at one wave per SIMD).  Fewer
   // queries: the per-32-query kernel, whose waves split the keys.
-  if ((int64_t)ceil_div(a.nq, 128) * a.H >= 128) {
+  if (wide) {
     attention_wide_kernel<1><<<dim3(ceil_div(a.nq, 128), a.H), 256, 0, st>>>(a);
   } else {
     attention_bf16_kernel<<<dim3(ceil_div(a.nq, 32), a.H), 256, 0, st>>>(a);

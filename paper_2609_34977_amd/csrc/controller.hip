@@ -70,9 +70,11 @@ __global__ void __launch_bounds__(256) lens_prep_kernel(const float* __restrict_
                                                         const int32_t* __restrict__ cand,
                                                         const int32_t* __restrict__ cand_sample,
                                                         const float* __restrict__ tmean,
-                                                        AT* __restrict__ hc, double* __restrict__ F) {
+                                                        AT* __restrict__ hc, double* __restrict__ F,
+                                                        const int32_t* __restrict__ nc_dev) {
   __shared__ double red[3][4];
   const int c = blockIdx.x;
+  if (nc_dev && c >= *nc_dev) return;
   const float* hr = h + (int64_t)cand[c] * d;
   const float* tq = tmean + (int64_t)cand_sample[c] * d;
   AT* out = hc + (int64_t)c * d;
@@ -120,10 +122,11 @@ __device__ __forceinline__ void admit_row(double S, double T, int c, const int32
 __global__ void __launch_bounds__(256) lens_admit_kernel(const float* __restrict__ logits, int V,
                                                          const int32_t* __restrict__ cand,
                                                          const double* __restrict__ F,
-                                                         LensAdmitArgs p) {
+                                                         LensAdmitArgs p, const int32_t* __restrict__ nc_dev) {
   __shared__ float redf[4];
   __shared__ double redd[2][4];
   const int c = blockIdx.x;
+  if (nc_dev && c >= *nc_dev) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float* z = logits + (int64_t)c * V;
   float m = -INFINITY;
@@ -160,8 +163,10 @@ __device__ __forceinline__ StatD stat_merge(StatD a, StatD b) {
 __global__ void __launch_bounds__(64) lens_admit_stats_kernel(const float* __restrict__ stats, int ntiles,
                                                               const int32_t* __restrict__ cand,
                                                               const double* __restrict__ F,
-                                                              LensAdmitArgs p) {
+                                                              LensAdmitArgs p,
+                                                              const int32_t* __restrict__ nc_dev) {
   const int c = blockIdx.x, lane = threadIdx.x;
+  if (nc_dev && c >= *nc_dev) return;
   const floatx4* row = reinterpret_cast<const floatx4*>(stats) + (int64_t)c * ntiles;
   StatD st{0.0, 0.0, 0.0};
   bool have = false;
@@ -198,31 +203,32 @@ hipError_t launch_text_mean(const float* h, int d, const int32_t* cu, int B, int
 }
 
 hipError_t launch_lens_prep(bool bf16, const float* h, int d, const int32_t* cand,
-                            const int32_t* cand_sample, int nc, const float* tmean, void* hc, double* F,
-                            hipStream_t st) {
+                            const int32_t* cand_sample, int nc, const int32_t* nc_dev, const float* tmean,
+                            void* hc, double* F, hipStream_t st) {
   if (nc <= 0) return hipSuccess;
   if (d % 4) return hipErrorInvalidValue;
   if (bf16)
     lens_prep_kernel<uint16_t><<<nc, 256, 0, st>>>(h, d, cand, cand_sample, tmean,
-                                                    reinterpret_cast<uint16_t*>(hc), F);
+                                                    reinterpret_cast<uint16_t*>(hc), F, nc_dev);
   else
     lens_prep_kernel<float><<<nc, 256, 0, st>>>(h, d, cand, cand_sample, tmean,
-                                                 reinterpret_cast<float*>(hc), F);
+                                                 reinterpret_cast<float*>(hc), F, nc_dev);
   return hipGetLastError();
 }
 
-hipError_t launch_lens_admit(const float* logits, int V, const int32_t* cand, int nc, const double* F,
-                             const LensAdmitArgs& p, hipStream_t st) {
+hipError_t launch_lens_admit(const float* logits, int V, const int32_t* cand, int nc, const int32_t* nc_dev,
+                             const double* F, const LensAdmitArgs& p, hipStream_t st) {
   if (nc <= 0) return hipSuccess;
-  lens_admit_kernel<<<nc, 256, 0, st>>>(logits, V, cand, F, p);
+  lens_admit_kernel<<<nc, 256, 0, st>>>(logits, V, cand, F, p, nc_dev);
   return hipGetLastError();
 }
 
 hipError_t launch_lens_admit_stats(const float* stats, int ntiles, const int32_t* cand, int nc,
-                                   const double* F, const LensAdmitArgs& p, hipStream_t st) {
+                                   const int32_t* nc_dev, const double* F, const LensAdmitArgs& p,
+                                   hipStream_t st) {
   if (nc <= 0) return hipSuccess;
   if (ntiles <= 0) return hipErrorInvalidValue;
-  lens_admit_stats_kernel<<<nc, 64, 0, st>>>(stats, ntiles, cand, F, p);
+  lens_admit_stats_kernel<<<nc, 64, 0, st>>>(stats, ntiles, cand, F, p, nc_dev);
   return hipGetLastError();
 }
 

@@ -80,6 +80,8 @@ __device__ __forceinline__ GroupView group_view(const GemmArgs& a, int gi) {
   v.A = sel3(gi, a.g[0].A, a.g[1].A, a.g[2].A);
   v.rows = sel3(gi, a.g[0].a_rows, a.g[1].a_rows, a.g[2].a_rows);
   v.M = sel3(gi, a.g[0].M, a.g[1].M, a.g[2].M);
+  const int32_t* md = sel3(gi, a.g[0].m_dev, a.g[1].m_dev, a.g[2].m_dev);
+  if (md) v.M = min(v.M, *md);
   v.W = sel3(gi, a.g[0].W, a.g[1].W, a.g[2].W);
   v.W2 = sel3(gi, a.g[0].W2, a.g[1].W2, a.g[2].W2);
   v.out = sel3(gi, a.g[0].out, a.g[1].out, a.g[2].out);
@@ -109,6 +111,7 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(GemmArgs a) {
   const TileCoord tc = decode_tile(a, xcd_remap(blockIdx.x, a.total_tiles), BM, BN);
   const GroupView G = group_view(a, tc.gi);
   const int M = G.M;
+  if (tc.m0 >= M) return;  // a device row count below the launch's bound
   const int kbeg = tc.s * a.k_per_split;
   const int kend = min(a.K, kbeg + a.k_per_split);
   const int nt = kend > kbeg ? (kend - kbeg) / BK : 0;
@@ -331,6 +334,7 @@ __global__ void __launch_bounds__(256) gemm_stream_kernel(GemmArgs a) {
   const TileCoord tc = decode_tile(a, xcd_remap(blockIdx.x, a.total_tiles), BM, BN);
   const GroupView G = group_view(a, tc.gi);
   const int M = G.M;
+  if (tc.m0 >= M) return;  // a device row count below the launch's bound
   const int kbeg = tc.s * a.k_per_split;
   const int kend = min(a.K, kbeg + a.k_per_split);
   const int nkb = kend > kbeg ? (kend - kbeg) / KB : 0;
@@ -1120,6 +1124,7 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const TileCoord tc = decode_tile(a, blockIdx.x, T, T);
   const GroupView G = group_view(a, tc.gi);
+  if (tc.m0 >= G.M) return;  // a device row count below the launch's bound
   const int kbeg = tc.s * a.k_per_split;
   const int kend = min(a.K, kbeg + a.k_per_split);
   const int m = tc.m0 + ty, n = tc.n0 + tx;
@@ -1355,6 +1360,12 @@ int max_rows(const GemmArgs& a) {
   for (int i = 0; i < a.ngroups; ++i) maxM = std::max(maxM, a.g[i].M);
   return maxM;
 }
+// a group whose rows come from a device count (streaming, LDS-staged, fp32 kernels only)
+bool has_row_count(const GemmArgs& a) {
+  for (int i = 0; i < a.ngroups; ++i)
+    if (a.g[i].m_dev) return true;
+  return false;
+}
 }  // namespace
 
 int gemm_tile_unsplit_blocks(const GemmArgs& a, int split_max) {
@@ -1391,6 +1402,7 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
   }
   const bool dual = a.epilogue == EPI_SWIGLU;
   const bool gemv_ok = gemv_fits(maxM, a.K);
+  if (a.epilogue == EPI_QKV_BF16 && has_row_count(a)) return hipErrorInvalidValue;
   if (a.epilogue == EPI_QKV_BF16) {
     // the tile kernel without split, one head of 128 columns per wave, 16-byte stores
     if (gemm_tile_unsplit_blocks(a, split_max) == 0 || !a.rope || !a.pos) return hipErrorInvalidValue;
@@ -1411,6 +1423,7 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
     for (int i = 0; i < a.ngroups; ++i)
       if (a.g[i].N % 128 || a.g[i].a_rows) return hipErrorInvalidValue;
   }
+  if ((gemv_ok || (maxM > 256 && tile_path_fits(a, dual))) && has_row_count(a)) return hipErrorInvalidValue;
   if (gemv_ok) return launch_gemv(a, maxM, dual, st);
   if (maxM > 256 && tile_path_fits(a, dual)) return launch_tile(a, split_max, dual, st);
   TileCfg tc = pick_bf16_tile(maxM, dual);

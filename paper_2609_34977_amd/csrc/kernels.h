@@ -19,6 +19,10 @@ struct GemmGroup {
   int tiles_m, tiles_n;   // filled by the launcher
   int tile_begin;         // filled by the launcher
   int kind;               // EPI_QKV_BF16 only: 1 = RoPE'd rows (Q, K), 2 = transposed rows (V^T)
+  // Optional device row count: the kernel takes min(M, *m_dev) rows (M is then
+  // the bound the launch is sized for).  Streaming, LDS-staged and fp32
+  // kernels only; the launcher rejects it where it would pick another kernel.
+  const int32_t* m_dev;
 };
 
 enum GemmEpilogue {
@@ -93,6 +97,7 @@ struct AttnArgs {
   void* o;                 // [nq, d]
   int nq, rows, H, dh, d;
   float scale;             // 1/sqrt(dh)
+  const int32_t* nq_dev;   // optional device query count: min(nq, *nq_dev) queries (nq = the bound)
 };
 hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t st);
 hipError_t launch_attention_f32(const AttnArgs& a, int max_seq, hipStream_t st);
@@ -103,9 +108,11 @@ hipError_t launch_attention_f32(const AttnArgs& a, int max_seq, hipStream_t st);
 hipError_t launch_text_mean(const float* h, int d, const int32_t* cu, int B, int n_text, float* tmean,
                             hipStream_t st);
 // hc[c] = h[cand[c]] in the activation dtype, F[c] = (1 + cos(h[cand[c]], tmean[b])) / 2.
+// With nc_dev non-null the launch is sized for nc candidates and
+// min(nc, *nc_dev) of them are processed (also for the two admission launches).
 hipError_t launch_lens_prep(bool bf16, const float* h, int d, const int32_t* cand,
-                            const int32_t* cand_sample, int nc, const float* tmean, void* hc, double* F,
-                            hipStream_t st);
+                            const int32_t* cand_sample, int nc, const int32_t* nc_dev, const float* tmean,
+                            void* hc, double* F, hipStream_t st);
 struct LensAdmitArgs {
   double log_v;      // ln V
   double w1;         // weight of S_sa
@@ -116,11 +123,12 @@ struct LensAdmitArgs {
   float* s_out;      // [rows] S_sa of this layer, or null
 };
 // Per candidate c (logits row c of [nc, V]): E_ii, S_sa, acc update, flag.
-hipError_t launch_lens_admit(const float* logits, int V, const int32_t* cand, int nc, const double* F,
-                             const LensAdmitArgs& p, hipStream_t st);
+hipError_t launch_lens_admit(const float* logits, int V, const int32_t* cand, int nc, const int32_t* nc_dev,
+                             const double* F, const LensAdmitArgs& p, hipStream_t st);
 // The same from EPI_LENS_STATS tiles: stats [nc][ntiles][4].
 hipError_t launch_lens_admit_stats(const float* stats, int ntiles, const int32_t* cand, int nc,
-                                   const double* F, const LensAdmitArgs& p, hipStream_t st);
+                                   const int32_t* nc_dev, const double* F, const LensAdmitArgs& p,
+                                   hipStream_t st);
 // Zero `bytes` (a multiple of 4) of device memory with a kernel.
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 

@@ -170,8 +170,11 @@ __global__ void __launch_bounds__(256) qkv_finalize_kernel(
     const float* __restrict__ Pq, const float* __restrict__ Pk, const float* __restrict__ Pv,
     int split, int64_t pstride, int nq, int R, int d, int dh, const int32_t* __restrict__ q_rows,
     const int32_t* __restrict__ pos, const float2* __restrict__ rope, AT* __restrict__ Q,
-    AT* __restrict__ K, AT* __restrict__ V, int64_t ldvt) {
+    AT* __restrict__ K, AT* __restrict__ V, int64_t ldvt, const int32_t* __restrict__ nq_dev) {
   int b = blockIdx.x;
+  // nq is the bound the grid is sized for; with a device count the Q blocks
+  // past it have nothing to do
+  if (nq_dev && b < nq && b >= *nq_dev) return;
   if (ldvt > 0 && b >= nq + R) {
     // one 32 x 64 tile of V, written transposed
     __shared__ __attribute__((aligned(16))) uint16_t tT[64 * 40];  // [column][row], pitch 40
@@ -559,11 +562,101 @@ __global__ void __launch_bounds__(256) logits_argmax_kernel(const float* __restr
   if (tid == 0 && next) next[b] = bi[0];
 }
 
+// Index of this thread among the block's threads with `on` set (thread
+// order), and their number in `total`.  256 threads; every thread calls it.
+__device__ int block_rank(bool on, int* wtot, int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t m = __ballot(on);
+  const int below = __popcll(m & ((1ull << lane) - 1ull));
+  if (lane == 0) wtot[wave] = __popcll(m);
+  __syncthreads();
+  int base = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    base += w < wave ? wtot[w] : 0;
+    total += wtot[w];
+  }
+  __syncthreads();
+  return base + below;
+}
+
+// Bookkeeping of the online controller for layer l, on the device: one block,
+// one thread per packed row (R <= 256).  For l inside the decision window it
+// applies the layer's admissions (candidate c with flag[c] set: admit[row] =
+// l, the frozen target's bypass bit joins the row's code), writes every row's
+// code for layers l..L-1, builds layer l's row lists in `reg` (attention rows,
+// row -> slot map, FFN rows, row -> slot map; R ints each, rows in order) with
+// their counts at cnt[2 (l & 1)], and for l + 1 inside the window the next
+// candidate list (visual rows not admitted yet: cand[i] = row, cand[R + i] =
+// its sample) with its count at cnt[4].  l = -1 initialises the row state and
+// builds the candidate list of layer 0.
+__global__ void __launch_bounds__(256) online_plan_kernel(int l, int L, int Wn, int R, int bit,
+                                                          const int32_t* __restrict__ vis,
+                                                          const int32_t* __restrict__ flag,
+                                                          int32_t* __restrict__ cand, int32_t* __restrict__ admit,
+                                                          int32_t* __restrict__ code, uint8_t* __restrict__ codes,
+                                                          int32_t* __restrict__ reg, int32_t* __restrict__ cnt) {
+  __shared__ int wtot[4];
+  __shared__ int s_admit[256], s_code[256];
+  const int r = threadIdx.x;
+  const bool row = r < R;
+  if (row) {
+    s_admit[r] = l < 0 ? -1 : admit[r];
+    s_code[r] = l < 0 ? 0 : code[r];
+  }
+  const int nc = (l >= 0 && l < Wn) ? cnt[4] : 0;
+  const bool adm = r < nc && flag[r] != 0;
+  const int arow = adm ? cand[r] : 0;
+  __syncthreads();
+  if (adm) {
+    s_admit[arow] = l;
+    s_code[arow] |= bit;
+  }
+  __syncthreads();
+  const int a_r = row ? s_admit[r] : 0, c_r = row ? s_code[r] : 0;
+  if (row) {
+    admit[r] = a_r;
+    code[r] = c_r;
+  }
+  if (l >= 0) {
+    if (row)
+      for (int l2 = l; l2 < L; ++l2) codes[(size_t)l2 * R + r] = (uint8_t)c_r;
+    const bool onA = row && !(c_r & 1), onF = row && !(c_r & 2);
+    int nA, nF;
+    const int iA = block_rank(onA, wtot, nA);
+    const int iF = block_rank(onF, wtot, nF);
+    if (row) {
+      if (onA) reg[iA] = r;
+      reg[R + r] = onA ? iA : -1;
+      if (onF) reg[2 * R + iF] = r;
+      reg[3 * R + r] = onF ? iF : -1;
+    }
+    if (r == 0) {
+      cnt[2 * (l & 1)] = nA;
+      cnt[2 * (l & 1) + 1] = nF;
+    }
+  }
+  if (l + 1 < Wn) {
+    const bool on = row && vis[r] >= 0 && a_r < 0;
+    int n;
+    const int i = block_rank(on, wtot, n);
+    if (on) {
+      cand[i] = r;
+      cand[R + i] = vis[r];
+    }
+    if (r == 0) cnt[4] = n;
+  }
+}
+
 // ------------------------------------------------------------------ host side
 struct LayerTables {
   int nA = 0, nF = 0;
   int offA = -1, offF = -1;         // offsets of the row lists (ints)
   int offSlotA = -1, offSlotF = -1;  // offsets of the row -> slot maps
+  // >= 0: the live counts (attention rows, FFN rows) are the two ints at this
+  // offset on the device, and nA, nF are the bounds the launches are sized for
+  int offCnt = -1;
 };
 
 // Pinned host buffer for the row tables of one thread's prefill calls.  It is
@@ -715,23 +808,31 @@ PrefillWs prefill_layout(const spider_decoder_cfg& c, int R, char* base) {
 }
 
 // Integer tables of the online prefill (offsets in ints from the table base):
-// positions, sample starts, cu_seqlens, two regions for the row lists of the
-// current layer (alternating, so the slot map of the previous layer's pending
-// residual stays intact until it is consumed), then the candidate list and
-// the sample of each candidate.
+// positions, sample starts, cu_seqlens, the sample of every visual row (-1
+// for text rows), two regions for the row lists of the current layer
+// (alternating, so the slot map of the previous layer's pending residual stays
+// intact until it is consumed), the candidate list and the sample of each
+// candidate; then the row state kept on the device when the bookkeeping runs
+// there: admission layer and code per row, the list counts (attention and FFN
+// rows of the two regions, candidates) and the codes [L][R] as bytes.
 struct OnlineTabs {
-  int pos, start, cu, reg[2], cand, total;
+  int pos, start, cu, vis, reg[2], cand, admit, code, cnt, codes, total;
 };
 
-OnlineTabs online_tabs(int R, int B) {
+OnlineTabs online_tabs(int R, int B, int L) {
   OnlineTabs t;
   t.pos = 0;
   t.start = R;
   t.cu = 2 * R;
-  t.reg[0] = (2 * R + B + 1 + 63) / 64 * 64;
+  t.vis = 2 * R + B + 1;
+  t.reg[0] = (3 * R + B + 1 + 63) / 64 * 64;
   t.reg[1] = t.reg[0] + 4 * R;
   t.cand = t.reg[1] + 4 * R;
-  t.total = t.cand + 2 * R;
+  t.admit = t.cand + 2 * R;
+  t.code = t.admit + R;
+  t.cnt = t.code + R;
+  t.codes = t.cnt + 8;
+  t.total = t.codes + (int)(((int64_t)L * R + 3) / 4);
   return t;
 }
 
@@ -758,7 +859,7 @@ OnlineWs online_layout(const spider_decoder_cfg& c, int B, int R, int V, char* b
   OnlineWs w{};
   w.p = prefill_layout(c, R, cv);
   const size_t es = c.dtype == SPIDER_BF16 ? 2 : 4;
-  w.tab = reinterpret_cast<int32_t*>(cv.take((size_t)online_tabs(R, B).total * 4));
+  w.tab = reinterpret_cast<int32_t*>(cv.take((size_t)online_tabs(R, B, c.L).total * 4));
   w.hc = cv.take((size_t)R * c.d * es);
   w.tmean = reinterpret_cast<float*>(cv.take((size_t)B * c.d * 4));
   w.F = reinterpret_cast<double*>(cv.take((size_t)R * 8));
@@ -901,6 +1002,8 @@ struct PrefillRun {
   spider_status layer(int l, const LayerTables& T) {
     const spider_layer_weights& w = W[l];
     const int d = c.d, dh = d / c.H;
+    const int32_t* cntA = T.offCnt >= 0 ? tab + T.offCnt : nullptr;
+    const int32_t* cntF = T.offCnt >= 0 ? tab + T.offCnt + 1 : nullptr;
     const int64_t ps_ = pstride();
     AT* xn = reinterpret_cast<AT*>(ws.xn);
     AT* qb = reinterpret_cast<AT*>(ws.q);
@@ -930,6 +1033,7 @@ struct PrefillRun {
       if (T.nA > 0) {
         ga.ngroups = 3;
         ga.g[0] = GemmGroup{xn, tab + T.offA, T.nA, w.wq, nullptr, d, ws.Pq, d, ps_, 0, 0, 0};
+        ga.g[0].m_dev = cntA;
         ga.g[1] = gk;
         ga.g[2] = gv;
       } else {
@@ -965,7 +1069,7 @@ struct PrefillRun {
         const int vblocks = bf16() ? (vt_rows(R) / 32) * (d / 64) : R;
         qkv_finalize_kernel<AT><<<T.nA + R + vblocks, 256, 0, st>>>(
             ws.Pq, ws.Pk, ws.Pv, ga.split, ps_, T.nA, R, d, dh, tab + T.offA, dpos, ws.rope, qb, kb, vb,
-            ldvt);
+            ldvt, cntA);
         SPIDER_LAUNCHED("qkv_finalize");
         if (ck) {
           kv_store_kernel<AT><<<R, 256, 0, st>>>(kb, ws.Pv, ga.split, ps_, d, row_sample, dpos, ck, cv,
@@ -978,7 +1082,7 @@ struct PrefillRun {
       {
         ProfScope ps(KC_ATTENTION, st);
         AttnArgs aa{qb, tab + T.offA, kb, vb, bf16() ? (int64_t)vt_rows(R) : 0, dstart, ob, T.nA, R,
-                    c.H, dh, d, (float)(1.0 / std::sqrt((double)dh))};
+                    c.H, dh, d, (float)(1.0 / std::sqrt((double)dh)), cntA};
         hipError_t e = bf16() ? launch_attention_bf16(aa, st) : launch_attention_f32(aa, max_s, st);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "attention: %s", hipGetErrorString(e));
       }
@@ -988,6 +1092,7 @@ struct PrefillRun {
       go.lda = d;
       go.epilogue = EPI_PARTIAL_F32;
       go.g[0] = GemmGroup{ob, nullptr, T.nA, w.wo, nullptr, d, ws.Pres, d, ps_, 0, 0, 0};
+      go.g[0].m_dev = cntA;
       {
         ProfScope ps(KC_GEMM_O, st);
         hipError_t e = gemm(go, 8);
@@ -1011,6 +1116,7 @@ struct PrefillRun {
       gu.lda = d;
       gu.epilogue = EPI_SWIGLU;
       gu.g[0] = GemmGroup{xn, nullptr, T.nF, w.wg, w.wu, c.d_ff, act, c.d_ff, 0, 0, 0, 0};
+      gu.g[0].m_dev = cntF;
       // the QKV partials are consumed before attention: free scratch for the
       // GEMM's split tail tiles until the next layer's QKV GEMM
       gu.scratch = ws.Pq;
@@ -1026,6 +1132,7 @@ struct PrefillRun {
       gd.lda = c.d_ff;
       gd.epilogue = EPI_PARTIAL_F32;
       gd.g[0] = GemmGroup{act, nullptr, T.nF, w.wd, nullptr, d, ws.Pres, d, ps_, 0, 0, 0};
+      gd.g[0].m_dev = cntF;
       {
         ProfScope ps(KC_GEMM_DOWN, st);
         hipError_t e = gemm(gd, 8);
@@ -1093,12 +1200,36 @@ struct OnlineParams {
   double w1, w2, t_skip;
 };
 
+// Whether the online prefill keeps its bookkeeping on the device.  Needs at
+// most 256 rows (one thread per row in online_plan_kernel); every GEMM of the
+// call is then a streaming, LDS-staged or fp32 kernel whose split-K factor and
+// per-element summation order do not depend on the row count, so launches
+// sized for the bound and reading the live count on the device give the bits
+// of launches sized for the live rows.  Text rows never bypass, so each
+// sub-layer keeps at least B * n_text rows: five or more keep the static
+// prefill off the decode-row kernel, which is also what the bf16 logits lens
+// needs of its candidates.  The bf16 attention has to take its per-32-query
+// kernel at the bound as it does at the live count.
+bool online_on_device(const spider_decoder_cfg& c, int B, int R, int n_text, int nvis, int V) {
+  if (R > 256 || (int64_t)B * n_text < 5) return false;
+  if (c.dtype == SPIDER_BF16) {
+    if ((int64_t)ceil_div(R, 128) * c.H >= 128) return false;
+    if (!lens_fused(c, V) && nvis > 0 && nvis < 5) return false;
+  }
+  return true;
+}
+
 // Prefill with the online controller: at every layer l < floor(L/2) the
 // visual rows not yet in skip mode are scored on the hidden state entering
 // layer l, admitted rows get their frozen target bypassed from layer l on,
-// and layer l runs with the updated row lists.  The admission flags come back
-// to the host once per decision-window layer (the stream is synchronised
-// there); the row lists of layer l are built after it.
+// and layer l runs with the updated row lists.
+//
+// Up to 256 rows (online_on_device) the admissions, codes, candidate lists and
+// row lists stay on the device (online_plan_kernel after each window layer's
+// lens); every launch of a window layer is sized for its bound and reads the
+// live count, and the codes and admission layers come back once, at the end.
+// Otherwise the admission flags come back to the host once per window layer
+// (the stream is synchronised there) and the row lists are built there.
 template <typename AT>
 spider_status run_prefill_online(const spider_decoder_cfg& c, const spider_layer_weights* W, int B,
                                  const int32_t* cu, const void* x, const OnlineParams& op,
@@ -1106,19 +1237,131 @@ spider_status run_prefill_online(const spider_decoder_cfg& c, const spider_layer
                                  const OnlineWs& ows, hipStream_t st) {
   const bool bf16 = c.dtype == SPIDER_BF16;
   const int R = cu[B], L = c.L, Wn = c.L / 2, d = c.d;
-  const OnlineTabs ot = online_tabs(R, B);
+  const OnlineTabs ot = online_tabs(R, B, L);
   std::memset(codes, 0, (size_t)L * R);
   std::vector<int32_t> admit(R, -1);
 
   std::vector<int32_t> fixed(ot.reg[0], 0);
   const int max_s = fill_positions(B, cu, fixed.data() + ot.pos, fixed.data() + ot.start);
   std::copy(cu, cu + B + 1, fixed.begin() + ot.cu);
+  int nvis = 0;
+  for (int b = 0; b < B; ++b)
+    for (int r = cu[b]; r < cu[b + 1]; ++r) {
+      const bool visual = r < cu[b + 1] - op.n_text;
+      fixed[ot.vis + r] = visual ? b : -1;
+      nvis += visual;
+    }
+  const bool on_dev = online_on_device(c, B, R, op.n_text, nvis, op.V);
   SPIDER_TRY(upload_ints(fixed.data(), fixed.size(), ows.tab, st));
 
   PrefillRun<AT> run{c, W, h, ows.p, ows.tab, ows.tab + ot.pos, ows.tab + ot.start, R, max_s, st};
   SPIDER_TRY(run.begin(x));
   SPIDER_HIP(launch_fill_zero(ows.acc, (size_t)R * sizeof(double), st));
   if (s_sa_out && Wn > 0) SPIDER_HIP(launch_fill_zero(s_sa_out, (size_t)Wn * R * sizeof(float), st));
+
+  int32_t* dcand = ows.tab + ot.cand;
+  uint8_t* dcodes = reinterpret_cast<uint8_t*>(ows.tab + ot.codes);
+  // Logit lens and admission test of layer l over `nc` candidates (with
+  // nc_dev: a launch bound, the live count on the device); sets ows.flag.
+  auto lens = [&](int l, int nc, const int32_t* nc_dev) -> spider_status {
+    SPIDER_TRY(run.flush());
+    {
+      ProfScope ps(KC_LENS_PREP, st);
+      hipError_t e = launch_text_mean(h, d, ows.tab + ot.cu, B, op.n_text, ows.tmean, st);
+      if (e == hipSuccess)
+        e = launch_lens_prep(bf16, h, d, dcand, dcand + (nc_dev ? R : nc), nc, nc_dev, ows.tmean, ows.hc,
+                             ows.F, st);
+      SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lens_prep: %s", hipGetErrorString(e));
+    }
+    const bool fused = lens_fused(c, op.V);
+    const int ntiles = op.V / 128;
+    {
+      ProfScope ps(KC_GEMM_LENS, st);
+      GemmArgs gl{};
+      gl.ngroups = 1;
+      gl.K = d;
+      gl.lda = d;
+      hipError_t e = hipSuccess;
+      if (fused) {
+        // up to 256 candidates per launch (one pass over the unembedding each)
+        const int nchunk = (nc + 255) / 256;
+        const int per = (nc + nchunk - 1) / nchunk;
+        gl.epilogue = EPI_LENS_STATS;
+        for (int c0 = 0; c0 < nc && e == hipSuccess; c0 += per) {
+          const int mc = std::min(per, nc - c0);
+          GemmArgs gc = gl;
+          gc.g[0] = GemmGroup{reinterpret_cast<const uint16_t*>(ows.hc) + (size_t)c0 * d, nullptr, mc,
+                              op.wu, nullptr, op.V, ows.stats + (size_t)c0 * ntiles * 4, ntiles, 0,
+                              0, 0, 0};
+          gc.g[0].m_dev = nc_dev;  // one launch then (nc <= 256)
+          e = launch_gemm_bf16(gc, 1, st);
+        }
+      } else {
+        gl.epilogue = EPI_PARTIAL_F32;
+        gl.g[0] = GemmGroup{ows.hc, nullptr, nc, op.wu, nullptr, op.V, ows.logits, op.V,
+                            (int64_t)nc * op.V, 0, 0, 0};
+        gl.g[0].m_dev = nc_dev;
+        e = bf16 ? launch_gemm_bf16(gl, 1, st) : launch_gemm_f32(gl, 1, st);
+      }
+      SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_lens: %s", hipGetErrorString(e));
+    }
+    {
+      ProfScope ps(KC_LENS_ADMIT, st);
+      LensAdmitArgs p{std::log((double)op.V), op.w1, op.w2 * op.slc_sel[l], op.t_skip, ows.acc, ows.flag,
+                      s_sa_out ? s_sa_out + (size_t)l * R : nullptr};
+      hipError_t e = fused ? launch_lens_admit_stats(ows.stats, ntiles, dcand, nc, nc_dev, ows.F, p, st)
+                           : launch_lens_admit(ows.logits, op.V, dcand, nc, nc_dev, ows.F, p, st);
+      SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lens_admit: %s", hipGetErrorString(e));
+    }
+    return SPIDER_OK;
+  };
+  auto grow_back = [&](size_t bytes) -> spider_status {
+    if (g_back.cap < bytes) {
+      if (g_back.host) SPIDER_HIP(hipHostFree(g_back.host));
+      g_back.host = nullptr;
+      g_back.cap = 0;
+      SPIDER_HIP(hipHostMalloc(&g_back.host, bytes));
+      g_back.cap = bytes;
+    }
+    return SPIDER_OK;
+  };
+
+  if (on_dev) {
+    auto plan = [&](int l) -> spider_status {
+      const int bit = (l >= 0 && l < Wn) ? (op.target[l] == 1 ? 2 : 1) : 0;
+      online_plan_kernel<<<1, 256, 0, st>>>(l, L, Wn, R, bit, ows.tab + ot.vis, ows.flag, dcand,
+                                            ows.tab + ot.admit, ows.tab + ot.code, dcodes,
+                                            ows.tab + ot.reg[l > 0 ? (l & 1) : 0], ows.tab + ot.cnt);
+      SPIDER_LAUNCHED("online_plan");
+      return SPIDER_OK;
+    };
+    SPIDER_TRY(plan(-1));
+    LayerTables T;
+    for (int l = 0; l < L; ++l) {
+      if (l < Wn && nvis > 0) SPIDER_TRY(lens(l, nvis, ows.tab + ot.cnt + 4));
+      if (l <= Wn) {
+        SPIDER_TRY(plan(l));
+        const int rg = ot.reg[l & 1];
+        T.nA = T.nF = R;
+        T.offA = rg;
+        T.offSlotA = rg + R;
+        T.offF = rg + 2 * R;
+        T.offSlotF = rg + 3 * R;
+        T.offCnt = ot.cnt + 2 * (l & 1);
+      }
+      SPIDER_TRY(run.layer(l, T));
+    }
+    SPIDER_TRY(run.flush());
+    const size_t cbytes = (size_t)L * R, abytes = (size_t)R * sizeof(int32_t);
+    SPIDER_TRY(grow_back(abytes + cbytes));
+    uint8_t* back = reinterpret_cast<uint8_t*>(g_back.host);
+    SPIDER_HIP(hipMemcpyAsync(back, ows.tab + ot.admit, abytes, hipMemcpyDeviceToHost, st));
+    SPIDER_HIP(hipMemcpyAsync(back + abytes, dcodes, cbytes, hipMemcpyDeviceToHost, st));
+    SPIDER_HIP(hipStreamSynchronize(st));
+    std::memcpy(codes, back + abytes, cbytes);
+    if (admit_out) std::memcpy(admit_out, back, abytes);
+    return SPIDER_OK;
+  }
 
   std::vector<int32_t> cand, lists;
   LayerTables T;
@@ -1133,61 +1376,10 @@ spider_status run_prefill_online(const spider_decoder_cfg& c, const spider_layer
         for (int b = 0; b < B; ++b)
           for (int r = cu[b]; r < cu[b + 1] - op.n_text; ++r)
             if (admit[r] < 0) cand.push_back(b);
-        SPIDER_TRY(run.flush());
-        int32_t* dcand = ows.tab + ot.cand;
         SPIDER_TRY(upload_ints(cand.data(), cand.size(), dcand, st));
-        {
-          ProfScope ps(KC_LENS_PREP, st);
-          hipError_t e = launch_text_mean(h, d, ows.tab + ot.cu, B, op.n_text, ows.tmean, st);
-          if (e == hipSuccess) e = launch_lens_prep(bf16, h, d, dcand, dcand + nc, nc, ows.tmean, ows.hc, ows.F, st);
-          SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lens_prep: %s", hipGetErrorString(e));
-        }
-        const bool fused = lens_fused(c, op.V);
-        const int ntiles = op.V / 128;
-        {
-          ProfScope ps(KC_GEMM_LENS, st);
-          GemmArgs gl{};
-          gl.ngroups = 1;
-          gl.K = d;
-          gl.lda = d;
-          hipError_t e = hipSuccess;
-          if (fused) {
-            // up to 256 candidates per launch (one pass over the unembedding each)
-            const int nchunk = (nc + 255) / 256;
-            const int per = (nc + nchunk - 1) / nchunk;
-            gl.epilogue = EPI_LENS_STATS;
-            for (int c0 = 0; c0 < nc && e == hipSuccess; c0 += per) {
-              const int mc = std::min(per, nc - c0);
-              GemmArgs gc = gl;
-              gc.g[0] = GemmGroup{reinterpret_cast<const uint16_t*>(ows.hc) + (size_t)c0 * d, nullptr, mc,
-                                  op.wu, nullptr, op.V, ows.stats + (size_t)c0 * ntiles * 4, ntiles, 0,
-                                  0, 0, 0};
-              e = launch_gemm_bf16(gc, 1, st);
-            }
-          } else {
-            gl.epilogue = EPI_PARTIAL_F32;
-            gl.g[0] = GemmGroup{ows.hc, nullptr, nc, op.wu, nullptr, op.V, ows.logits, op.V,
-                                (int64_t)nc * op.V, 0, 0, 0};
-            e = bf16 ? launch_gemm_bf16(gl, 1, st) : launch_gemm_f32(gl, 1, st);
-          }
-          SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_lens: %s", hipGetErrorString(e));
-        }
-        {
-          ProfScope ps(KC_LENS_ADMIT, st);
-          LensAdmitArgs p{std::log((double)op.V), op.w1, op.w2 * op.slc_sel[l], op.t_skip, ows.acc, ows.flag,
-                          s_sa_out ? s_sa_out + (size_t)l * R : nullptr};
-          hipError_t e = fused ? launch_lens_admit_stats(ows.stats, ntiles, dcand, nc, ows.F, p, st)
-                               : launch_lens_admit(ows.logits, op.V, dcand, nc, ows.F, p, st);
-          SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lens_admit: %s", hipGetErrorString(e));
-        }
+        SPIDER_TRY(lens(l, nc, nullptr));
         const size_t fbytes = (size_t)nc * sizeof(int32_t);
-        if (g_back.cap < fbytes) {
-          if (g_back.host) SPIDER_HIP(hipHostFree(g_back.host));
-          g_back.host = nullptr;
-          g_back.cap = 0;
-          SPIDER_HIP(hipHostMalloc(&g_back.host, fbytes));
-          g_back.cap = fbytes;
-        }
+        SPIDER_TRY(grow_back(fbytes));
         SPIDER_HIP(hipMemcpyAsync(g_back.host, ows.flag, fbytes, hipMemcpyDeviceToHost, st));
         SPIDER_HIP(hipStreamSynchronize(st));
         const int32_t* flag = reinterpret_cast<const int32_t*>(g_back.host);
