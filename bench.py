@@ -219,11 +219,40 @@ def cpu_baseline(w, n_layers: int, W_dev=None):
                        f"skip codes), decoder time extrapolated by {w.dec.L}/{n_layers}; {rows} rows")}
 
 
+def kmeans_passes(attn, feats, n_anchor, K, max_iter):
+    """Lloyd passes per tile that read the features in a call allowed max_iter of them:
+    pass 1, then every pass up to and including the first that changes no assignment
+    (the launches after it return at once).  Found from the assignments after
+    1, 2, ... passes, each its own call."""
+    from paper_2609_34977_amd import _lib
+
+    prev, passes = None, None
+    for k in range(1, max_iter + 1):
+        cl = _lib.score(attn, feats, n_anchor, K, k)["cluster"]
+        if prev is None:
+            passes = torch.full((cl.shape[0],), max_iter, dtype=torch.int64, device=cl.device)
+        else:
+            settled = (cl == prev).all(dim=1) & (passes == max_iter)
+            passes[settled] = k
+        prev = cl
+    return passes.cpu()
+
+
 def score_sweep(w, dev, args):
     """Scoring (spider_score) over many tiles: time per call, and the compulsory
     HBM bytes (CLS attention + every tapped layer's features, read once, plus
     the outputs) over that time.  Tiles are the workload's synthetic tiles
-    repeated up to G (20 distinct tiles are generated)."""
+    repeated up to G (20 distinct tiles are generated).
+
+    Per kernel class also the effective bytes its design reads from HBM (each
+    input row once per pass that reads it; L2 re-reads of the anchors and
+    centroids not counted) and the rate they imply:
+      score_prep     CLS rows + every tapped layer's rows, a_i and 1/|F| out
+      anchor_topk    a in, anchor and non-anchor lists out
+      anchor_maxsim  the last layer's rows, m out
+      kmeans         the last layer's non-anchor rows once per working pass
+      score_final    every tapped layer's non-anchor rows twice (cluster sums,
+                     scores), cluster ids and scores out"""
     import dataclasses
     from synth.vision import vision_inputs
     from paper_2609_34977_amd import _lib
@@ -233,31 +262,43 @@ def score_sweep(w, dev, args):
     attn0, feats0 = vision_inputs(base, w.seed)
     attn0, feats0 = attn0.to(dev), [f.to(dev) for f in feats0]
     n_anchor, _ = _lib.budget(sc.keep, sc.r_num, sc.r_den)
+    na = min(n_anchor, sc.n)
+    passes0 = kmeans_passes(attn0, feats0, na, sc.K, sc.kmeans_iter)
     for G in (20, 64, 256, 512):
         reps = (G + 19) // 20
         attn = attn0.repeat(reps, 1, 1)[:G].contiguous()
         feats = [f.repeat(reps, 1, 1)[:G].contiguous() for f in feats0]
+        passes = int(passes0.repeat(reps)[:G].sum())
         for _ in range(2):
-            _lib.score(attn, feats, min(n_anchor, sc.n), sc.K, sc.kmeans_iter)
+            _lib.score(attn, feats, na, sc.K, sc.kmeans_iter)
         torch.cuda.synchronize()
         _lib.profile_mask(None)
         _lib.profile_enable(True)
         iters = 5
         t0 = time.perf_counter()
         for _ in range(iters):
-            _lib.score(attn, feats, min(n_anchor, sc.n), sc.K, sc.kmeans_iter)
+            _lib.score(attn, feats, na, sc.K, sc.kmeans_iter)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
         prof = _lib.profile_read()
         _lib.profile_enable(False)
         ms = (t1 - t0) * 1e3 / iters
         H, n, dv = attn.shape[1], sc.n, feats[0].shape[2]
-        byts = G * (H * (n + 1) * 4 + len(feats) * n * dv * feats[0].element_size() + 16 * n)
+        es, nl, m = feats[0].element_size(), len(feats), n - na
+        byts = G * (H * (n + 1) * 4 + nl * n * dv * es + 16 * n)
+        row = dv * es
+        eff = {"score_prep": G * (H * n * 4 + nl * n * row + (1 + nl) * n * 4),
+               "anchor_topk": G * 3 * n * 4,
+               "anchor_maxsim": G * (n * row + n * 4),
+               "kmeans": passes * m * row,
+               "score_final": G * (2 * nl * m * row + 8 * n)}
         kms = {k: round(v[1] / iters, 4) for k, v in prof.items() if v[0]}
+        kgb = {k: round(eff[k] / (kms[k] * 1e-3) / 1e9, 1) for k in eff if kms.get(k)}
         ach = byts / (ms * 1e-3) / 1e9
         print(json.dumps({"mode": "score_sweep", "tiles": G, "ms_per_call": ms,
                           "compulsory_bytes": byts, "achieved_GBs": ach, "frac_of_hbm_peak": ach / HBM_PEAK_GBS,
-                          "kernel_ms_per_call": kms}), flush=True)
+                          "kernel_ms_per_call": kms, "kmeans_working_passes": passes,
+                          "kernel_effective_bytes": eff, "kernel_effective_GBs": kgb}), flush=True)
         del attn, feats
         torch.cuda.empty_cache()
 

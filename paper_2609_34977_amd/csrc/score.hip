@@ -5,7 +5,7 @@
 //   u^l_i = F^l_i / |F^l_i|,  mu^l_C = mean_{j in C} u^l_j.
 //
 // Kernels (all per tile g, enqueued in this order):
-//   score_prep     grid (ceil(n/4), G) x 256: a_i (sequential fp32 head sum,
+//   score_prep     grid (ceil(n/16), G) x 256: a_i (sequential fp32 head sum,
 //                  then one IEEE division) and 1/|F^l_i| for every tapped layer.
 //   anchor_topk    grid G x 1024: LDS bitonic sort of 64-bit keys
 //                  (~order(a), i); the first n_anchor are the anchors; block
@@ -55,7 +55,11 @@ struct Feat<float> {
     return {*reinterpret_cast<const floatx4*>(p), *reinterpret_cast<const floatx4*>(p + 4)};
   }
   __device__ static inline float raw_at(const Raw& v, int e) { return e < 4 ? v.a[e] : v.b[e - 4]; }
-  static constexpr int kPrepRowBatch = 4;
+  __device__ static inline Raw load8_nt(const float* p) {
+    return {__builtin_nontemporal_load(reinterpret_cast<const floatx4*>(p)),
+            __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(p + 4))};
+  }
+  static constexpr int kPrepRowBatch = 2;
 };
 template <>
 struct Feat<uint16_t> {
@@ -72,10 +76,13 @@ struct Feat<uint16_t> {
   __device__ static inline float load1(const uint16_t* p) { return bf16_bits_to_f32(*p); }
   typedef u32x4 Raw;
   __device__ static inline Raw load8_raw(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+  __device__ static inline Raw load8_nt(const uint16_t* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  }
   __device__ static inline float raw_at(const Raw& v, int e) {
     return __uint_as_float((e & 1) ? (v[e >> 1] & 0xFFFF0000u) : (v[e >> 1] << 16));
   }
-  static constexpr int kPrepRowBatch = 8;
+  static constexpr int kPrepRowBatch = 4;
 };
 
 struct FeatArgs {
@@ -108,40 +115,31 @@ __device__ inline void load_slice(const FT* row, int d, int lane, float* x) {
 __device__ inline int slice_dim(int v, int lane) { return (v >> 3) * 512 + lane * 8 + (v & 7); }
 
 // ------------------------------------------------------------- score_prep
-// Row norms of every tapped layer and the head-mean anchor scores, 32 patches
+// Row norms of every tapped layer and the head-mean anchor scores, 16 patches
 // per block (the compulsory single read of the features and the CLS rows).
-// Each wave owns 8 patches; per tapped layer it issues the 16-byte loads of
-// a batch of rows (8 bf16 / 4 fp32 rows, NCH chunks of 512 elements each)
-// before reducing any of them.  Ordinary loads: the later passes re-read the
-// same rows, from the last-level cache while the tiles fit in it.  A lane
-// sums its chunks in ascending order and the wave sum is a fixed butterfly.
-// Threads 0..31 own one patch's head mean each: all head loads are issued
-// (8 at a time) before the sum, which runs over h = 0..H-1 in order, then one
-// IEEE division.
-constexpr int kPrepRows = 32;
+// Each wave owns 4 patches; per tapped layer it issues the 16-byte loads of
+// a batch of rows (4 bf16 / 2 fp32 rows, NCH chunks of 512 elements each)
+// before reducing any of them.  Small batches keep the kernel at ~58 VGPRs,
+// 8 waves per SIMD: more waves in flight moved more bytes than more loads per
+// wave (8-row batches at 97 VGPRs ran 35 % slower).  A lane sums its chunks
+// in ascending order and the wave sum is a fixed butterfly.  The last 16
+// threads own one patch's head mean each, after their rows: all head loads
+// are issued (8 at a time) before the sum, which runs over h = 0..H-1 in
+// order, then one IEEE division.  Loads are non-temporal when the features
+// exceed the last-level cache (kPrepNtBytes): the later passes re-read the
+// same rows, from that cache while the tiles fit in it, and from HBM anyway
+// once they do not.
+constexpr int kPrepRows = 16;
+constexpr int64_t kPrepNtBytes = 256ll << 20;  // MI355X Infinity Cache
 
-template <typename FT, int NCH>
+template <typename FT, int NCH, bool NT>
 __global__ void __launch_bounds__(256) score_prep_kernel(
     int n, int H, int d, int n_layers, const float* __restrict__ attn, int64_t as_g,
     int64_t as_h, int col0, FeatArgs fa, float* __restrict__ a_out, float* __restrict__ nu) {
   const int g = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int i0 = blockIdx.x * kPrepRows;
-  if (attn && threadIdx.x < kPrepRows && i0 + (int)threadIdx.x < n) {  // null: scores given in a_out
-    const int i = i0 + threadIdx.x;
-    const float* col = attn + (int64_t)g * as_g + col0 + i;
-    float acc = 0.f;
-    for (int h0 = 0; h0 < H; h0 += 8) {
-      float v[8];
-#pragma unroll
-      for (int t = 0; t < 8; ++t) v[t] = h0 + t < H ? col[(int64_t)(h0 + t) * as_h] : 0.f;
-#pragma unroll
-      for (int t = 0; t < 8; ++t)
-        if (h0 + t < H) acc = __fadd_rn(acc, v[t]);
-    }
-    a_out[(int64_t)g * n + i] = __fdiv_rn(acc, (float)H);
-  }
-  constexpr int RW = 8;  // rows per wave, in batches of RB
+  constexpr int RW = kPrepRows / 4;  // rows per wave, in batches of RB
   constexpr int RB = Feat<FT>::kPrepRowBatch;
   const int r0 = i0 + RW * wave;
   for (int l = 0; l < n_layers; ++l) {
@@ -154,7 +152,7 @@ __global__ void __launch_bounds__(256) score_prep_kernel(
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
           const int e0 = lane * 8 + 512 * c;
-          if (e0 < d) x[r][c] = Feat<FT>::load8_raw(row + e0);
+          if (e0 < d) x[r][c] = NT ? Feat<FT>::load8_nt(row + e0) : Feat<FT>::load8_raw(row + e0);
         }
       }
 #pragma unroll
@@ -175,18 +173,38 @@ __global__ void __launch_bounds__(256) score_prep_kernel(
       }
     }
   }
+  const int t = threadIdx.x - (256 - kPrepRows);
+  if (attn && t >= 0 && i0 + t < n) {  // null: scores given in a_out
+    const int i = i0 + t;
+    const float* col = attn + (int64_t)g * as_g + col0 + i;
+    float acc = 0.f;
+    for (int h0 = 0; h0 < H; h0 += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = h0 + u < H ? col[(int64_t)(h0 + u) * as_h] : 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (h0 + u < H) acc = __fadd_rn(acc, v[u]);
+    }
+    a_out[(int64_t)g * n + i] = __fdiv_rn(acc, (float)H);
+  }
 }
 
 template <typename FT>
 void launch_score_prep(int G, int n, int H, int d, int n_layers, const float* attn, int64_t as_g, int64_t as_h,
                        int col0, const FeatArgs& fa, float* a_out, float* nu, hipStream_t st) {
   const dim3 grid(ceil_div(n, kPrepRows), G);
-  if (d <= 512)
-    score_prep_kernel<FT, 1><<<grid, 256, 0, st>>>(n, H, d, n_layers, attn, as_g, as_h, col0, fa, a_out, nu);
-  else if (d <= 1024)
-    score_prep_kernel<FT, 2><<<grid, 256, 0, st>>>(n, H, d, n_layers, attn, as_g, as_h, col0, fa, a_out, nu);
-  else
-    score_prep_kernel<FT, 4><<<grid, 256, 0, st>>>(n, H, d, n_layers, attn, as_g, as_h, col0, fa, a_out, nu);
+  const bool nt = (int64_t)G * n * d * (int64_t)sizeof(FT) * n_layers > kPrepNtBytes;
+#define SPIDER_PREP(NCH_, NT_) \
+  score_prep_kernel<FT, NCH_, NT_><<<grid, 256, 0, st>>>(n, H, d, n_layers, attn, as_g, as_h, col0, fa, a_out, nu)
+  if (d <= 512) {
+    if (nt) SPIDER_PREP(1, true); else SPIDER_PREP(1, false);
+  } else if (d <= 1024) {
+    if (nt) SPIDER_PREP(2, true); else SPIDER_PREP(2, false);
+  } else {
+    if (nt) SPIDER_PREP(4, true); else SPIDER_PREP(4, false);
+  }
+#undef SPIDER_PREP
 }
 
 // ------------------------------------------------------------- anchor_topk

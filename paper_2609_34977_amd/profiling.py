@@ -298,6 +298,16 @@ def sweep_table(args):
             lines.append(f"| {r['tiles']} | {r['ms_per_call']:.3f} | {r['compulsory_bytes'] / 1e6:.1f} | "
                          f"{r['frac_of_hbm_peak']:.3f} | " +
                          " | ".join(f"{r['kernel_ms_per_call'].get(k, 0):.4f}" for k in ks) + " |")
+        if "kernel_effective_GBs" in rows[0]:
+            ke = list(rows[0]["kernel_effective_GBs"])
+            lines += ["", "Per kernel class: effective MB (what its design reads and writes once per pass), "
+                          "GB/s and fraction of the 8 TB/s HBM peak.", "",
+                      "| tiles | K-means working passes | " +
+                      " | ".join(f"{k} MB / GB/s / frac" for k in ke) + " |", "|---|---|" + "---|" * len(ke)]
+            for r in rows:
+                lines.append(f"| {r['tiles']} | {r['kmeans_working_passes']} | " + " | ".join(
+                    f"{r['kernel_effective_bytes'][k] / 1e6:.1f} / {r['kernel_effective_GBs'].get(k, 0):.0f} / "
+                    f"{r['kernel_effective_GBs'].get(k, 0) / 8000:.2f}" for k in ke) + " |")
     with open(args.out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
