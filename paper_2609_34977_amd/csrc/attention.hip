@@ -26,6 +26,9 @@ namespace spider {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+// The online softmax keeps a stale running max until a key block's max
+// exceeds it by this much in the base-2 exponent (weights <= 2^kLazyLog2).
+constexpr float kLazyLog2 = 8.0f;
 
 typedef float float2v __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
@@ -70,7 +73,18 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
   }
   const int jb0 = lo_row & ~31;
   const int nblk = (hi_row - jb0) / 32 + 1;
+  // a key block [j0, j0 + 31] is fully visible to every valid query iff
+  // j0 >= st_max and j0 + 31 <= q_min (invalid lanes store nothing)
+  int st_max = qok ? qstart : -1, q_min = qok ? qrow : 0x7FFFFFFF;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    st_max = max(st_max, __shfl_xor(st_max, o, 64));
+    q_min = min(q_min, __shfl_xor(q_min, o, 64));
+  }
+  st_max = __builtin_amdgcn_readfirstlane(st_max);
+  q_min = __builtin_amdgcn_readfirstlane(q_min);
   const float sc = a.scale * kLog2e;
+  const float lazy = kLazyLog2 / sc;  // in raw score units
   float m_run = -INFINITY, l_run = 0.f;
   floatx16 o[DH / 32];
 #pragma unroll
@@ -102,40 +116,51 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int t = 0; t < DH / 16; ++t)
       s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[t]), qf[t], s, 0, 0, 0);
-    // ---- online softmax (this lane: query lo, keys 8*(r/4) + 4*hi + r%4)
+    // ---- online softmax (this lane: query lo, keys 8*(r/4) + 4*hi + r%4) on
+    // the raw scores, as in attention_wide_kernel: masks only where some query
+    // cannot see the whole key block, the scale folded into the exponent's
+    // FMA, a lazily moved running max and a vote before any rescale.
+    const bool full = j0 >= st_max && j0 + 31 <= q_min;
     float mx = -INFINITY;
+    if (full) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = j0 + 8 * (r >> 2) + 4 * hi + (r & 3);
-      const bool vis = qok && key >= qstart && key <= qrow;
-      s[r] = vis ? s[r] * sc : -INFINITY;
-      mx = fmaxf(mx, s[r]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    float alpha = 1.f, sum = 0.f;
-    float p[16];
-    if (m_new == -INFINITY) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) p[r] = 0.f;
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
     } else {
-      alpha = exp2f(m_run - m_new);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        p[r] = exp2f(s[r] - m_new);
-        sum += p[r];
+        const int key = j0 + 8 * (r >> 2) + 4 * hi + (r & 3);
+        const bool vis = qok && key >= qstart && key <= qrow;
+        s[r] = vis ? s[r] : -INFINITY;
+        mx = fmaxf(mx, s[r]);
       }
     }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const bool move = mx > m_run + lazy;
+    const float m_new = move ? mx : m_run;
+    const float msc = m_new == -INFINITY ? 0.f : m_new * sc;  // no visible key yet: weights 0
+    const float alpha = move ? __builtin_amdgcn_exp2f(fmaf(m_run, sc, -msc)) : 1.f;
+    float p[16], s0 = 0.f, s1 = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; r += 2) {
+      p[r] = __builtin_amdgcn_exp2f(fmaf(s[r], sc, -msc));
+      p[r + 1] = __builtin_amdgcn_exp2f(fmaf(s[r + 1], sc, -msc));
+      s0 += p[r];
+      s1 += p[r + 1];
+    }
+    float sum = s0 + s1;
     sum += __shfl_xor(sum, 32, 64);
     l_run = l_run * alpha + sum;
     m_run = m_new;
+    if (__any(move)) {
 #pragma unroll
-    for (int c = 0; c < DH / 32; ++c)
+      for (int c = 0; c < DH / 32; ++c)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[c][r] *= alpha;
+        for (int r = 0; r < 16; ++r) o[c][r] *= alpha;
+    }
     // ---- O^T += V^T P^T, two k-blocks of 16 keys.  The fp32 weights enter the
-    // bf16 MFMA as hi + lo parts (hi = bf16(p), lo = bf16(p - hi)), so P keeps
-    // ~16 significant bits and the softmax stays fp32 up to that split.
+    // bf16 MFMA as hi + lo parts (hi = bf16(p), lo = bf16(p - hi), hardware
+    // round to nearest even), so P keeps ~16 significant bits and the softmax
+    // stays fp32 up to that split.
     bf16x8 pf[2][2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -143,10 +168,9 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float a0 = p[8 * u + 2 * e], a1 = p[8 * u + 2 * e + 1];
-        const uint16_t h0 = f32_to_bf16_bits(a0), h1 = f32_to_bf16_bits(a1);
-        wh[e] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        wl[e] = (uint32_t)f32_to_bf16_bits(a0 - bf16_bits_to_f32(h0)) |
-                ((uint32_t)f32_to_bf16_bits(a1 - bf16_bits_to_f32(h1)) << 16);
+        wh[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(float2v{a0, a1}, bf16x2v));
+        const float2v rest{a0 - __uint_as_float(wh[e] << 16), a1 - __uint_as_float(wh[e] & 0xFFFF0000u)};
+        wl[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(rest, bf16x2v));
       }
       pf[u][0] = __builtin_bit_cast(bf16x8, u32x4{wh[0], wh[1], wh[2], wh[3]});
       pf[u][1] = __builtin_bit_cast(bf16x8, u32x4{wl[0], wl[1], wl[2], wl[3]});
@@ -181,7 +205,8 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
   float M = m_run;
 #pragma unroll
   for (int w = 0; w < NW - 1; ++w) M = fmaxf(M, xm[w][lo]);
-  const float f0 = m_run == -INFINITY ? 0.f : exp2f(m_run - M);
+  const float Msc = M * sc;  // maxima are raw scores; weights exp2((m - M) sc)
+  const float f0 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(fmaf(m_run, sc, -Msc));
   float L = f0 * l_run;
 #pragma unroll
   for (int c = 0; c < DH / 32; ++c)
@@ -190,7 +215,7 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
 #pragma unroll
   for (int w = 0; w < NW - 1; ++w) {
     const float mw = xm[w][lo];
-    const float fw = mw == -INFINITY ? 0.f : exp2f(mw - M);
+    const float fw = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(fmaf(mw, sc, -Msc));
     L += fw * xl[w][lo];
     const float* srcp = xo[w] + lane * 64;
 #pragma unroll
@@ -320,6 +345,7 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
   };
 
   const float sc = a.scale * kLog2e;
+  const float lazy = kLazyLog2 / sc;  // in raw score units
   float m_run[QT], l_run[QT];
   floatx16 o[QT][DH / 32];
 #pragma unroll
@@ -362,8 +388,11 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
     __builtin_amdgcn_sched_barrier(0);
     // Online softmax on the raw scores: the scale enters the exponent through
     // one FMA, exp2 is the hardware instruction, keys are masked only in key
-    // blocks some query of the wave cannot fully see, and the accumulators
-    // are rescaled only when some lane's running max moved.
+    // blocks some query of the wave cannot fully see.  The running max moves
+    // only when the block's max exceeds it by more than kLazyLog2 in the
+    // exponent (weights then stay below 2^kLazyLog2), so the accumulators are
+    // rescaled a few times per query instead of at almost every key block;
+    // a rescale runs when some lane's max moved (wave vote).
     const bool full = j0 >= wst_max && j0 + 31 <= wq_min;
     bf16x8 pf[QT][2][2];
 #pragma unroll
@@ -382,25 +411,24 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
         }
       }
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run[t], mx);
-      float alpha = 1.f, sum = 0.f;
-      float p[16];
-      if (m_new == -INFINITY) {
+      const bool move = mx > m_run[t] + lazy;
+      const float m_new = move ? mx : m_run[t];
+      // no visible key yet: every weight is exp2(-inf) = 0
+      const float msc = m_new == -INFINITY ? 0.f : m_new * sc;
+      const float alpha = move ? __builtin_amdgcn_exp2f(fmaf(m_run[t], sc, -msc)) : 1.f;
+      float p[16], s0 = 0.f, s1 = 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) p[r] = 0.f;
-      } else {
-        const float msc = m_new * sc;
-        alpha = __builtin_amdgcn_exp2f(fmaf(m_run[t], sc, -msc));
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          p[r] = __builtin_amdgcn_exp2f(fmaf(s[t][r], sc, -msc));
-          sum += p[r];
-        }
+      for (int r = 0; r < 16; r += 2) {
+        p[r] = __builtin_amdgcn_exp2f(fmaf(s[t][r], sc, -msc));
+        p[r + 1] = __builtin_amdgcn_exp2f(fmaf(s[t][r + 1], sc, -msc));
+        s0 += p[r];
+        s1 += p[r + 1];
       }
+      float sum = s0 + s1;
       sum += __shfl_xor(sum, 32, 64);
       l_run[t] = l_run[t] * alpha + sum;
       m_run[t] = m_new;
-      if (__any(alpha != 1.f)) {
+      if (__any(move)) {
 #pragma unroll
         for (int c = 0; c < DH / 32; ++c)
 #pragma unroll
