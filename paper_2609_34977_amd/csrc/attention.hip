@@ -30,6 +30,14 @@ constexpr float kLog2e = 1.4426950408889634f;
 // exceeds it by this much in the base-2 exponent (weights <= 2^kLazyLog2).
 constexpr float kLazyLog2 = 8.0f;
 
+// Lane l and lane l ^ 32 of a value, as (lower-half lane's, upper-half lane's)
+// in both lanes of the pair: one v_permlane32_swap, no LDS round trip (a
+// ds_bpermute's lgkmcnt wait would also wait for every fragment read in flight).
+__device__ __forceinline__ float2 lane_pair(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 typedef float float2v __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 
@@ -134,7 +142,10 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
         mx = fmaxf(mx, s[r]);
       }
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    {
+      const float2 pm = lane_pair(mx);
+      mx = fmaxf(pm.x, pm.y);
+    }
     const bool move = mx > m_run + lazy;
     const float m_new = move ? mx : m_run;
     const float msc = m_new == -INFINITY ? 0.f : m_new * sc;  // no visible key yet: weights 0
@@ -147,8 +158,8 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
       s0 += p[r];
       s1 += p[r + 1];
     }
-    float sum = s0 + s1;
-    sum += __shfl_xor(sum, 32, 64);
+    const float2 ps = lane_pair(s0 + s1);
+    const float sum = ps.x + ps.y;
     l_run = l_run * alpha + sum;
     m_run = m_new;
     if (__any(move)) {
@@ -410,7 +421,10 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
           mx = fmaxf(mx, s[t][r]);
         }
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      {
+        const float2 pm = lane_pair(mx);
+        mx = fmaxf(pm.x, pm.y);
+      }
       const bool move = mx > m_run[t] + lazy;
       const float m_new = move ? mx : m_run[t];
       // no visible key yet: every weight is exp2(-inf) = 0
@@ -424,8 +438,8 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
         s0 += p[r];
         s1 += p[r + 1];
       }
-      float sum = s0 + s1;
-      sum += __shfl_xor(sum, 32, 64);
+      const float2 ps = lane_pair(s0 + s1);
+      const float sum = ps.x + ps.y;
       l_run[t] = l_run[t] * alpha + sum;
       m_run[t] = m_new;
       if (__any(move)) {
