@@ -239,15 +239,22 @@ def mfma(args):
                 if re.search(pat, name):
                     d = per.setdefault(label, {}).setdefault(r["Dispatch_Id"], {})
                     d[r["Counter_Name"]] = float(r["Counter_Value"])
+                    d["ns"] = float(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
                     break
     lines = [f"# {args.title}", "", "Command (repository root, one MI355X; `cd /tmp && export TMPDIR=/tmp` first):",
              "", "```"] + (args.command or []) + ["```", "",
              "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x SQ_BUSY_CYCLES / 32 shader engines), "
              "summed over the group's dispatches; flops = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 (an exact "
              "count of the MFMA work issued).  Counter runs serialise dispatches, so these fractions "
-             "describe the kernels themselves, not the step's overlap.", "",
-             "| kernel group | dispatches | MFMA busy | TFLOP issued (all dispatches) | TFLOP/s while running |",
-             "|---|---|---|---|---|"]
+             "describe the kernels themselves, not the step's overlap.  Clock = GRBM_GUI_ACTIVE / 8 XCDs "
+             "over the dispatches' own durations (their timestamps): the clock the chip sustained while "
+             "they ran.  TFLOP/s = the issued flops over those durations; the last column divides it by "
+             "the bf16 peak at that clock (2.5 PFLOP/s x clock / 2.4 GHz).  The GRBM window of a dispatch "
+             "includes some time around it, so for dispatches of tens of microseconds the clock reads above "
+             "the part's 2.4 GHz maximum: the column means something for the long dispatches only.", "",
+             "| kernel group | dispatches | MFMA busy | TFLOP issued (all dispatches) | clock GHz | TFLOP/s | "
+             "frac of 2.5 PFLOP/s | frac of the peak at that clock |",
+             "|---|---|---|---|---|---|---|---|"]
     for _, label in _MFMA_GROUPS:
         if label not in per:
             continue
@@ -256,9 +263,11 @@ def mfma(args):
         cyc = sum(d.get("SQ_BUSY_CYCLES", 0) for d in ds) / 32.0
         mops = sum(d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) for d in ds)
         tf = mops * 512 / 1e12
-        secs = cyc / (args.clock_ghz * 1e9)
-        lines.append(f"| {label} | {len(per[label])} | {busy / max(1024 * cyc, 1):.3f} | {tf:.2f} | "
-                     f"{tf / max(secs, 1e-12):.0f} (at {args.clock_ghz} GHz) |")
+        secs = sum(d.get("ns", 0) for d in ds) * 1e-9
+        ghz = sum(d.get("GRBM_GUI_ACTIVE", 0) for d in ds) / 8.0 / max(secs, 1e-12) / 1e9
+        rate = tf / max(secs, 1e-12)
+        lines.append(f"| {label} | {len(per[label])} | {busy / max(1024 * cyc, 1):.3f} | {tf:.2f} | {ghz:.2f} | "
+                     f"{rate:.0f} | {rate / 2500:.3f} | {rate / (2500 * ghz / 2.4):.3f} |")
     with open(args.out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -341,7 +350,6 @@ def main():
     m.add_argument("--csv", required=True)
     m.add_argument("--out", required=True)
     m.add_argument("--title", default="MFMA counters")
-    m.add_argument("--clock-ghz", type=float, default=2.4)
     m.add_argument("--command", action="append")
     w = sub.add_parser("sweep-table")
     w.add_argument("--jsonl", required=True)
