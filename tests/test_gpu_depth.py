@@ -18,9 +18,12 @@ end-to-end error logged: it is the recorded drift, not a gate.
 
 Cases: LLaVA-1.5-7B keep 128 (every layer of 32, its random per-layer mask),
 LLaVA-NeXT five tiles with Algorithm 1's admission (every layer of 32),
-LLaVA-1.5-13B batch 8 (six of 40 layers incl. the first and last), and the
+LLaVA-1.5-13B batch 8 (six of 40 layers incl. the first and last), the
 stress shape at its real size (4 x 2944 rows, keep-all, per-row codes, the
-first two layers).
+first two layers), and the benchmark's default step (the stress shape at keep
+288 per tile, 6014 rows, a random per-layer mask with p = 0.25: every third
+layer and the last, through the same selection and kernels the benchmark
+times).
 """
 import numpy as np
 import pytest
@@ -34,11 +37,12 @@ from gpu_common import need_gpu, log
 BAR = 2e-2
 
 CASES = {
-    # name: (workload, keep, layers checked (None = all), per-row codes)
-    "llava15_7b_keep128": ("llava15_7b", None, None, False),
-    "llava_next_7b_adaptive": ("llava_next_7b", None, None, False),
-    "llava15_13b_batch8": ("llava15_13b", None, (0, 7, 15, 23, 31, 39), False),
-    "stress_keep_all_11776_rows": ("stress", 576, (0, 1), True),
+    # name: (workload, keep, layers checked (None = all), per-row codes, skip p (None = the workload's))
+    "llava15_7b_keep128": ("llava15_7b", None, None, False, None),
+    "llava_next_7b_adaptive": ("llava_next_7b", None, None, False, None),
+    "llava15_13b_batch8": ("llava15_13b", None, (0, 7, 15, 23, 31, 39), False, None),
+    "stress_keep_all_11776_rows": ("stress", 576, (0, 1), True, None),
+    "stress_keep288_skip0.25_6014_rows": ("stress", 288, tuple(range(0, 32, 3)) + (31,), False, 0.25),
 }
 
 
@@ -60,9 +64,9 @@ def _per_row_codes(L, cu, n_text, seed, p_attn=0.25, p_ffn=0.25):
 @pytest.mark.parametrize("case", list(CASES))
 def test_layer_by_layer(case):
     L = need_gpu()
-    name, keep, layers, per_row = CASES[case]
+    name, keep, layers, per_row, skip_p = CASES[case]
     log(f"[depth] {case}")
-    g = gpu_pipeline(name, keep=keep)
+    g = gpu_pipeline(name, keep=keep, skip_p=skip_p)
     o = oracle_plan(g)
     eq = selection_equal(g, o)
     assert eq["idx_equal"] and eq["cu_equal"], eq
