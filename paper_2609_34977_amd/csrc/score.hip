@@ -10,10 +10,11 @@
 //   anchor_topk    grid G x 1024: LDS bitonic sort of 64-bit keys
 //                  (~order(a), i); the first n_anchor are the anchors; block
 //                  scans write the ascending anchor and non-anchor lists.
-//   anchor_maxsim  grid (ceil(n/32), G) x 256: m_i = max_p u_i . u_p.  bf16
-//                  features use v_mfma_f32_32x32x16_bf16 on the raw rows
-//                  (exact products, fp32 accumulation) scaled by the two
-//                  inverse norms; fp32 features use a wave-per-row FMA loop.
+//   anchor_maxsim  m_i = max_p u_i . u_p.  bf16: grid (ceil(n/128), G) x 256,
+//                  v_mfma_f32_32x32x16_bf16 on the raw rows (exact products,
+//                  fp32 accumulation; anchors staged in LDS per 64-dimension
+//                  chunk) scaled by the two inverse norms; fp32: grid
+//                  (ceil(n/4), G), a wave-per-row FMA loop.
 //   kmeans         grid G x (512|256): Lloyd passes; each wave keeps every
 //                  centroid's slice of dimensions in registers, processes
 //                  rows round-robin, and the per-wave partial sums are
@@ -310,66 +311,110 @@ __global__ void __launch_bounds__(1024) anchor_topk_kernel(int n, int n_anchor,
 }
 
 // ------------------------------------------------------------- anchor_maxsim
-// bf16: per block 32 data rows; the 4 waves split the anchor tiles of 32.
+// m_i = max_p u_i . u_p over the anchors p of the tile (bf16 features):
+// one block per 128 rows, one 32-row tile per wave (B operand: lane % 32 owns
+// a row and its output), the anchors in tiles of 32 (A operand), up to 8 tiles
+// per pass over the rows.  The anchors go through LDS one 64-dimension chunk
+// at a time (double buffered; 16-byte chunk q of anchor a at slot
+// q ^ ((a >> 1) & 7), so a 16-lane read of 16 anchors hits distinct banks)
+// and serve all four waves; each wave reads its own rows once, the next
+// chunk's loads in flight while the current chunk's MFMAs run.  A lane
+// covers k in [k0 + 32 hi, k0 + 32 hi + 32) as 4 chunks of 8 for both
+// operands (v_mfma_f32_32x32x16_bf16, exact products, fp32 accumulation in
+// chunk order), then acc * nu_row * nu_anchor, maxed.
+constexpr int kMaxAnchorTiles = 8;
+
 __global__ void __launch_bounds__(256) anchor_maxsim_bf16_kernel(
     int n, int d, int n_anchor, FeatArgs fa, int last, const float* __restrict__ nu_last,
     int64_t nu_stride_g, const int32_t* __restrict__ anc_list, float* __restrict__ mvec) {
-  __shared__ float red[4][32];
+  __shared__ __attribute__((aligned(16))) uint8_t abuf[2][kMaxAnchorTiles * 32 * 128];
   const int g = blockIdx.y;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int r0 = blockIdx.x * 32;
-  const int hi = lane >> 5, lo = lane & 31;
-  const int my_row = r0 + lo;  // data row owned by this lane (B operand / output column)
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, hi = lane >> 5, lo = lane & 31;
+  const int my_row = blockIdx.x * 128 + 32 * wave + lo;
   const bool row_ok = my_row < n;
-  const uint16_t* rowp =
-      reinterpret_cast<const uint16_t*>(feat_row<uint16_t>(fa, last, g, row_ok ? my_row : 0));
+  const uint16_t* rowp = feat_row<uint16_t>(fa, last, g, row_ok ? my_row : 0);
   const float* nu_g = nu_last + (int64_t)g * nu_stride_g;
+  const int32_t* anc = anc_list + (int64_t)g * n;
+  const float nu_r = row_ok ? nu_g[my_row] : 0.f;
   float best = -INFINITY;
   const int n_at = (n_anchor + 31) / 32;
-  for (int at = wave; at < n_at; at += 4) {
-    const int p_idx = at * 32 + lo;  // anchor owned by this lane for the A operand
-    const bool anc_ok = p_idx < n_anchor;
-    const int prow = anc_ok ? anc_list[(int64_t)g * n + p_idx] : 0;
-    const uint16_t* ap = feat_row<uint16_t>(fa, last, g, prow);
-    floatx16 acc = {};
-    for (int k0 = 0; k0 < d; k0 += 64) {
-      // this lane covers k in [k0 + 32*hi, k0 + 32*hi + 32) as 4 chunks of 8;
-      // A (anchors) and B (rows) use the same k permutation.
-      bf16x8 av[4], bv[4];
+  const int nkc = (d + 63) / 64;
+  // staging: thread (anchor a = tid / 8 + 32 j of the pass, chunk q = tid % 8)
+  const int sq = tid & 7, sa0 = tid >> 3;
+  for (int t0 = 0; t0 < n_at; t0 += kMaxAnchorTiles) {
+    const int nt = min(kMaxAnchorTiles, n_at - t0);
+    const uint16_t* sp[kMaxAnchorTiles];
+#pragma unroll
+    for (int j = 0; j < kMaxAnchorTiles; ++j) {
+      const int p = 32 * (t0 + j) + sa0;
+      sp[j] = (j < nt && p < n_anchor) ? feat_row<uint16_t>(fa, last, g, anc[p]) : nullptr;
+    }
+    u32x4 ast[kMaxAnchorTiles], bv[4], bn[4];
+    auto load_anchors = [&](int k0) {
+      const int kk = k0 + 8 * sq;
+#pragma unroll
+      for (int j = 0; j < kMaxAnchorTiles; ++j)
+        ast[j] = (sp[j] && kk + 8 <= d) ? *reinterpret_cast<const u32x4*>(sp[j] + kk) : u32x4{0, 0, 0, 0};
+    };
+    auto store_anchors = [&](int buf) {
+#pragma unroll
+      for (int j = 0; j < kMaxAnchorTiles; ++j)
+        if (j < nt) {
+          const int a = sa0 + 32 * j;
+          *reinterpret_cast<u32x4*>(&abuf[buf][a * 128 + 16 * (sq ^ ((a >> 1) & 7))]) = ast[j];
+        }
+    };
+    auto load_rows = [&](int k0, u32x4* dst) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const int kk = k0 + 32 * hi + 8 * c;
-        uint4 ua = make_uint4(0, 0, 0, 0), ub = make_uint4(0, 0, 0, 0);
-        if (kk + 8 <= d) {
-          if (anc_ok) ua = *reinterpret_cast<const uint4*>(ap + kk);
-          if (row_ok) ub = *reinterpret_cast<const uint4*>(rowp + kk);
+        dst[c] = (row_ok && kk + 8 <= d) ? *reinterpret_cast<const u32x4*>(rowp + kk) : u32x4{0, 0, 0, 0};
+      }
+    };
+    floatx16 acc[kMaxAnchorTiles];
+#pragma unroll
+    for (int j = 0; j < kMaxAnchorTiles; ++j) acc[j] = floatx16{};
+    load_anchors(0);
+    load_rows(0, bv);
+    store_anchors(0);
+    __syncthreads();
+    for (int kc = 0; kc < nkc; ++kc) {
+      const bool more = kc + 1 < nkc;
+      if (more) {
+        load_anchors(64 * (kc + 1));
+        load_rows(64 * (kc + 1), bn);
+      }
+      const uint8_t* ab = abuf[kc & 1];
+#pragma unroll
+      for (int j = 0; j < kMaxAnchorTiles; ++j)
+        if (j < nt) {
+          const int a = 32 * j + lo;
+          bf16x8 av[4];
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            av[c] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ab + a * 128 + 16 * ((4 * hi + c) ^ ((a >> 1) & 7))));
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[c], __builtin_bit_cast(bf16x8, bv[c]), acc[j], 0, 0, 0);
         }
-        av[c] = __builtin_bit_cast(bf16x8, ua);
-        bv[c] = __builtin_bit_cast(bf16x8, ub);
-      }
+      if (more) store_anchors((kc + 1) & 1);  // that buffer was last read before the previous barrier
+      __syncthreads();
 #pragma unroll
-      for (int c = 0; c < 4; ++c) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[c], bv[c], acc, 0, 0, 0);
+      for (int c = 0; c < 4; ++c) bv[c] = bn[c];
     }
-    // acc[r]: anchor 8*(r/4) + 4*hi + r%4 of this tile, data row = lo
-    const float nu_r = row_ok ? nu_g[my_row] : 0.f;
+    // acc[j][r]: anchor 32 (t0 + j) + 8 (r / 4) + 4 hi + r % 4, data row my_row
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int pa = at * 32 + 8 * (r >> 2) + 4 * hi + (r & 3);
-      if (pa < n_anchor) {
-        const float nu_p = nu_g[anc_list[(int64_t)g * n + pa]];
-        best = fmaxf(best, acc[r] * nu_r * nu_p);
+    for (int j = 0; j < kMaxAnchorTiles; ++j)
+      if (j < nt) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int pa = 32 * (t0 + j) + 8 * (r >> 2) + 4 * hi + (r & 3);
+          if (pa < n_anchor) best = fmaxf(best, acc[j][r] * nu_r * nu_g[anc[pa]]);
+        }
       }
-    }
   }
   best = fmaxf(best, __shfl_xor(best, 32, 64));
-  if (hi == 0) red[wave][lo] = best;
-  __syncthreads();
-  if (threadIdx.x < 32) {
-    float b = red[0][threadIdx.x];
-    for (int w = 1; w < 4; ++w) b = fmaxf(b, red[w][threadIdx.x]);
-    const int row = r0 + threadIdx.x;
-    if (row < n) mvec[(int64_t)g * n + row] = n_anchor > 0 ? b : 0.f;
-  }
+  if (hi == 0 && row_ok) mvec[(int64_t)g * n + my_row] = n_anchor > 0 ? best : 0.f;
 }
 
 // fp32 features: one wave per data row, loop over anchors.
@@ -957,7 +1002,7 @@ extern "C" spider_status spider_score(int G, int n, int H, int d_v, int n_layers
     const float* nu_last = ws.nu + (size_t)last * n;
     const int64_t nu_stride = (int64_t)n_layers * n;
     if (feat_dtype == SPIDER_BF16)
-      anchor_maxsim_bf16_kernel<<<dim3(ceil_div(n, 32), G), 256, 0, st>>>(
+      anchor_maxsim_bf16_kernel<<<dim3(ceil_div(n, 128), G), 256, 0, st>>>(
           n, d_v, n_anchor, fa, last, nu_last, nu_stride, ws.anc, ws.mvec);
     else
       anchor_maxsim_f32_kernel<<<dim3(ceil_div(n, 4), G), 256, 0, st>>>(
