@@ -763,10 +763,10 @@ __global__ void __launch_bounds__(256) cluster_mean_kernel(int d, int K, int n_l
   }
 }
 
-// One wave per non-anchor row: s = sum_l nu_l * (F^l_i . mu^l_c) + m_i + mbar_c.
+// One wave per non-anchor row (fallback where the cluster means do not fit in LDS): s = sum_l nu_l * (F^l_i . mu^l_c) + m_i + mbar_c.
 template <typename FT, int VPL>
-__global__ void __launch_bounds__(256) score_rows_kernel(int n, int d, int n_anchor, int K,
-                                                         int n_layers, FeatArgs fa,
+__global__ void __launch_bounds__(256) score_rows_wave_kernel(int n, int d, int n_anchor, int K,
+                                                              int n_layers, FeatArgs fa,
                                                          const float* __restrict__ nu,
                                                          const int32_t* __restrict__ rest_list,
                                                          const float* __restrict__ mvec, ClusterWs cw,
@@ -796,6 +796,97 @@ __global__ void __launch_bounds__(256) score_rows_kernel(int n, int d, int n_anc
     s += dot * nu[((int64_t)g * n_layers + l) * n + i];
   }
   if (lane == 0) s_out[(int64_t)g * n + i] = s + mvec[(int64_t)g * n + i] + cw.mbar[(int64_t)g * K + k];
+}
+
+// The same scores, 64 rows per block and 16 per wave in batches of RB rows
+// whose feature loads (two tapped layers at a time) are all issued before
+// any is used; the tile's cluster means mu[l][k] (n_layers * K * d floats, at
+// most kMuLdsFloats) are staged in LDS once per block.  Per row and layer a
+// lane adds its dimensions in ascending order, then the wave sum, then
+// s += dot * nu_l in layer order: the arithmetic of score_rows_wave_kernel in
+// the same order, so the same bits.
+constexpr int kScoreRowsPerBlock = 64;
+constexpr int kMuLdsFloats = 8192;
+
+template <typename FT, int VPL>
+__global__ void __launch_bounds__(256) score_rows_kernel(int n, int d, int n_anchor, int K, int n_layers,
+                                                         FeatArgs fa, const float* __restrict__ nu,
+                                                         const int32_t* __restrict__ rest_list,
+                                                         const float* __restrict__ mvec, ClusterWs cw,
+                                                         float* __restrict__ s_out, float* __restrict__ m_out) {
+  __shared__ __attribute__((aligned(16))) float smu[kMuLdsFloats];
+  const int g = blockIdx.y;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m = n - n_anchor;
+  if (m_out && blockIdx.x == 0)
+    for (int i = threadIdx.x; i < n; i += blockDim.x) m_out[(int64_t)g * n + i] = mvec[(int64_t)g * n + i];
+  if (m <= 0) return;
+  const int lkd = n_layers * K * d;  // a multiple of 8 (d is)
+  const float* mug = cw.mu + (int64_t)g * lkd;
+  for (int t = threadIdx.x * 4; t < lkd; t += 1024)
+    *reinterpret_cast<float4*>(smu + t) = *reinterpret_cast<const float4*>(mug + t);
+  __syncthreads();
+  constexpr int RB = Feat<FT>::kPrepRowBatch;
+  constexpr int NCH = VPL / 8;
+  const int32_t* U = rest_list + (int64_t)g * n;
+  const int32_t* asg = cw.assign + (int64_t)g * n;
+  const int jw = blockIdx.x * kScoreRowsPerBlock + 16 * wave;
+  for (int jb = 0; jb < 16; jb += RB) {
+    if (jw + jb >= m) break;
+    int ii[RB], kc[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      const int j = min(jw + jb + r, m - 1);
+      ii[r] = U[j];
+      kc[r] = asg[j];
+    }
+    float sacc[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) sacc[r] = 0.f;
+    for (int l0 = 0; l0 < n_layers; l0 += 2) {
+      const bool two = l0 + 1 < n_layers;
+      typename Feat<FT>::Raw x[2][RB][NCH];
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+          const FT* row = feat_row<FT>(fa, q == 0 || !two ? l0 : l0 + 1, g, ii[r]);
+#pragma unroll
+          for (int c = 0; c < NCH; ++c) {
+            const int e0 = lane * 8 + 512 * c;
+            if (e0 < d && (q == 0 || two)) x[q][r][c] = Feat<FT>::load8_raw(row + e0);
+          }
+        }
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        if (q == 1 && !two) break;
+        const int l = l0 + q;
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+          const float* mu = smu + (l * K + kc[r]) * d;
+          float dot = 0.f;
+#pragma unroll
+          for (int c = 0; c < NCH; ++c) {
+            const int e0 = lane * 8 + 512 * c;
+            if (e0 < d) {
+              const float4 m0 = *reinterpret_cast<const float4*>(mu + e0);
+              const float4 m1 = *reinterpret_cast<const float4*>(mu + e0 + 4);
+              const float mv[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+#pragma unroll
+              for (int e = 0; e < 8; ++e) dot = fmaf(Feat<FT>::raw_at(x[q][r][c], e), mv[e], dot);
+            }
+          }
+          dot = wave_sum(dot);
+          sacc[r] += dot * nu[((int64_t)g * n_layers + l) * n + ii[r]];
+        }
+      }
+    }
+    if (lane == 0)
+#pragma unroll
+      for (int r = 0; r < RB; ++r)
+        if (jw + jb + r < m)
+          s_out[(int64_t)g * n + ii[r]] = sacc[r] + mvec[(int64_t)g * n + ii[r]] + cw.mbar[(int64_t)g * K + kc[r]];
+  }
 }
 
 struct ScoreWs {
@@ -894,8 +985,12 @@ hipError_t launch_cluster_kernels(int G, int n, int d, int n_anchor, int K, int 
       e = hipGetLastError();
       if (e != hipSuccess) return e;
     }
-    score_rows_kernel<FT, VPL><<<dim3(std::max(1, ceil_div(m, 4)), G), 256, 0, st>>>(
-        n, d, n_anchor, K, n_layers, fa, ws.nu, ws.rest, ws.mvec, ws.cw, s_out, m_out);
+    if ((int64_t)n_layers * K * d <= kMuLdsFloats)
+      score_rows_kernel<FT, VPL><<<dim3(std::max(1, ceil_div(m, kScoreRowsPerBlock)), G), 256, 0, st>>>(
+          n, d, n_anchor, K, n_layers, fa, ws.nu, ws.rest, ws.mvec, ws.cw, s_out, m_out);
+    else
+      score_rows_wave_kernel<FT, VPL><<<dim3(std::max(1, ceil_div(m, 4)), G), 256, 0, st>>>(
+          n, d, n_anchor, K, n_layers, fa, ws.nu, ws.rest, ws.mvec, ws.cw, s_out, m_out);
     return hipGetLastError();
   }
 }
