@@ -41,6 +41,17 @@ __device__ __forceinline__ float2 lane_pair(float v) {
 typedef float float2v __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 
+// 16-byte-per-lane DMA into LDS like dma16, from a wave-uniform base kept in
+// SGPRs plus a per-lane byte offset: moving the base each key block is two
+// scalar adds instead of 64-bit lane address arithmetic.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16_at(const void* base, uint32_t off, uint32_t lds) {
+  lds = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -119,29 +130,32 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
         vf[c][u][0] = *reinterpret_cast<const uint2*>(base);
         vf[c][u][1] = *reinterpret_cast<const uint2*>(base + 8);
       }
-    // ---- S^T = K Q^T
-    floatx16 s = {};
-#pragma unroll
-    for (int t = 0; t < DH / 16; ++t)
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[t]), qf[t], s, 0, 0, 0);
-    // ---- online softmax (this lane: query lo, keys 8*(r/4) + 4*hi + r%4) on
-    // the raw scores, as in attention_wide_kernel: masks only where some query
-    // cannot see the whole key block, the scale folded into the exponent's
-    // FMA, a lazily moved running max and a vote before any rescale.
-    const bool full = j0 >= st_max && j0 + 31 <= q_min;
-    float mx = -INFINITY;
-    if (full) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
+    // ---- S^T = K Q^T (this lane: query lo, keys 8*(r/4) + 4*hi + r%4).  As in
+    // attention_wide_kernel, keys some query of the block cannot see enter as
+    // -inf through the first MMA's accumulator, only in key blocks that hold
+    // such keys.
+    floatx16 s;
+    if (j0 >= st_max && j0 + 31 <= q_min) {
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[0]), qf[0], floatx16{}, 0, 0, 0);
     } else {
+      floatx16 bias;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = j0 + 8 * (r >> 2) + 4 * hi + (r & 3);
         const bool vis = qok && key >= qstart && key <= qrow;
-        s[r] = vis ? s[r] : -INFINITY;
-        mx = fmaxf(mx, s[r]);
+        bias[r] = vis ? 0.f : -INFINITY;
       }
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[0]), qf[0], bias, 0, 0, 0);
     }
+#pragma unroll
+    for (int t = 1; t < DH / 16; ++t)
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[t]), qf[t], s, 0, 0, 0);
+    // ---- online softmax on the raw scores, as in attention_wide_kernel: the
+    // scale folded into the exponent's FMA, a lazily moved running max and a
+    // vote before any rescale.
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
     {
       const float2 pm = lane_pair(mx);
       mx = fmaxf(pm.x, pm.y);
@@ -332,27 +346,44 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
   const int nblk = (bhi - jb0) / 32 + 1;  // every block holds at least one query
 
   // DMA of the key block at j0 into stage S: K tile rows 4i..4i+3 and V^T rows
-  // 16i..16i+15 for i = 2 wave + e (e = 0, 1); lane l writes 16 bytes at l*16
+  // 16i..16i+15 for i = 2 wave + e (e = 0, 1); lane l writes 16 bytes at l*16.
+  // Each lane's byte offset from the key block's first K row / V^T column is
+  // fixed, so a key block moves two scalar bases (the launcher keeps d * ldvt
+  // below 2^31); only a block reaching past the last row clamps per lane.
   const uint32_t ring_lds = lds_offset(ring);
+  uint32_t koff[2], voff[2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int i = 2 * wave + e;
+    const int row = 4 * i + (lane >> 4);
+    const int sig = (row & ~12) | ((row & 4) << 1) | ((row & 8) >> 1);
+    const int c = (lane & 15) ^ (row & 15);
+    koff[e] = (uint32_t)(sig * a.d + h * DH + 8 * c) * 2u;
+    const int rv = 16 * i + (lane >> 2);
+    const int cv = (lane & 3) ^ ((rv >> 2) & 3);
+    voff[e] = ((uint32_t)(h * DH + rv) * (uint32_t)a.ldvt + 8u * cv) * 2u;
+  }
   auto issue = [&](int j0, auto S) {
     constexpr int st = decltype(S)::value;
     const uint32_t base = ring_lds + st * STAGE;
+    if (j0 + 31 <= a.rows - 1) {
+      const uint16_t* kb = Kp + (int64_t)j0 * a.d;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int i = 2 * wave + e;
-      const int row = 4 * i + (lane >> 4);
-      const int sig = (row & ~12) | ((row & 4) << 1) | ((row & 8) >> 1);
-      const int key = min(j0 + sig, a.rows - 1);
-      const int c = (lane & 15) ^ (row & 15);
-      dma16(Kp + (int64_t)key * a.d + h * DH + 8 * c, base + i * 1024);
-    }
+      for (int e = 0; e < 2; ++e) dma16_at(kb, koff[e], base + (2 * wave + e) * 1024);
+    } else {
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int i = 2 * wave + e;
-      const int row = 16 * i + (lane >> 2);
-      const int c = (lane & 3) ^ ((row >> 2) & 3);
-      dma16(VT + (int64_t)(h * DH + row) * a.ldvt + j0 + 8 * c, base + KT_BYTES + i * 1024);
+      for (int e = 0; e < 2; ++e) {
+        const int i = 2 * wave + e;
+        const int row = 4 * i + (lane >> 4);
+        const int sig = (row & ~12) | ((row & 4) << 1) | ((row & 8) >> 1);
+        const int key = min(j0 + sig, a.rows - 1);
+        const int c = (lane & 15) ^ (row & 15);
+        dma16(Kp + (int64_t)key * a.d + h * DH + 8 * c, base + i * 1024);
+      }
     }
+    const uint16_t* vb = VT + j0;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) dma16_at(vb, voff[e], base + KT_BYTES + (2 * wave + e) * 1024);
   };
 
   const float sc = a.scale * kLog2e;
@@ -384,8 +415,27 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
       kf[k] = __builtin_bit_cast(bf16x8,
                                  *reinterpret_cast<const u32x4*>(kt + lo * 256 + 16 * ((2 * k + hi) ^ (lo & 15))));
     __builtin_amdgcn_sched_barrier(0);
+    // keys some query of the wave cannot see enter as -inf through the first
+    // MMA's accumulator (exactly 0 elsewhere), so the softmax below needs no
+    // masking branch and the scores stay in the MMA's registers
+    const bool full = j0 >= wst_max && j0 + 31 <= wq_min;
 #pragma unroll
-    for (int k = 0; k < DH / 16; ++k)
+    for (int t = 0; t < QT; ++t) {
+      if (full) {
+        s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0], qf[t][0], s[t], 0, 0, 0);
+      } else {
+        floatx16 bias;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = j0 + 16 * (r >> 3) + 8 * hi + (r & 7);
+          const bool vis = qok[t] && key >= qst[t] && key <= qrow[t];
+          bias[r] = vis ? 0.f : -INFINITY;
+        }
+        s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0], qf[t][0], bias, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int k = 1; k < DH / 16; ++k)
 #pragma unroll
       for (int t = 0; t < QT; ++t) s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[k], qf[t][k], s[t], 0, 0, 0);
 #pragma unroll
@@ -397,30 +447,18 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
             bf16x8, *reinterpret_cast<const u32x4*>(vt + row * 64 + 16 * ((2 * u + hi) ^ ((row >> 2) & 3))));
       }
     __builtin_amdgcn_sched_barrier(0);
-    // Online softmax on the raw scores: the scale enters the exponent through
-    // one FMA, exp2 is the hardware instruction, keys are masked only in key
-    // blocks some query of the wave cannot fully see.  The running max moves
-    // only when the block's max exceeds it by more than kLazyLog2 in the
-    // exponent (weights then stay below 2^kLazyLog2), so the accumulators are
-    // rescaled a few times per query instead of at almost every key block;
+    // Online softmax on the raw (already masked) scores: the scale enters the
+    // exponent through one FMA, exp2 is the hardware instruction.  The running
+    // max moves only when the block's max exceeds it by more than kLazyLog2 in
+    // the exponent (weights then stay below 2^kLazyLog2), so the accumulators
+    // are rescaled a few times per query instead of at almost every key block;
     // a rescale runs when some lane's max moved (wave vote).
-    const bool full = j0 >= wst_max && j0 + 31 <= wq_min;
     bf16x8 pf[QT][2][2];
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
       float mx = -INFINITY;
-      if (full) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][r]);
-      } else {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = j0 + 16 * (r >> 3) + 8 * hi + (r & 7);
-          const bool vis = qok[t] && key >= qst[t] && key <= qrow[t];
-          s[t][r] = vis ? s[t][r] : -INFINITY;
-          mx = fmaxf(mx, s[t][r]);
-        }
-      }
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][r]);
       {
         const float2 pm = lane_pair(mx);
         mx = fmaxf(pm.x, pm.y);
@@ -574,7 +612,8 @@ hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t st) {
   if (a.nq == 0) return hipSuccess;
   if (a.dh != 128 || a.ldvt < ((a.rows + 31) / 32) * 32 || a.ldvt % 32) return hipErrorInvalidValue;
   // a device query count is honoured by the per-32-query kernel only
-  const bool wide = (int64_t)ceil_div(a.nq, 128) * a.H >= 128;
+  // (the shared-tile kernel's per-lane DMA offsets are 32-bit byte offsets)
+  const bool wide = (int64_t)ceil_div(a.nq, 128) * a.H >= 128 && (int64_t)a.d * a.ldvt < (int64_t(1) << 31);
   if (wide && a.nq_dev) return hipErrorInvalidValue;
   // At least 128 blocks of 128 queries: the shared-tile kernel (one query tile
   // per wave: two waves per SIMD overlap one's softmax with the other's MMAs;
