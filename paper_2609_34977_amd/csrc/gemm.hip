@@ -748,7 +748,7 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
         if (decltype(FULL)::value || i < live) {
 #pragma unroll
           for (int u = 0; u < 4; ++u)
-            acc[i][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[q & 1][i], wf[q & 1][u], acc[i][u], 0, 0, 0);
+            acc[i][u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[q & 1][u], af[q & 1][i], acc[i][u], 0, 0, 0);
         }
         constexpr int a0 = p0 + i * (p1 - p0) / MH, a1 = p0 + (i + 1) * (p1 - p0) / MH;
         static_for<a0, a1>([&](auto P) { issue_piece(kd, SD, P); });
@@ -795,8 +795,13 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
     dma_wait_all();
   }
 
-  // D layout of the 32x32 MMA: column lane % 32, row 8 (r / 4) + 4 (lane / 32) + r % 4
-  auto acc_row = [&](int i, int r) { return 32 * (MH * mh + i) + 8 * (r >> 2) + 4 * hi + (r & 3); };
+  // The MMA takes the weight fragment as A and the activation fragment as B,
+  // so its D layout puts one activation row in each lane (row lane % 32 of the
+  // 32-row tile) and, in registers 4g..4g+3, the four consecutive output
+  // columns 8 g + 4 (lane / 32) + [0, 4) of the 32-column tile: every lane
+  // writes 16-byte (fp32) or 8-byte (bf16) row pieces.
+  const int lrow = 32 * MH * mh + lo;  // tile row of acc[0][*]; acc[i][*] is 32 i further
+  auto quad = [&](const floatx16& v, int g) { return floatx4{v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]}; };
   if constexpr (DUAL) {
     if (tail) {
       // fp32 partial sums of piece s: scratch[s][tail tile][BM][256], gate
@@ -804,14 +809,17 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
       float* sp = reinterpret_cast<float*>(a.scratch) +
                   ((int64_t)s * a.tail_tiles + (local - a.total_tiles)) * BM * 256;
 #pragma unroll
-      for (int i = 0; i < MH; ++i)
+      for (int i = 0; i < MH; ++i) {
+        const int row = lrow + 32 * i;
+        if (m0 + row < M) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+          for (int u = 0; u < 4; ++u)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = acc_row(i, r);
-            if (m0 + row < M) sp[row * 256 + (u >> 1) * 128 + 64 * nh + 32 * (u & 1) + lo] = acc[i][u][r];
-          }
+            for (int g = 0; g < 4; ++g)
+              *reinterpret_cast<floatx4*>(sp + row * 256 + (u >> 1) * 128 + 64 * nh + 32 * (u & 1) + 8 * g + 4 * hi) =
+                  quad(acc[i][u], g);
+        }
+      }
       return;
     }
     // bf16 silu(g) * u staged as a BM x 128 tile, written as 16-byte row pieces
@@ -822,9 +830,17 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          ot[acc_row(i, r) * OPITCH + 64 * nh + 32 * u + lo] =
-              f32_to_bf16_bits(silu(acc[i][u][r]) * acc[i][u + 2][r]);
+        for (int g = 0; g < 4; ++g) {
+          uint32_t w[2];
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const int r = 4 * g + 2 * e;
+            w[e] = (uint32_t)f32_to_bf16_bits(silu(acc[i][u][r]) * acc[i][u + 2][r]) |
+                   ((uint32_t)f32_to_bf16_bits(silu(acc[i][u][r + 1]) * acc[i][u + 2][r + 1]) << 16);
+          }
+          *reinterpret_cast<uint2*>(ot + (lrow + 32 * i) * OPITCH + 64 * nh + 32 * u + 8 * g + 4 * hi) =
+              make_uint2(w[0], w[1]);
+        }
     __syncthreads();
     const int rows = min(BM, M - m0);
     uint16_t* op = reinterpret_cast<uint16_t*>(G.out) + (int64_t)m0 * G.ldo + n0;
@@ -860,12 +876,13 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < MH; ++i) {
         if (i < live) {
+          const uint8_t* cs = ring + (lrow + 32 * i) * 512;
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int row = 32 * (MH * mh + i) + 8 * (r >> 2) + 4 * hi + (r & 3);
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
-              const float2 c = *reinterpret_cast<const float2*>(ring + row * 512 + (32 * u + lo) * 8);
+              const int col = 32 * u + 8 * (r >> 2) + 4 * hi + (r & 3);
+              const float2 c = *reinterpret_cast<const float2*>(cs + col * 8);
               const float2 y = rope_rotate(acc[i][u][r], acc[i][u + 2][r], c.x, c.y);
               acc[i][u][r] = y.x;
               acc[i][u + 2][r] = y.y;
@@ -888,12 +905,19 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = 8 * (r >> 2) + 4 * hi + (r & 3);
-            if (kind == 1)
-              sw[row * QP + 32 * u + lo] = f32_to_bf16_bits(acc[i][u][r]);
-            else
-              sw[(32 * u + lo) * VP + row] = f32_to_bf16_bits(rb + row < M ? acc[i][u][r] : 0.f);
+          for (int g = 0; g < 4; ++g) {
+            const int col = 32 * u + 8 * g + 4 * hi;
+            if (kind == 1) {
+              *reinterpret_cast<uint2*>(sw + lo * QP + col) =
+                  make_uint2((uint32_t)f32_to_bf16_bits(acc[i][u][4 * g]) |
+                                 ((uint32_t)f32_to_bf16_bits(acc[i][u][4 * g + 1]) << 16),
+                             (uint32_t)f32_to_bf16_bits(acc[i][u][4 * g + 2]) |
+                                 ((uint32_t)f32_to_bf16_bits(acc[i][u][4 * g + 3]) << 16));
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                sw[(col + e) * VP + lo] = f32_to_bf16_bits(rb + lo < M ? acc[i][u][4 * g + e] : 0.f);
+            }
           }
       }
       __syncthreads();
@@ -918,17 +942,19 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmArgs a) {
       }
     }
   } else {
-    // fp32 partial sums: each store instruction writes two whole 128-byte row segments
+    // fp32 partial sums as 16-byte row pieces
     float* op = reinterpret_cast<float*>(G.out) + s * G.sstride;
 #pragma unroll
-    for (int i = 0; i < MH; ++i)
+    for (int i = 0; i < MH; ++i) {
+      const int m = m0 + lrow + 32 * i;
+      if (m < M) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = m0 + acc_row(i, r);
-          if (m < M) op[(int64_t)m * G.ldo + n0 + wrow(u) + lo] = acc[i][u][r];
-        }
+          for (int g = 0; g < 4; ++g)
+            *reinterpret_cast<floatx4*>(op + (int64_t)m * G.ldo + n0 + wrow(u) + 8 * g + 4 * hi) = quad(acc[i][u], g);
+      }
+    }
   }
 }
 
