@@ -70,6 +70,10 @@ PARITY = {
     "7b_704_rows_layer_mask": ("llava_next_7b", 2, [0, 704], 64, 0.5, 0.5, False),
     "7b_256_rows": ("llava15_7b", 1, [0, 256], 64, 0.3, 0.3, True),
     "7b_97_rows_dense": ("llava15_7b", 1, [0, 97], 64, 0.0, 0.0, False),
+    # 257..384 rows (just past the streaming kernel's bound): 128-row tiles of the
+    # large-row GEMM with split tail tiles in the SwiGLU launch
+    "7b_300_rows_every_ffn": ("llava15_7b", 1, [0, 300], 64, 0.3, 0.0, True),
+    "7b_two_samples_384_rows_dense": ("llava15_7b", 1, [0, 190, 384], 64, 0.0, 0.0, False),
     "13b_two_samples": ("llava15_13b", 1, [0, 256, 512], 128, 0.4, 0.2, True),
     # three ragged samples (the middle one text only) with a third of the visual
     # rows bypassing attention: query blocks of the shared-tile attention kernel
