@@ -126,3 +126,32 @@ def test_score_zero_norm_rows():
     # a row that is zero in the last layer has no similarity to any anchor
     for i in (3, 40, 41, 200, 575):
         assert m[i] == 0.0 and o["mvec"][i] == 0.0
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("variant", ["last_layer_only", "three_tapped_layers"])
+def test_score_tapped_layer_variants(variant):
+    """Eq. 3 over other sets of tapped layers (the layer ablations of Tab. 7): the last
+    layer alone, and three layers (the middle one, a second middle-layer stand-in, the
+    last).  Clustering always runs on the last entry; the oracle sums the same layers."""
+    L = need_gpu()
+    w = get_workload("llava15_7b", keep=128)
+    attn, feats = vision_inputs(w.score, 21)
+    fm, fl = feats[0], feats[-1]
+    layers = [fl] if variant == "last_layer_only" else [fm, fm.roll(1, dims=-1).contiguous(), fl]
+    n_anchor = (128 * 7) // 10
+    log(f"[score] {variant}: {len(layers)} tapped layer(s)")
+    out = L.score(attn.cuda(), [f.cuda() for f in layers], n_anchor, 4, w.score.kmeans_iter)
+    torch.cuda.synchronize()
+    o = oracle_tiles(attn, layers, 128, 7, 10, 4, w.score.kmeans_iter)[0]
+    cl = out["cluster"].cpu().numpy()[0]
+    s = out["s"].cpu().numpy()[0]
+    m = out["m"].cpu().numpy()[0]
+    assert np.array_equal(out["a"].cpu().numpy()[0], o["a"])
+    assert set(np.nonzero(cl < 0)[0]) == set(o["anchors"])
+    assert o["margin"].min() > 1e-4, "input too close to a K-means tie for an exact check"
+    assert np.array_equal(cl, o["cluster"])
+    na = o["cluster"] >= 0
+    err = np.abs(s[na] - o["s"][na]) / np.maximum(1.0, np.abs(o["s"][na]))
+    assert err.max() <= 1e-5, f"s error {err.max()}"
+    assert np.max(np.abs(m - o["mvec"]) / np.maximum(1.0, np.abs(o["mvec"]))) <= 1e-5
