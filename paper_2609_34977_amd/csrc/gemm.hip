@@ -1256,6 +1256,10 @@ bool tile_path_fits(const GemmArgs& a, bool dual) {
     const GemmGroup& g = a.g[i];
     if (g.N % (dual ? 128 : 256)) return false;
     if (dual && (reinterpret_cast<uintptr_t>(g.out) % 16 || g.ldo % 8)) return false;
+    // fp32 partial sums leave as 16-byte row pieces
+    if (!dual && a.epilogue != EPI_QKV_BF16 &&
+        (reinterpret_cast<uintptr_t>(g.out) % 16 || g.ldo % 4 || g.split_stride % 4))
+      return false;
   }
   return true;
 }
