@@ -953,6 +953,7 @@ struct PrefillRun {
   int R, max_s;
   hipStream_t st;
   int pend_split = 0;
+  int64_t pend_stride = 0;  // elements between the pending partial slabs
   const int32_t* pend_slot = nullptr;
   // optional KV cache output ([L][B][cap][d]) and the sample of every row
   AT* ck = nullptr;
@@ -964,6 +965,15 @@ struct PrefillRun {
   int64_t pstride() const { return (int64_t)R * c.d; }
 
   int split_cap(int cap) const { return std::min(split_max_for_rows(R), cap); }
+  // Split-K cap of a residual launch (O, down) over `rows` rows whose partial
+  // slabs are packed at rows * d: the residual buffer holds
+  // split_max_for_rows(R) * R rows of partials, so a layer with few active
+  // rows (e.g. only the text rows) may split as far as the streaming kernel
+  // wants even when R is large.
+  int split_cap_rows(int cap, int rows) const {
+    const int64_t slots = (int64_t)split_max_for_rows(R) * R;
+    return (int)std::max<int64_t>(1, std::min<int64_t>(std::min(cap, 8), slots / std::max(1, rows)));
+  }
   hipError_t gemm(GemmArgs& ga, int cap) {
     const int sm = split_cap(cap);
     return bf16() ? launch_gemm_bf16(ga, sm, st) : launch_gemm_f32(ga, sm, st);
@@ -991,7 +1001,7 @@ struct PrefillRun {
   spider_status flush() {
     if (pend_split == 0) return SPIDER_OK;
     ProfScope ps(KC_RESIDUAL, st);
-    launch_norm<AT>(R, h, c.d, ws.Pres, pend_split, pstride(), pend_slot, nullptr, 0.f, nullptr, 0,
+    launch_norm<AT>(R, h, c.d, ws.Pres, pend_split, pend_stride, pend_slot, nullptr, 0.f, nullptr, 0,
                     static_cast<AT*>(nullptr), st);
     SPIDER_LAUNCHED("residual_add");
     pend_split = 0;
@@ -1018,7 +1028,7 @@ struct PrefillRun {
     if (T.nA > 0 || ck) {
       {
         ProfScope ps(KC_RMSNORM, st);
-        launch_norm<AT>(R, h, d, ws.Pres, pend_split, ps_, pend_slot, w.attn_norm, c.eps, nullptr, 1,
+        launch_norm<AT>(R, h, d, ws.Pres, pend_split, pend_stride, pend_slot, w.attn_norm, c.eps, nullptr, 1,
                         xn, st);
         SPIDER_LAUNCHED("rmsnorm(attn)");
         pend_split = 0;
@@ -1091,20 +1101,22 @@ struct PrefillRun {
       go.K = d;
       go.lda = d;
       go.epilogue = EPI_PARTIAL_F32;
-      go.g[0] = GemmGroup{ob, nullptr, T.nA, w.wo, nullptr, d, ws.Pres, d, ps_, 0, 0, 0};
+      go.g[0] = GemmGroup{ob, nullptr, T.nA, w.wo, nullptr, d, ws.Pres, d, (int64_t)T.nA * d, 0, 0, 0};
       go.g[0].m_dev = cntA;
       {
         ProfScope ps(KC_GEMM_O, st);
-        hipError_t e = gemm(go, 8);
+        hipError_t e = bf16() ? launch_gemm_bf16(go, split_cap_rows(8, T.nA), st)
+                              : launch_gemm_f32(go, split_cap_rows(8, T.nA), st);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_o: %s", hipGetErrorString(e));
       }
       pend_split = go.split;
+      pend_stride = go.g[0].split_stride;
       pend_slot = tab + T.offSlotA;
     }
     if (T.nF > 0) {
       {
         ProfScope ps(KC_RMSNORM, st);
-        launch_norm<AT>(R, h, d, ws.Pres, pend_split, ps_, pend_slot, w.ffn_norm, c.eps,
+        launch_norm<AT>(R, h, d, ws.Pres, pend_split, pend_stride, pend_slot, w.ffn_norm, c.eps,
                         tab + T.offSlotF, 0, xn, st);
         SPIDER_LAUNCHED("rmsnorm(ffn)");
         pend_split = 0;
@@ -1131,14 +1143,16 @@ struct PrefillRun {
       gd.K = c.d_ff;
       gd.lda = c.d_ff;
       gd.epilogue = EPI_PARTIAL_F32;
-      gd.g[0] = GemmGroup{act, nullptr, T.nF, w.wd, nullptr, d, ws.Pres, d, ps_, 0, 0, 0};
+      gd.g[0] = GemmGroup{act, nullptr, T.nF, w.wd, nullptr, d, ws.Pres, d, (int64_t)T.nF * d, 0, 0, 0};
       gd.g[0].m_dev = cntF;
       {
         ProfScope ps(KC_GEMM_DOWN, st);
-        hipError_t e = gemm(gd, 8);
+        hipError_t e = bf16() ? launch_gemm_bf16(gd, split_cap_rows(8, T.nF), st)
+                              : launch_gemm_f32(gd, split_cap_rows(8, T.nF), st);
         SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "gemm_down: %s", hipGetErrorString(e));
       }
       pend_split = gd.split;
+      pend_stride = gd.g[0].split_stride;
       pend_slot = tab + T.offSlotF;
     }
     return SPIDER_OK;
