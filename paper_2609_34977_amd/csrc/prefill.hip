@@ -716,8 +716,33 @@ struct TableBuilder {
   std::vector<int32_t>& tab;
   int base;
   std::map<std::string, std::pair<int, int>> seen[2];
+  // whole code columns already added (hash -> column, its tables): a layer
+  // whose column repeats an earlier one reuses its tables without rebuilding
+  // the per-sub-layer keys (R bytes each)
+  std::multimap<uint64_t, std::pair<const uint8_t*, LayerTables>> cols;
+
+  static uint64_t hash_col(const uint8_t* p, int n) {
+    uint64_t h = 1469598103934665603ull;  // FNV-1a offset basis
+    int i = 0;
+    for (; i + 8 <= n; i += 8) {
+      uint64_t w;
+      std::memcpy(&w, p + i, 8);
+      h = (h ^ w) * 1099511628211ull;
+    }
+    for (; i < n; ++i) h = (h ^ p[i]) * 1099511628211ull;
+    return h;
+  }
 
   LayerTables add(const uint8_t* col, int R) {
+    const uint64_t hc = hash_col(col, R);
+    for (auto [it, end] = cols.equal_range(hc); it != end; ++it)
+      if (std::memcmp(it->second.first, col, (size_t)R) == 0) return it->second.second;
+    const LayerTables t = add_new(col, R);
+    cols.emplace(hc, std::make_pair(col, t));
+    return t;
+  }
+
+  LayerTables add_new(const uint8_t* col, int R) {
     LayerTables t;
     for (int which = 0; which < 2; ++which) {
       const uint8_t bit = which == 0 ? 1 : 2;
