@@ -18,10 +18,20 @@ T_skip, the token bypasses sub-layer m(l) from layer l (inclusive) to the
 last layer (Eq. 6, Algorithm 1).  Layer l's forward runs after its
 admissions.  Text rows never skip.
 
+The ablations of the skip rule (Tab. 8), selected by ``variant`` bits (the
+readings are the ones the paper's ablation text gives):
+
+* NO_EII: the retention score is F_itc alone, S_sa = max(0, 1 - F_itc);
+* NO_FITC: the retention score is E_ii alone, S_sa = max(0, 1 - E_ii);
+* NO_ACCUM: no accumulation, S_skip(i, l) = S_fuse(i, l) (each layer's score
+  is tested against T_skip on its own);
+* WHOLE_LAYER (without SLC): S_fuse = w1 * S_sa (no SLC term) and an admitted
+  token bypasses both sub-layers of every remaining layer.
+
 Parity pins: with w1 = 0 the result equals Algorithm 1's plan with the same
 SLC tables followed by the plain prefill; with all decoder weights zero the
 hidden states never change, so the crossing layer follows by hand from the
-closed-form E_ii and F_itc.
+closed-form E_ii and F_itc (for every variant).
 """
 from __future__ import annotations
 
@@ -31,9 +41,11 @@ from .asl_skip import SKIP_ATTN_BIT, SKIP_FFN_BIT, ATTN, entropy_norm, itc, skip
 from .bf16 import round_bf16
 from .decoder import layer_forward
 
+NO_EII, NO_FITC, NO_ACCUM, WHOLE_LAYER = 1, 2, 4, 8
+
 
 def prefill_online(x, weights, cu_seqlens, n_text, W_unembed, slc_sel, m, w1, w2, T_skip, cfg,
-                   recipe="bf16", dtype=np.float64):
+                   recipe="bf16", dtype=np.float64, variant=0):
     """Returns (h [rows, d], codes [L, rows] uint8, admit [rows] int (-1 = never), S_sa [W, rows])."""
     get = weights if callable(weights) else (lambda l: weights[l])
     cu = np.asarray(cu_seqlens, np.int64)
@@ -58,12 +70,18 @@ def prefill_online(x, weights, cu_seqlens, n_text, W_unembed, slc_sel, m, w1, w2
                     continue
                 E = entropy_norm(np.asarray(rnd(h[cand]), np.float64), W_unembed)
                 F = itc(h[cand], h[s0 + n_vis:s1])
-                S = skippability(E, F)
+                S = skippability(np.zeros_like(E) if variant & NO_EII else E,
+                                 np.zeros_like(F) if variant & NO_FITC else F)
+                slc_term = 0.0 if variant & WHOLE_LAYER else float(w2) * float(slc_sel[l])
                 for t, i in enumerate(cand):
                     S_tab[l, i] = S[t]
-                    acc[i] = acc[i] + (float(w1) * float(S[t]) + float(w2) * float(slc_sel[l]))
+                    fuse = float(w1) * float(S[t]) + slc_term
+                    acc[i] = fuse if variant & NO_ACCUM else acc[i] + fuse
                     if acc[i] >= float(T_skip):
                         admit[i] = l
-                        codes[l:, i] |= SKIP_ATTN_BIT if int(m[l]) == ATTN else SKIP_FFN_BIT
+                        if variant & WHOLE_LAYER:
+                            codes[l:, i] |= SKIP_ATTN_BIT | SKIP_FFN_BIT
+                        else:
+                            codes[l:, i] |= SKIP_ATTN_BIT if int(m[l]) == ATTN else SKIP_FFN_BIT
         h = layer_forward(h, get(l), cu, codes[l], cfg, recipe, dtype)
     return h, codes, admit, S_tab

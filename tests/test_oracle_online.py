@@ -96,3 +96,75 @@ def test_constant_states_cross_where_the_closed_form_says():
     assert np.all(codes[:, n_vis:] == 0)
     # the least peaked rows never cross inside the window
     assert admit[0] == -1 and admit[n_vis - 1] >= 0
+
+
+@pytest.mark.parametrize("variant", [1, 2, 4, 8, 4 | 8, 1 | 4])
+def test_skip_rule_ablations_cross_where_the_closed_form_says(variant):
+    """The skip-rule ablations of Tab. 8 on constant states (zero decoder weights):
+    without E_ii or F_itc the retention score is the other term alone; without
+    accumulation a row is admitted at the first window layer whose own S_fuse
+    reaches T_skip (here: layer 0 or never); without SLC S_fuse = w1 S_sa and an
+    admitted row bypasses both sub-layers."""
+    from oracle.online import NO_EII, NO_FITC, NO_ACCUM, WHOLE_LAYER
+    dec = _tiny(12)
+    zero = [{"attn_norm": np.ones(dec.d), "ffn_norm": np.ones(dec.d),
+             "wq": np.zeros((dec.d, dec.d)), "wk": np.zeros((dec.d, dec.d)), "wv": np.zeros((dec.d, dec.d)),
+             "wo": np.zeros((dec.d, dec.d)), "wg": np.zeros((dec.d_ff, dec.d)), "wu": np.zeros((dec.d_ff, dec.d)),
+             "wd": np.zeros((dec.d, dec.d_ff))} for _ in range(dec.L)]
+    V, c = 4, 1.0
+    WU = np.zeros((V, dec.d))
+    WU[0, 0] = c
+    alphas = [0.0, 1.0, 2.5, 6.0, 12.0]
+    n_vis, n_text = len(alphas), 3
+    x = np.zeros((n_vis + n_text, dec.d))
+    for i, a in enumerate(alphas):
+        x[i, 0] = a
+    x[n_vis:, 1] = 1.0         # cos = 0: F_itc = 1/2 for every visual row
+    cu = np.array([0, n_vis + n_text])
+    sel = np.full(dec.L, 0.25)
+    m = np.array([l % 2 for l in range(dec.L)], np.uint8)
+    w1, w2 = 2.0, 1.0
+    T = (0.8 if variant & WHOLE_LAYER else 1.0) if variant & NO_ACCUM else 2.4
+    h, codes, admit, S = prefill_online(x, zero, cu, n_text, WU, sel, m, w1, w2, T, dec, recipe="f32",
+                                        variant=variant)
+    assert np.array_equal(h, x)
+    W = dec.L // 2
+    for i, a in enumerate(alphas):
+        E = 0.0 if variant & NO_EII else _entropy_closed_form(c * a, V)
+        F = 0.0 if variant & NO_FITC else 0.5
+        s = max(0.0, 1.0 - (E + F))
+        step = w1 * s + (0.0 if variant & WHOLE_LAYER else w2 * 0.25)
+        if variant & NO_ACCUM:
+            expect = 0 if step >= T else -1
+        elif step > 0:
+            cross = math.ceil(T / step - 1e-12) - 1
+            expect = cross if cross < W else -1
+        else:
+            expect = -1
+        assert admit[i] == expect, (i, a, s, admit[i], expect)
+        if expect >= 0:
+            if variant & WHOLE_LAYER:
+                bit = ak.SKIP_ATTN_BIT | ak.SKIP_FFN_BIT
+            else:
+                bit = ak.SKIP_ATTN_BIT if m[expect] == ak.ATTN else ak.SKIP_FFN_BIT
+            assert np.all(codes[:expect, i] == 0) and np.all(codes[expect:, i] == bit)
+        else:
+            assert np.all(codes[:, i] == 0)
+        assert np.allclose(S[:min(W, expect + 1 if expect >= 0 else W), i], s)
+    assert np.all(codes[:, n_vis:] == 0)
+    assert (admit >= 0).any() and (admit < 0).any() or variant & NO_EII
+
+
+def test_ablation_bits_zero_is_the_paper_rule():
+    dec = _tiny(8)
+    r = np.random.default_rng(5)
+    W = _weights(dec, r)
+    cu = np.array([0, 30, 70])
+    x = r.standard_normal((70, dec.d))
+    WU = r.standard_normal((16, dec.d))
+    sel = r.uniform(0.2, 1.0, dec.L)
+    m = (r.random(dec.L) < 0.5).astype(np.uint8)
+    a = prefill_online(x, W, cu, 10, WU, sel, m, 3.0, 1.0, 2.0, dec, recipe="f32")
+    b = prefill_online(x, W, cu, 10, WU, sel, m, 3.0, 1.0, 2.0, dec, recipe="f32", variant=0)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
