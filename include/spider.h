@@ -448,6 +448,39 @@ spider_status spider_prefill_online(const spider_decoder_cfg* cfg,
                                     spider_stream stream);
 
 /* ------------------------------------------------------------------------
+ * spider_prefill_online_ablation - spider_prefill_online under the ablations
+ * of the skip rule (Tab. 8 and its discussion; Sec. 4.2.1), selected by the
+ * bits of `ablation` (0 gives spider_prefill_online exactly):
+ *   SPIDER_ONLINE_NO_EII      the retention score is F_itc alone:
+ *                             S_sa = max(0, 1 - F_itc);
+ *   SPIDER_ONLINE_NO_FITC     the retention score is E_ii alone:
+ *                             S_sa = max(0, 1 - E_ii);
+ *   SPIDER_ONLINE_NO_ACCUM    no accumulation: acc_i = w1 * S_sa + w2 * slc_sel[l]
+ *                             of the current window layer alone;
+ *   SPIDER_ONLINE_WHOLE_LAYER without the SLC term: S_fuse = w1 * S_sa, and an
+ *                             admitted row bypasses both sub-layers (code 3)
+ *                             in layers l .. L-1 (target is then ignored but
+ *                             must still be valid).
+ * Arguments, outputs, workspace and synchronisation as spider_prefill_online;
+ * bits outside these four give SPIDER_ERR_INVALID_ARG.  (The ablation without
+ * S_sa, all visual rows following the offline SLC list, is spider_prefill with
+ * a per-layer mask.)
+ * ------------------------------------------------------------------------ */
+#define SPIDER_ONLINE_NO_EII 1u
+#define SPIDER_ONLINE_NO_FITC 2u
+#define SPIDER_ONLINE_NO_ACCUM 4u
+#define SPIDER_ONLINE_WHOLE_LAYER 8u
+
+spider_status spider_prefill_online_ablation(const spider_decoder_cfg* cfg,
+                                             const spider_layer_weights* layers, int B,
+                                             const int32_t* cu_seqlens, const void* x, int n_text,
+                                             const void* w_unembed, int V, const double* slc_sel,
+                                             const uint8_t* target, double w1, double w2, double T_skip,
+                                             uint32_t ablation, uint8_t* codes_out, int32_t* admit_out,
+                                             float* s_sa_out, float* h_out, void* workspace,
+                                             size_t workspace_bytes, spider_stream stream);
+
+/* ------------------------------------------------------------------------
  * Kernel-class profiler (process-global, not thread-safe; for benchmarks).
  * When enabled, every launch of the library records a pair of HIP events on
  * its stream.  spider_profile_read() synchronises on the recorded events and

@@ -71,6 +71,9 @@ _SIGS = {
     "spider_prefill_online": ([ctypes.POINTER(DecoderCfg), ctypes.POINTER(LayerWeights), _I, _VP, _VP,
                                _I, _VP, _I, _VP, _VP, _D, _D, _D, _VP, _VP, _VP, _VP, _VP, _SZ, _VP],
                               _I),
+    "spider_prefill_online_ablation": ([ctypes.POINTER(DecoderCfg), ctypes.POINTER(LayerWeights), _I, _VP,
+                                        _VP, _I, _VP, _I, _VP, _VP, _D, _D, _D, ctypes.c_uint32, _VP, _VP,
+                                        _VP, _VP, _VP, _SZ, _VP], _I),
     "spider_prefill_kv": ([ctypes.POINTER(DecoderCfg), ctypes.POINTER(LayerWeights), _I, _VP, _VP, _VP, _VP,
                            ctypes.POINTER(KVCache), _VP, _SZ, _VP], _I),
     "spider_decode_workspace_size": ([ctypes.POINTER(DecoderCfg), _I, _I, _I], _SZ),
@@ -352,11 +355,16 @@ def prefill_online_workspace_size(cfg: DecoderCfg, B: int, rows: int, V: int) ->
     return lib().spider_prefill_online_workspace_size(ctypes.byref(cfg), B, rows, V)
 
 
+# skip-rule ablation bits of spider_prefill_online_ablation
+ONLINE_NO_EII, ONLINE_NO_FITC, ONLINE_NO_ACCUM, ONLINE_WHOLE_LAYER = 1, 2, 4, 8
+
+
 def prefill_online(cfg: DecoderCfg, weights, cu_seqlens, x: torch.Tensor, n_text: int,
                    w_unembed: torch.Tensor, slc_sel, target, w1: float, w2: float, T_skip: float,
                    s_sa: bool = True, out: Optional[torch.Tensor] = None,
-                   workspace: Optional[torch.Tensor] = None, weight_table=None):
-    """Prefill driven by the online skip controller.
+                   workspace: Optional[torch.Tensor] = None, weight_table=None, ablation: int = 0):
+    """Prefill driven by the online skip controller (``ablation``: SPIDER_ONLINE_* bits,
+    0 = the paper's rule through spider_prefill_online).
 
     Returns (h [rows, d] fp32, codes [L, rows] uint8, admit [rows] int32,
     S_sa [L//2, rows] fp32 or None)."""
@@ -377,11 +385,14 @@ def prefill_online(cfg: DecoderCfg, weights, cu_seqlens, x: torch.Tensor, n_text
     if workspace is None or workspace.numel() < wsz + 256:
         workspace = _ws(wsz, dev)
     wt = weight_table if weight_table is not None else layer_weights(weights)
-    _check(lib().spider_prefill_online(ctypes.byref(cfg), wt, B, cu.ctypes.data, _ptr(x), n_text,
-                                       _ptr(w_unembed), V, sel.ctypes.data, tgt.ctypes.data, w1, w2,
-                                       T_skip, codes.ctypes.data if codes.size else None,
-                                       admit.ctypes.data if admit.size else None, _ptr(s_out),
-                                       _ptr(out), _aligned(workspace), wsz, _stream(dev)))
+    head = (ctypes.byref(cfg), wt, B, cu.ctypes.data, _ptr(x), n_text, _ptr(w_unembed), V,
+            sel.ctypes.data, tgt.ctypes.data, w1, w2, T_skip)
+    tail = (codes.ctypes.data if codes.size else None, admit.ctypes.data if admit.size else None,
+            _ptr(s_out), _ptr(out), _aligned(workspace), wsz, _stream(dev))
+    if ablation:
+        _check(lib().spider_prefill_online_ablation(*head, ablation, *tail))
+    else:
+        _check(lib().spider_prefill_online(*head, *tail))
     return out, codes, admit, s_out
 
 

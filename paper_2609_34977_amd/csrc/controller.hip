@@ -108,10 +108,12 @@ __global__ void __launch_bounds__(256) lens_prep_kernel(const float* __restrict_
 __device__ __forceinline__ void admit_row(double S, double T, int c, const int32_t* __restrict__ cand,
                                           const double* __restrict__ F, const LensAdmitArgs& p) {
   const double H = log(S) - T / S;
-  const double E = H / p.log_v;
-  const double ssa = fmax(0.0, 1.0 - (E + F[c]));
+  const double E = (p.ablation & SPIDER_ONLINE_NO_EII) ? 0.0 : H / p.log_v;
+  const double Fc = (p.ablation & SPIDER_ONLINE_NO_FITC) ? 0.0 : F[c];
+  const double ssa = fmax(0.0, 1.0 - (E + Fc));
   const int r = cand[c];
-  const double a = p.acc[r] + (p.w1 * ssa + p.w2_sel);
+  const double fuse = p.w1 * ssa + p.w2_sel;
+  const double a = (p.ablation & SPIDER_ONLINE_NO_ACCUM) ? fuse : p.acc[r] + fuse;
   p.acc[r] = a;
   p.flag[c] = a >= p.t_skip ? 1 : 0;
   if (p.s_out) p.s_out[r] = (float)ssa;

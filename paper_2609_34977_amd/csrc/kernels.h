@@ -121,6 +121,7 @@ struct LensAdmitArgs {
   double* acc;       // [rows] accumulated skip score (indexed by packed row)
   int32_t* flag;     // [nc] 1 = admitted at this layer
   float* s_out;      // [rows] S_sa of this layer, or null
+  uint32_t ablation; // SPIDER_ONLINE_* bits: E_ii or F_itc left out, no accumulation
 };
 // Per candidate c (logits row c of [nc, V]): E_ii, S_sa, acc update, flag.
 hipError_t launch_lens_admit(const float* logits, int V, const int32_t* cand, int nc, const int32_t* nc_dev,

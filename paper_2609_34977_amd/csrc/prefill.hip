@@ -1237,6 +1237,12 @@ struct OnlineParams {
   const double* slc_sel;
   const uint8_t* target;
   double w1, w2, t_skip;
+  uint32_t ablation;  // SPIDER_ONLINE_* bits
+  // code bits an admission at window layer l sets: the layer's SLC target, or
+  // both sub-layers without SLC
+  int bypass_bits(int l) const {
+    return (ablation & SPIDER_ONLINE_WHOLE_LAYER) ? 3 : (target[l] == 1 ? 2 : 1);
+  }
 };
 
 // Whether the online prefill keeps its bookkeeping on the device.  Needs at
@@ -1346,8 +1352,9 @@ spider_status run_prefill_online(const spider_decoder_cfg& c, const spider_layer
     }
     {
       ProfScope ps(KC_LENS_ADMIT, st);
-      LensAdmitArgs p{std::log((double)op.V), op.w1, op.w2 * op.slc_sel[l], op.t_skip, ows.acc, ows.flag,
-                      s_sa_out ? s_sa_out + (size_t)l * R : nullptr};
+      const double w2_sel = (op.ablation & SPIDER_ONLINE_WHOLE_LAYER) ? 0.0 : op.w2 * op.slc_sel[l];
+      LensAdmitArgs p{std::log((double)op.V), op.w1, w2_sel, op.t_skip, ows.acc, ows.flag,
+                      s_sa_out ? s_sa_out + (size_t)l * R : nullptr, op.ablation};
       hipError_t e = fused ? launch_lens_admit_stats(ows.stats, ntiles, dcand, nc, nc_dev, ows.F, p, st)
                            : launch_lens_admit(ows.logits, op.V, dcand, nc, nc_dev, ows.F, p, st);
       SPIDER_REQUIRE(e == hipSuccess, SPIDER_ERR_HIP, "lens_admit: %s", hipGetErrorString(e));
@@ -1367,7 +1374,7 @@ spider_status run_prefill_online(const spider_decoder_cfg& c, const spider_layer
 
   if (on_dev) {
     auto plan = [&](int l) -> spider_status {
-      const int bit = (l >= 0 && l < Wn) ? (op.target[l] == 1 ? 2 : 1) : 0;
+      const int bit = (l >= 0 && l < Wn) ? op.bypass_bits(l) : 0;
       online_plan_kernel<<<1, 256, 0, st>>>(l, L, Wn, R, bit, ows.tab + ot.vis, ows.flag, dcand,
                                             ows.tab + ot.admit, ows.tab + ot.code, dcodes,
                                             ows.tab + ot.reg[l > 0 ? (l & 1) : 0], ows.tab + ot.cnt);
@@ -1422,7 +1429,7 @@ spider_status run_prefill_online(const spider_decoder_cfg& c, const spider_layer
         SPIDER_HIP(hipMemcpyAsync(g_back.host, ows.flag, fbytes, hipMemcpyDeviceToHost, st));
         SPIDER_HIP(hipStreamSynchronize(st));
         const int32_t* flag = reinterpret_cast<const int32_t*>(g_back.host);
-        const uint8_t bit = op.target[l] == 1 ? 2 : 1;
+        const uint8_t bit = (uint8_t)op.bypass_bits(l);
         for (int i = 0; i < nc; ++i) {
           if (!flag[i]) continue;
           const int r = cand[i];
@@ -1689,12 +1696,14 @@ extern "C" size_t spider_prefill_online_workspace_size(const spider_decoder_cfg*
   return online_layout(*cfg, B, std::max(rows, 1), V, nullptr).bytes;
 }
 
-extern "C" spider_status spider_prefill_online(
-    const spider_decoder_cfg* cfg, const spider_layer_weights* layers, int B, const int32_t* cu_seqlens,
-    const void* x, int n_text, const void* w_unembed, int V, const double* slc_sel, const uint8_t* target,
-    double w1, double w2, double T_skip, uint8_t* codes_out, int32_t* admit_out, float* s_sa_out,
-    float* h_out, void* workspace, size_t workspace_bytes, spider_stream stream) {
-  clear_error();
+namespace spider {
+namespace {
+spider_status prefill_online_entry(const spider_decoder_cfg* cfg, const spider_layer_weights* layers, int B,
+                                   const int32_t* cu_seqlens, const void* x, int n_text, const void* w_unembed,
+                                   int V, const double* slc_sel, const uint8_t* target, double w1, double w2,
+                                   double T_skip, uint32_t ablation, uint8_t* codes_out, int32_t* admit_out,
+                                   float* s_sa_out, float* h_out, void* workspace, size_t workspace_bytes,
+                                   spider_stream stream) {
   SPIDER_TRY(validate_cfg(cfg));
   SPIDER_TRY(validate_cu(B, cu_seqlens, layers));
   SPIDER_REQUIRE(n_text >= 1, SPIDER_ERR_INVALID_ARG, "spider_prefill_online: n_text must be >= 1");
@@ -1731,13 +1740,39 @@ extern "C" spider_status spider_prefill_online(
   SPIDER_REQUIRE(((uintptr_t)workspace % 256) == 0, SPIDER_ERR_WORKSPACE,
                  "spider_prefill_online: workspace must be 256-byte aligned");
   const OnlineWs ows = online_layout(*cfg, B, R, V, reinterpret_cast<char*>(workspace));
-  const OnlineParams op{n_text, w_unembed, V, slc_sel, target, w1, w2, T_skip};
+  const OnlineParams op{n_text, w_unembed, V, slc_sel, target, w1, w2, T_skip, ablation};
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (cfg->dtype == SPIDER_BF16)
     return run_prefill_online<uint16_t>(*cfg, layers, B, cu_seqlens, x, op, codes_out, admit_out, s_sa_out,
                                         h_out, ows, st);
   return run_prefill_online<float>(*cfg, layers, B, cu_seqlens, x, op, codes_out, admit_out, s_sa_out,
                                    h_out, ows, st);
+}
+}  // namespace
+}  // namespace spider
+
+extern "C" spider_status spider_prefill_online(
+    const spider_decoder_cfg* cfg, const spider_layer_weights* layers, int B, const int32_t* cu_seqlens,
+    const void* x, int n_text, const void* w_unembed, int V, const double* slc_sel, const uint8_t* target,
+    double w1, double w2, double T_skip, uint8_t* codes_out, int32_t* admit_out, float* s_sa_out,
+    float* h_out, void* workspace, size_t workspace_bytes, spider_stream stream) {
+  clear_error();
+  return prefill_online_entry(cfg, layers, B, cu_seqlens, x, n_text, w_unembed, V, slc_sel, target, w1, w2,
+                              T_skip, 0u, codes_out, admit_out, s_sa_out, h_out, workspace, workspace_bytes,
+                              stream);
+}
+
+extern "C" spider_status spider_prefill_online_ablation(
+    const spider_decoder_cfg* cfg, const spider_layer_weights* layers, int B, const int32_t* cu_seqlens,
+    const void* x, int n_text, const void* w_unembed, int V, const double* slc_sel, const uint8_t* target,
+    double w1, double w2, double T_skip, uint32_t ablation, uint8_t* codes_out, int32_t* admit_out,
+    float* s_sa_out, float* h_out, void* workspace, size_t workspace_bytes, spider_stream stream) {
+  clear_error();
+  SPIDER_REQUIRE((ablation & ~15u) == 0, SPIDER_ERR_INVALID_ARG,
+                 "spider_prefill_online_ablation: unknown ablation bits 0x%x", ablation & ~15u);
+  return prefill_online_entry(cfg, layers, B, cu_seqlens, x, n_text, w_unembed, V, slc_sel, target, w1, w2,
+                              T_skip, ablation, codes_out, admit_out, s_sa_out, h_out, workspace,
+                              workspace_bytes, stream);
 }
 
 extern "C" spider_status spider_prefill_kv(const spider_decoder_cfg* cfg, const spider_layer_weights* layers, int B,

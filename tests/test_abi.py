@@ -240,6 +240,29 @@ def test_prefill_online_validation_before_any_hip_call(L):
     assert lib_mod.prefill_online_workspace_size(bf, 1, 192, 32000) > lib_mod.prefill_workspace_size(bf, 1, 192)
 
 
+def test_prefill_online_ablation_validation_before_any_hip_call(L):
+    """The ablation entry point: unknown bits are rejected first, the other
+    checks are those of spider_prefill_online."""
+    bf = lib_mod.decoder_cfg(4, 4096, 32, 11008, lib_mod.BF16)
+    W = (lib_mod.LayerWeights * bf.L)()
+    for i in range(bf.L):
+        W[i] = lib_mod.LayerWeights(*([0x1000] * 9))
+    cu = np.array([0, 10], np.int32)
+    sel = np.zeros(bf.L, np.float64)
+    tgt = np.zeros(bf.L, np.uint8)
+    codes = np.zeros((bf.L, 10), np.uint8)
+
+    def call(bits, n_text=4, ws_bytes=1 << 40):
+        return L.spider_prefill_online_ablation(ctypes.byref(bf), W, 1, cu.ctypes.data, 0x1000, n_text, 0x1000,
+                                                32000, sel.ctypes.data, tgt.ctypes.data, 1.0, 0.5, 1.0, bits,
+                                                codes.ctypes.data, None, None, 0x1000, 0x100000, ws_bytes, None)
+    assert call(16) == INVALID and b"ablation" in L.spider_last_error()
+    assert call(0x80000000) == INVALID
+    assert call(1 | 8, n_text=0) == INVALID
+    for bits in (0, 1, 2, 4, 8, 15):
+        assert call(bits, ws_bytes=100) == WORKSPACE
+
+
 @pytest.mark.parametrize("n,num,den", [(576, 1, 2), (1000, 2, 5), (7, 1, 2), (1369, 1, 2), (50, 1, 1), (50, 0, 3)])
 def test_budget_ratio_matches_oracle(L, n, num, den):
     assert lib_mod.budget_ratio(n, num, den) == mp.budget_ratio(n, num, den)

@@ -1,0 +1,126 @@
+"""GPU prefill under the skip-rule ablations (spider_prefill_online_ablation,
+Tab. 8) against the oracle's online prefill with the same ablation bits.
+
+Each variant changes how S_sa, the accumulated score or the bypassed
+sub-layers are formed; the thresholds are chosen as in test_gpu_online, from
+the scores the oracle's rows reach under that variant (the per-layer S_fuse
+without accumulation), and checked to keep every decision clear of T_skip.
+Bars as for the paper's rule: admission layers and the mask identical, S_sa
+within 1e-4 (layer 0 and fp32) / 1e-2 (bf16 later layers), h per sample
+within 2e-2 (bf16) / 1e-4 (fp32).  The last case has two text rows, so the
+admissions go through the host between window layers.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import asl_skip as ak
+from oracle.online import prefill_online, NO_ACCUM, WHOLE_LAYER
+from synth import get_workload
+from synth.decoder_inputs import layer_weights
+from synth.online_inputs import decoder_rows, unembed
+from gpu_common import need_gpu, rel_err, log
+from test_gpu_online import W1, W2, _policy
+
+CASES = {
+    # name: (workload, layers, cu_seqlens, n_text, V)
+    "tiny_fp32": ("tiny", 8, [0, 80], 32, 1000),
+    "7b_two_window_layers": ("llava15_7b", 4, [0, 128], 64, 32000),
+    "tiny_fp32_host_admission": ("tiny", 8, [0, 80], 2, 1000),
+}
+VARIANTS = {"no_eii": 1, "no_fitc": 2, "no_accum": 4, "whole_layer": 8}
+
+
+def _fuse(S, sel, l, variant):
+    return W1 * S + (0.0 if variant & WHOLE_LAYER else W2 * sel[l])
+
+
+def _margins(S, admit, sel, T, vis_rows, variant):
+    acc = np.zeros(len(vis_rows))
+    out = []
+    for l in range(S.shape[0]):
+        live = np.array([admit[r] < 0 or admit[r] >= l for r in vis_rows])
+        f = _fuse(S[l, vis_rows], sel, l, variant)
+        acc = np.where(live, f if variant & NO_ACCUM else acc + f, acc)
+        out.append(float(np.min(np.abs(acc[live] - T))) if live.any() else np.inf)
+    return out
+
+
+def _thresholds(S_free, sel, vis_rows, variant, n_max=8):
+    W = S_free.shape[0]
+    if variant & NO_ACCUM:
+        a = np.sort(np.concatenate([_fuse(S_free[l, vis_rows], sel, l, variant) for l in range(W)]))
+    else:
+        a = np.sort(sum(_fuse(S_free[l, vis_rows], sel, l, variant) for l in range(W)))
+    lo, hi = np.quantile(a, 0.1), np.quantile(a, 0.9)
+    gaps = [(a[i + 1] - a[i], 0.5 * (a[i] + a[i + 1])) for i in range(len(a) - 1)
+            if lo <= a[i] and a[i + 1] <= hi]
+    gaps.sort(reverse=True)
+    return [t for _, t in gaps[:n_max]]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("variant", list(VARIANTS))
+@pytest.mark.parametrize("case", list(CASES))
+def test_online_ablation_parity(case, variant):
+    L = need_gpu()
+    bits = VARIANTS[variant]
+    wl, n_layers, cu, n_text, V = CASES[case]
+    dec = get_workload(wl).dec
+    bf16 = dec.dtype == "bf16"
+    recipe = "bf16" if bf16 else "f32"
+    cu = np.array(cu, np.int32)
+    rows = int(cu[-1])
+    Wn = n_layers // 2
+    log(f"[online ablation] case={case} variant={variant} L={n_layers} rows={rows} V={V}")
+    x = decoder_rows(dec, cu, n_text, seed=5)
+    wu_cpu = unembed(dec, V, seed=6)
+    vis_rows = [r for b in range(len(cu) - 1) for r in range(int(cu[b]), int(cu[b + 1]) - n_text)]
+
+    sa, sf = _policy(n_layers)
+    na, nf = ak.slc_normalize(sa, sf)
+    m, sel = ak.skip_targets(na, nf)
+    cfg_o = dataclasses.replace(dec, L=n_layers)
+    wts = lambda l: {k: v.float().numpy() for k, v in layer_weights(dec, l, 0, "cpu").items()}
+    xo = x.float().numpy()
+    wuo = wu_cpu.float().numpy()
+
+    def oracle(T):
+        return prefill_online(xo, wts, cu, n_text, wuo, sel, m, W1, W2, T, cfg_o, recipe=recipe, variant=bits)
+
+    _, _, _, S_free = oracle(np.inf)
+    margin_need = [1e-3] + [2e-2 if bf16 else 1e-3] * (Wn - 1)
+    chosen = None
+    for T in _thresholds(S_free, sel, vis_rows, bits):
+        ref = oracle(T)
+        mg = _margins(ref[3], ref[2], sel, T, vis_rows, bits)
+        if all(v >= need for v, need in zip(mg, margin_need)):
+            chosen = (T, ref)
+            break
+    assert chosen is not None, "no threshold keeps the oracle's decisions clear of it"
+    T, (h_o, codes_o, admit_o, S_o) = chosen
+    hist = np.bincount(admit_o[vis_rows] + 1, minlength=Wn + 1)
+    log(f"  T_skip={T:.6f}: never admitted {hist[0]}, admitted per window layer {hist[1:].tolist()}")
+
+    sel_g, tgt_g = L.slc_policy(sa, sf, 1e-8)
+    W = [layer_weights(dec, l, 0, "cuda") for l in range(n_layers)]
+    cfg = L.decoder_cfg(n_layers, dec.d, dec.H, dec.d_ff, L.BF16 if bf16 else L.F32, dec.eps, dec.theta)
+    h, codes, admit, S = L.prefill_online(cfg, W, cu, x.cuda(), n_text, wu_cpu.cuda(), sel_g, tgt_g, W1, W2, T,
+                                          ablation=bits)
+    torch.cuda.synchronize()
+    h = h.cpu().numpy()
+    S = S.cpu().numpy()
+    for l in range(Wn):
+        cand = [r for r in vis_rows if admit_o[r] < 0 or admit_o[r] >= l]
+        e = float(np.max(np.abs(S[l, cand] - S_o[l, cand]))) if cand else 0.0
+        assert e <= (1e-4 if (l == 0 or not bf16) else 1e-2), (l, e)
+    assert np.array_equal(admit, admit_o.astype(np.int32))
+    assert np.array_equal(codes, codes_o)
+    if bits & WHOLE_LAYER:
+        assert set(np.unique(codes)) <= {0, 3}
+    tol = 2e-2 if bf16 else 1e-4
+    for b in range(len(cu) - 1):
+        e = rel_err(h[cu[b]:cu[b + 1]], h_o[cu[b]:cu[b + 1]])
+        assert e <= tol, f"sample {b}: {e}"
