@@ -288,7 +288,13 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
   __shared__ int red[2][4];
   const int tid = threadIdx.x, lane = tid & 63, hi = lane >> 5, lo = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int h = blockIdx.y;
+  // One-dimensional grid, heads innermost, query tiles from the last one down.
+  // The compacted queries are packed by sample in ascending position, so
+  // within a sample a later tile sees more keys: the causal tiles start
+  // longest first and the blocks that start last are short ones.
+  const int ntiles = (a.nq + 128 * QT - 1) / (128 * QT);
+  const int tile = ntiles - 1 - (int)blockIdx.x / a.H;
+  const int h = (int)blockIdx.x % a.H;
   const uint16_t* Q = reinterpret_cast<const uint16_t*>(a.q);
   const uint16_t* Kp = reinterpret_cast<const uint16_t*>(a.k);
   const uint16_t* VT = reinterpret_cast<const uint16_t*>(a.v);
@@ -299,7 +305,7 @@ __global__ void __launch_bounds__(256, QT == 1 ? 2 : 1) attention_wide_kernel(At
   int wlo = 0x7FFFFFFF, whi = -1;
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
-    qa[t] = blockIdx.x * (128 * QT) + wave * (32 * QT) + 32 * t + lo;
+    qa[t] = tile * (128 * QT) + wave * (32 * QT) + 32 * t + lo;
     qok[t] = qa[t] < a.nq;
     qrow[t] = qok[t] ? a.q_rows[qa[t]] : -1;
     qst[t] = qok[t] ? a.row_start[qrow[t]] : 0x7FFFFFFF;
@@ -620,7 +626,7 @@ hipError_t launch_attention_bf16(const AttnArgs& a, hipStream_t st) {
   // two tiles per wave measured 1.7x slower at one wave per SIMD).  Fewer
   // queries: the per-32-query kernel, whose waves split the keys.
   if (wide) {
-    attention_wide_kernel<1><<<dim3(ceil_div(a.nq, 128), a.H), 256, 0, st>>>(a);
+    attention_wide_kernel<1><<<ceil_div(a.nq, 128) * a.H, 256, 0, st>>>(a);
   } else {
     attention_bf16_kernel<<<dim3(ceil_div(a.nq, 32), a.H), 256, 0, st>>>(a);
   }
