@@ -30,7 +30,8 @@ CASES = {
     "7b_two_window_layers": ("llava15_7b", 4, [0, 128], 64, 32000),
     "tiny_fp32_host_admission": ("tiny", 8, [0, 80], 2, 1000),
 }
-VARIANTS = {"no_eii": 1, "no_fitc": 2, "no_accum": 4, "whole_layer": 8}
+VARIANTS = {"no_eii": 1, "no_fitc": 2, "no_accum": 4, "whole_layer": 8, "no_eii_no_accum": 5,
+            "no_accum_whole_layer": 12}
 
 
 def _fuse(S, sel, l, variant):
