@@ -75,6 +75,10 @@ def parse():
     p.add_argument("--decode", type=int, default=0,
                    help="after the step, also time this many greedy decode steps (LM head included) over the "
                         "KV cache of the pruned and skipped prefill; reported in the `decode` field")
+    p.add_argument("--vendor-gemm", action="store_true",
+                   help="context, not the benchmark step: the library's per-launch decoder GEMM times in a "
+                        "prefill without skipping beside torch.nn.functional.linear (hipBLASLt) on the same "
+                        "shapes, one JSON line per workload")
     p.add_argument("--projector", action="store_true",
                    help="prune before the projector: the step also runs LLaVA's two-layer GELU projector "
                         "(ViT width -> decoder width) on the kept rows only")
@@ -590,6 +594,57 @@ def run_step(w, args, dev, weights=None, online=False, projector_on=False, decod
     return res, W
 
 
+GEMM_SHAPES = ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down")
+
+
+def vendor_gemm(args, dev):
+    """Context for the decoder GEMMs.  For each workload the prefill runs without
+    skipping (every sub-layer over every row, so each launch has M = the decoder
+    rows) and its per-launch time per GEMM class is read from the profiled pre-pass;
+    beside it torch.nn.functional.linear (hipBLASLt) runs the same products in bf16:
+    QKV [M, 3d], O [M, d], gate and up stacked [M, 2 d_ff] (plain products: no SwiGLU,
+    bf16 outputs), down [M, d] over K = d_ff.  Both read cold weights: the prefill
+    streams 32+ layers of distinct weights, the library call cycles through copies
+    totalling more than the 256 MB last-level cache.  Up to 256 rows the library's
+    classes end with fp32 split-K partials whose sum happens in the next kernel (the
+    norm, or the QKV finalize), which is not counted here."""
+    import torch.nn.functional as F
+    from synth import get_workload
+    for name, keep in (("stress", 576), ("stress", 288), ("llava15_13b", None), ("llava_next_7b", 128),
+                       ("llava15_7b", 128)):
+        w = get_workload(name, keep=keep, L=args.layers, skip_p=0.0)
+        res, _ = run_step(w, args, dev, cpu=False)
+        M = res["config"]["decoder_rows"]
+        d, dff = w.dec.d, w.dec.d_ff
+        shapes = {"gemm_qkv": (3 * d, d), "gemm_o": (d, d), "gemm_gateup": (2 * dff, d), "gemm_down": (d, dff)}
+        km, ln = res["kernel_ms_per_step"], res["launches_per_step"]
+        ours = {c: 1e3 * km[c] / ln[c] for c in GEMM_SHAPES if ln.get(c)}
+        vend = {}
+        for c in GEMM_SHAPES:
+            N, K = shapes[c]
+            a = torch.randn(M, K, device=dev, dtype=torch.bfloat16)
+            copies = max(2, -(-(1 << 30) // (N * K * 2)))
+            ws = [torch.randn(N, K, device=dev, dtype=torch.bfloat16) for _ in range(copies)]
+            for i in range(copies):
+                F.linear(a, ws[i])
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            n = 4 * copies
+            e0.record()
+            for i in range(n):
+                F.linear(a, ws[i % copies])
+            e1.record()
+            torch.cuda.synchronize()
+            vend[c] = 1e3 * e0.elapsed_time(e1) / n
+            del a, ws
+            torch.cuda.empty_cache()
+        tf = {c: 2.0 * M * shapes[c][0] * shapes[c][1] / 1e6 for c in GEMM_SHAPES}  # flop / us -> TFLOP/s
+        print(json.dumps({"mode": "vendor_gemm", "workload": res["config"]["workload"], "rows": M, "d": d,
+                          "d_ff": dff, "ours_us": ours, "hipblaslt_us": vend,
+                          "ours_tflops": {c: tf[c] / ours[c] for c in ours},
+                          "hipblaslt_tflops": {c: tf[c] / vend[c] for c in vend}}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -616,6 +671,9 @@ def main():
         return
     if args.curve:
         curve(args, dev)
+        return
+    if args.vendor_gemm:
+        vendor_gemm(args, dev)
         return
     cpu = not args.no_cpu_baseline and not args.online and not args.projector
     res, W = run_step(w, args, dev, online=args.online, projector_on=args.projector, decode=args.decode,

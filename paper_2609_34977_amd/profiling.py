@@ -274,7 +274,8 @@ def mfma(args):
 
 
 def sweep_table(args):
-    """Markdown table of bench.py JSON lines (score / select sweeps, the stress curve)."""
+    """Markdown table of bench.py JSON lines (score / select sweeps, the stress curve, the
+    hipBLASLt context)."""
     rows = []
     with open(args.jsonl) as f:
         for ln in f:
@@ -292,6 +293,18 @@ def sweep_table(args):
                          f"{r['tokens_per_s']:.0f} | {r['prefill_tflop_per_step']:.1f} | "
                          f"{r['prefill_tflop_per_step'] / r['ms_per_step'] * 1e3:.0f} | {ro['kernel']} | "
                          f"{ro['bound']} | {ro['achieved']:.0f} {ro['unit']} | {ro['frac']:.3f} |")
+    elif rows and rows[0].get("mode") == "vendor_gemm":
+        cls = ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down")
+        lines += ["", "Per launch, microseconds (TFLOP/s); last column: the library's time over hipBLASLt's.", "",
+                  "| workload | rows | class | library us (TFLOP/s) | hipBLASLt us (TFLOP/s) | ratio |",
+                  "|---|---|---|---|---|---|"]
+        for r in rows:
+            for c in cls:
+                if c not in r["ours_us"]:
+                    continue
+                lines.append(f"| {r['workload']} | {r['rows']} | {c} | {r['ours_us'][c]:.1f} "
+                             f"({r['ours_tflops'][c]:.0f}) | {r['hipblaslt_us'][c]:.1f} "
+                             f"({r['hipblaslt_tflops'][c]:.0f}) | {r['ours_us'][c] / r['hipblaslt_us'][c]:.2f} |")
     elif rows and rows[0].get("mode") == "select_sweep":
         lines += ["", "| keep / tile | tiles | kept rows | select ms | select frac of HBM | gather ms | "
                       "gather MB | gather frac of HBM |", "|---|---|---|---|---|---|---|---|"]

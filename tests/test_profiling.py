@@ -138,3 +138,20 @@ def test_stats_table_keeps_library_kernels_and_class_line(tmp_path):
     assert "| `gemm_tile_kernel<4, true, false>` | 4 | 1.00 |" in text
     # 4 launches; the tail reduction's time is part of the class
     assert "4 launches, 1.10 us per launch" in text
+
+
+def test_vendor_gemm_table_rows_and_ratio(tmp_path):
+    line = {"mode": "vendor_gemm", "workload": "stress_keep288_skip0", "rows": 6014, "d": 4096, "d_ff": 11008,
+            "ours_us": {"gemm_qkv": 500.0, "gemm_o": 180.0, "gemm_gateup": 900.0},
+            "hipblaslt_us": {"gemm_qkv": 550.0, "gemm_o": 200.0, "gemm_gateup": 880.0, "gemm_down": 480.0},
+            "ours_tflops": {"gemm_qkv": 1210.0, "gemm_o": 1120.0, "gemm_gateup": 1205.0},
+            "hipblaslt_tflops": {"gemm_qkv": 1100.0, "gemm_o": 1008.0, "gemm_gateup": 1232.0, "gemm_down": 1100.0}}
+    src = tmp_path / "v.jsonl"
+    src.write_text("# a comment line\n" + json.dumps(line) + "\n")
+    out = tmp_path / "v.md"
+    P.sweep_table(argparse.Namespace(jsonl=str(src), out=str(out), title="t", command=["cmd"], note=None))
+    rows = [ln for ln in out.read_text().splitlines() if ln.startswith("| stress")]
+    # a class the library did not launch is left out; the ratio is library / hipBLASLt
+    assert len(rows) == 3
+    assert rows[0].split("|")[3].strip() == "gemm_qkv" and rows[0].rstrip("| ").endswith("0.91")
+    assert "900.0 (1205)" in rows[2] and rows[2].rstrip("| ").endswith("1.02")
