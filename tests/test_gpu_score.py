@@ -155,3 +155,43 @@ def test_score_tapped_layer_variants(variant):
     err = np.abs(s[na] - o["s"][na]) / np.maximum(1.0, np.abs(o["s"][na]))
     assert err.max() <= 1e-5, f"s error {err.max()}"
     assert np.max(np.abs(m - o["mvec"]) / np.maximum(1.0, np.abs(o["mvec"]))) <= 1e-5
+
+
+WIDE = {
+    # name: (patches n, width d_v, heads, tapped layers, keep, K): the feature-width
+    # paths past 1024 (SigLIP-like 27 x 27 x 1152, a Qwen-ViT-like 1280 with three
+    # taps) and the largest tile the entry point takes (4096 patches, d_v 2048: the
+    # anchor top-k sorts 4096 keys)
+    "siglip_729x1152": (729, 1152, 16, (13, 26), 182, 4),
+    "qwen_1024x1280_three_taps": (1024, 1280, 16, (8, 16, 32), 256, 4),
+    "max_4096x2048": (4096, 2048, 16, (12, 24), 1024, 4),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", list(WIDE))
+def test_score_wide_features_and_largest_tile(case):
+    """Same bars as test_score_parity on one tile of each shape (seeded CLIP-style taps)."""
+    import dataclasses
+    L = need_gpu()
+    n, dv, H, layers, keep, K = WIDE[case]
+    cfg = dataclasses.replace(get_workload("llava15_7b", keep=keep).score, G=1, n=n, d_v=dv, H=H,
+                              layers=layers, keep=keep, K=K)
+    log(f"[score wide] case={case} n={n} d_v={dv} taps={layers} keep={keep} K={K}")
+    attn, feats = vision_inputs(cfg, 7)
+    n_anchor = (keep * 7) // 10
+    out = L.score(attn.cuda(), [f.cuda() for f in feats], n_anchor, K, cfg.kmeans_iter)
+    torch.cuda.synchronize()
+    a, cl = out["a"].cpu().numpy()[0], out["cluster"].cpu().numpy()[0]
+    s, m = out["s"].cpu().numpy()[0], out["m"].cpu().numpy()[0]
+    o = oracle_tiles(attn, feats, keep, 7, 10, K, cfg.kmeans_iter)[0]
+    assert np.array_equal(a, o["a"])
+    assert set(np.nonzero(cl < 0)[0]) == set(o["anchors"])
+    assert o["margin"].min() > 1e-4, "input too close to a K-means tie for an exact check"
+    assert np.array_equal(cl, o["cluster"])
+    na = o["cluster"] >= 0
+    assert np.all(np.isinf(s[~na]))
+    err = np.abs(s[na] - o["s"][na]) / np.maximum(1.0, np.abs(o["s"][na]))
+    assert err.max() <= 1e-5, f"s error {err.max()}"
+    merr = np.abs(m - o["mvec"]) / np.maximum(1.0, np.abs(o["mvec"]))
+    assert merr.max() <= 1e-5, f"m error {merr.max()}"
