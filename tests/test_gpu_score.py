@@ -158,27 +158,33 @@ def test_score_tapped_layer_variants(variant):
 
 
 WIDE = {
-    # name: (patches n, width d_v, heads, tapped layers, keep, K): the feature-width
-    # paths past 1024 (SigLIP-like 27 x 27 x 1152, a Qwen-ViT-like 1280 with three
-    # taps) and the largest tile the entry point takes (4096 patches, d_v 2048: the
-    # anchor top-k sorts 4096 keys)
-    "siglip_729x1152": (729, 1152, 16, (13, 26), 182, 4),
-    "qwen_1024x1280_three_taps": (1024, 1280, 16, (8, 16, 32), 256, 4),
-    "max_4096x2048": (4096, 2048, 16, (12, 24), 1024, 4),
+    # name: (patches n, width d_v, heads, tapped layers, keep, K, fp32 features): the
+    # feature-width paths of the scoring kernels not taken by the CLIP-L and tiny
+    # workloads -- bf16 at d_v <= 512 (ViT-S-like 384), fp32 past 512 (the CLIP-L
+    # tile with its bf16 features widened exactly), past 1024 (SigLIP-like 27 x 27 x
+    # 1152, a Qwen-ViT-like 1280 with three taps) -- and the largest tile the entry
+    # point takes (4096 patches, d_v 2048: the anchor top-k sorts 4096 keys)
+    "vit_s_576x384_bf16": (576, 384, 6, (6, 12), 144, 4, False),
+    "clip_l_576x1024_fp32": (576, 1024, 16, (12, 24), 128, 4, True),
+    "siglip_729x1152": (729, 1152, 16, (13, 26), 182, 4, False),
+    "qwen_1024x1280_three_taps": (1024, 1280, 16, (8, 16, 32), 256, 4, False),
+    "max_4096x2048": (4096, 2048, 16, (12, 24), 1024, 4, False),
 }
 
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("case", list(WIDE))
-def test_score_wide_features_and_largest_tile(case):
+def test_score_feature_width_paths(case):
     """Same bars as test_score_parity on one tile of each shape (seeded CLIP-style taps)."""
     import dataclasses
     L = need_gpu()
-    n, dv, H, layers, keep, K = WIDE[case]
+    n, dv, H, layers, keep, K, f32 = WIDE[case]
     cfg = dataclasses.replace(get_workload("llava15_7b", keep=keep).score, G=1, n=n, d_v=dv, H=H,
                               layers=layers, keep=keep, K=K)
-    log(f"[score wide] case={case} n={n} d_v={dv} taps={layers} keep={keep} K={K}")
+    log(f"[score width] case={case} n={n} d_v={dv} taps={layers} keep={keep} K={K} fp32={f32}")
     attn, feats = vision_inputs(cfg, 7)
+    if f32:
+        feats = [f.float() for f in feats]
     n_anchor = (keep * 7) // 10
     out = L.score(attn.cuda(), [f.cuda() for f in feats], n_anchor, K, cfg.kmeans_iter)
     torch.cuda.synchronize()
