@@ -49,6 +49,11 @@ CASES = {
     "7b_two_window_layers": ("llava15_7b", 4, [0, 128], 64, 32000),
     "7b_100_visual": ("llava15_7b", 2, [0, 164], 64, 32000),
     "7b_unfused_lens_v32064": ("llava15_7b", 2, [0, 192], 64, 32064),
+    # the logits path's row tiles of 64, 192 and 256 candidates (the last one with
+    # the bookkeeping on the host: 320 rows)
+    "7b_unfused_lens_v32064_64_candidates": ("llava15_7b", 2, [0, 128], 64, 32064),
+    "7b_unfused_lens_v32064_192_candidates": ("llava15_7b", 2, [0, 256], 64, 32064),
+    "7b_unfused_lens_v32064_256_candidates": ("llava15_7b", 2, [0, 320], 64, 32064),
 }
 
 

@@ -169,6 +169,15 @@ WIDE = {
     "siglip_729x1152": (729, 1152, 16, (13, 26), 182, 4, False),
     "qwen_1024x1280_three_taps": (1024, 1280, 16, (8, 16, 32), 256, 4, False),
     "max_4096x2048": (4096, 2048, 16, (12, 24), 1024, 4, False),
+    # the score pass per cluster-mean layout: the block kernel while layers x K x d_v
+    # fits its LDS (8192 floats), the per-wave kernel past that, for each width class
+    # and dtype
+    "qwen_1024x1280_fp32": (1024, 1280, 16, (8, 16), 256, 4, True),
+    "qwen_1024x1280_fp32_K3": (1024, 1280, 16, (8, 16), 256, 3, True),
+    "siglip_729x1152_K3": (729, 1152, 16, (13, 26), 182, 3, False),
+    "vit_s_576x384_K8_three_taps": (576, 384, 6, (4, 8, 12), 144, 8, False),
+    "vit_s_576x384_fp32_K8_three_taps": (576, 384, 6, (4, 8, 12), 144, 8, True),
+    "clip_l_576x1024_fp32_K8": (576, 1024, 16, (12, 24), 128, 8, True),
 }
 
 
@@ -201,3 +210,42 @@ def test_score_feature_width_paths(case):
     assert err.max() <= 1e-5, f"s error {err.max()}"
     merr = np.abs(m - o["mvec"]) / np.maximum(1.0, np.abs(o["mvec"]))
     assert merr.max() <= 1e-5, f"m error {merr.max()}"
+
+
+NT_BATCH = {
+    # name: (patches n, width d_v, fp32 features, tiles G): one call over more than
+    # 256 MB of features, which the scoring pass reads with non-temporal loads
+    "bf16_384": (576, 384, False, 312),
+    "bf16_1024": (576, 1024, False, 120),
+    "bf16_1152": (729, 1152, False, 88),
+    "fp32_384": (576, 384, True, 160),
+    "fp32_1024": (576, 1024, True, 64),
+    "fp32_1280": (1024, 1280, True, 32),
+}
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", list(NT_BATCH))
+def test_score_nontemporal_batch_matches_small_batch(case):
+    """A batch past 256 MB of features (non-temporal loads in the scoring pass) gives
+    the bits of the same tiles scored 8 at a time (cached loads): the batch repeats
+    8 seeded tiles, so every tile is compared."""
+    import dataclasses
+    L = need_gpu()
+    n, dv, f32, G = NT_BATCH[case]
+    cfg = dataclasses.replace(get_workload("llava15_7b", keep=128).score, G=8, n=n, d_v=dv,
+                              layers=(12, 24), keep=n // 4, K=4)
+    attn, feats = vision_inputs(cfg, 11)
+    if f32:
+        feats = [f.float() for f in feats]
+    esize = 4 if f32 else 2
+    assert G * n * dv * esize * len(feats) > (256 << 20) and G % 8 == 0
+    log(f"[score nt] case={case} G={G} n={n} d_v={dv} fp32={f32}")
+    n_anchor = (cfg.keep * 7) // 10
+    attn_d, feats_d = attn.cuda(), [f.cuda() for f in feats]
+    small = L.score(attn_d, feats_d, n_anchor)
+    big = L.score(attn_d.repeat(G // 8, 1, 1), [f.repeat(G // 8, 1, 1) for f in feats_d], n_anchor)
+    torch.cuda.synchronize()
+    for k in ("a", "cluster", "s", "m"):
+        ref = small[k].repeat(G // 8, 1)
+        assert torch.equal(big[k], ref), k
