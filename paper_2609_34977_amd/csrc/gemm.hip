@@ -1,14 +1,17 @@
 // Decoder GEMMs: out = A[rows] x W^T with W in nn.Linear layout [N, K].
 //
-// Up to 256 rows (the pruned-prefill regime: a few hundred rows against
-// multi-MB weight matrices) gemm_stream_kernel below streams every weight
-// element from HBM exactly once, straight into MFMA registers.  More rows use
-// gemm_bf16_kernel: 256 threads = 4 waves, block tile BM x BN x 32 with
-// v_mfma_f32_16x16x32_bf16 (fp32 accumulation), a wave owning a
+// Up to 4 rows (decoding) gemv_kernel streams the weights against the few
+// activation rows.  Up to 256 rows (the pruned-prefill regime: a few hundred
+// rows against multi-MB weight matrices) gemm_stream_kernel streams every
+// weight element from HBM once through an LDS ring into the MFMAs.  More rows
+// use gemm_tile_kernel (256-column tiles of 128-256 rows).  Shapes neither of
+// the last two takes (N not a multiple of their column tiles, unaligned
+// outputs) use gemm_bf16_kernel: 256 threads = 4 waves, block tile BM x BN x
+// 32 with v_mfma_f32_16x16x32_bf16 (fp32 accumulation), a wave owning a
 // (BM/WGM) x (BN/WGN) sub-tile; a ring of PF register stages of 16-byte
 // global loads in flight, double-buffered LDS (row pitch 40 bf16: the
 // 16 rows x 16 bytes of a fragment read hit distinct banks), one barrier per
-// k-tile.  Both kernels may gather A rows through a row list and take a
+// k-tile.  The kernels may gather A rows through a row list and take a
 // grouped launch: up to three problems sharing K (Q over the query rows, K and
 // V over all rows) in one grid.  Logical tiles are ordered (group, n-tile,
 // k-split, m-tile) and the hardware block id is remapped so consecutive
@@ -1462,10 +1465,14 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
     const int per16 = dual ? 8 : 4;
     return reinterpret_cast<uintptr_t>(g.out) % 16 == 0 && g.ldo % per16 == 0 && g.split_stride % per16 == 0;
   };
+  // Shapes the streaming and tile kernels do not take go to the LDS-staged kernel
+  // (up to 256 rows a tile of all rows, non-dual; the SwiGLU launch fits the
+  // streaming kernel whenever K and N are multiples of 64 and its output is
+  // aligned, so its fallback is the 128 x 64 tile at any row count)
   for (int i = 0; i < a.ngroups; ++i)
     if (a.g[i].N % tc.BN || (tc.stream && (a.K % 64 || !vec_out(a.g[i])))) {
-      tc = maxM <= 256 ? TileCfg{std::max(64, (maxM + 63) / 64 * 64), dual ? 32 : 64, false}
-                       : TileCfg{128, dual ? 64 : 128, false};
+      tc = maxM <= 256 && !dual ? TileCfg{std::max(64, (maxM + 63) / 64 * 64), 64, false}
+                                : TileCfg{128, dual ? 64 : 128, false};
       break;
     }
   for (int i = 0; i < a.ngroups; ++i)
@@ -1484,13 +1491,7 @@ hipError_t launch_gemm_bf16(GemmArgs& a, int split_max, hipStream_t st) {
       default: dual ? launch_stream<8, true>(a, st) : launch_stream<8, false>(a, st); break;
     }
   } else if (dual) {
-    switch (tc.BM * 1000 + tc.BN) {
-      case 64032: launch_cfg<64, 32, 4, 1, true>(a, st); break;
-      case 128032: launch_cfg<128, 32, 4, 1, true>(a, st); break;
-      case 192032: launch_cfg<192, 32, 4, 1, true>(a, st); break;
-      case 256032: launch_cfg<256, 32, 4, 1, true>(a, st); break;
-      default: launch_cfg<128, 64, 2, 2, true>(a, st); break;
-    }
+    launch_cfg<128, 64, 2, 2, true>(a, st);
   } else {
     switch (tc.BM * 1000 + tc.BN) {
       case 64064: launch_cfg<64, 64, 2, 2, false>(a, st); break;
