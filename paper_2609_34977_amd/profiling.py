@@ -31,6 +31,7 @@ import hashlib
 import json
 import os
 import re
+import sys
 import statistics
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -188,6 +189,54 @@ def stats(args):
     with open(args.out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
+
+
+_KERNEL_SYM = re.compile(r"spider::\(anonymous namespace\)::([A-Za-z0-9_]+_kernel(?:<[^()]*>)?)")
+
+
+def library_kernels(lib_path=None, names_file=None):
+    """Kernel instantiations of the library: the host-side launch stubs that
+    `nm -C` lists for the built shared object (one per template instantiation),
+    or the names in a text file, one per line."""
+    if names_file:
+        with open(names_file) as f:
+            text = f.read()
+    else:
+        import subprocess
+        text = subprocess.run(["nm", "-C", lib_path], check=True, capture_output=True, text=True).stdout
+    out = set()
+    for line in text.splitlines():
+        line = line.replace("__device_stub__", "")
+        m = _KERNEL_SYM.search(line)
+        if m:
+            out.add(m.group(1))
+        elif re.fullmatch(r"[A-Za-z0-9_]+_kernel(<[^()]*>)?", line.strip()):
+            out.add(line.strip())
+    return sorted(out)
+
+
+def coverage(args):
+    """Every kernel instantiation of the library with the number of its
+    dispatches in a traced run (rocprofv3 --kernel-trace --stats), zero flagged."""
+    calls = {}
+    with open(args.csv) as f:
+        for r in csv.DictReader(f):
+            m = _KERNEL_SYM.search(r["Name"])
+            if m:
+                calls[m.group(1)] = calls.get(m.group(1), 0) + int(r["Calls"])
+    kernels = library_kernels(args.lib, args.names)
+    never = [k for k in kernels if not calls.get(k)]
+    lines = [f"# {args.title}", "", "Commands (run from the repository root on one MI355X):", "", "```"]
+    lines += (args.command or []) + ["```", "",
+              f"{len(kernels)} kernel instantiations in the library, {len(kernels) - len(never)} dispatched "
+              f"during the run, {len(never)} never" + (": " + ", ".join(f"`{k}`" for k in never) if never else "") + ".",
+              "", "| kernel | dispatches |", "|---|---|"]
+    for k in kernels:
+        lines.append(f"| `{k}` | {calls.get(k, 0)} |")
+    with open(args.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines[:12]))
+    return 0 if not never else 1
 
 
 def bench_table(args):
@@ -364,6 +413,13 @@ def main():
     m.add_argument("--out", required=True)
     m.add_argument("--title", default="MFMA counters")
     m.add_argument("--command", action="append")
+    c = sub.add_parser("coverage")
+    c.add_argument("--csv", required=True, help="kernel statistics of the traced run")
+    c.add_argument("--lib", default=None, help="the built library (its kernel instantiations via nm -C)")
+    c.add_argument("--names", default=None, help="or a file of kernel instantiation names")
+    c.add_argument("--out", required=True)
+    c.add_argument("--title", default="Kernel coverage")
+    c.add_argument("--command", action="append")
     w = sub.add_parser("sweep-table")
     w.add_argument("--jsonl", required=True)
     w.add_argument("--out", required=True)
@@ -381,6 +437,8 @@ def main():
         stats(args)
     elif args.cmd == "bench-table":
         bench_table(args)
+    elif args.cmd == "coverage":
+        sys.exit(coverage(args))
 
 
 if __name__ == "__main__":

@@ -155,3 +155,23 @@ def test_vendor_gemm_table_rows_and_ratio(tmp_path):
     assert len(rows) == 3
     assert rows[0].split("|")[3].strip() == "gemm_qkv" and rows[0].rstrip("| ").endswith("0.91")
     assert "900.0 (1205)" in rows[2] and rows[2].rstrip("| ").endswith("1.02")
+
+
+def test_coverage_lists_every_instantiation_and_flags_the_idle_ones(tmp_path):
+    names = tmp_path / "names.txt"
+    names.write_text("__device_stub__gemm_tile_kernel<4, true, false>\nnorm_kernel<float, 8>\nselect_kernel\n")
+    stats = tmp_path / "stats.csv"
+    with open(stats, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs", "MaxNs", "StdDev"])
+        w.writerow(["void spider::(anonymous namespace)::gemm_tile_kernel<4, true, false>(spider::GemmArgs)",
+                    "12", "100", "8", "1", "1", "9", "0"])
+        w.writerow(["spider::(anonymous namespace)::select_kernel(int, int)", "3", "30", "10", "1", "9", "11", "0"])
+        w.writerow(["at::native::vectorized_elementwise_kernel<4>(int)", "99", "5", "1", "1", "1", "1", "0"])
+    out = tmp_path / "cov.md"
+    rc = P.coverage(argparse.Namespace(csv=str(stats), lib=None, names=str(names), out=str(out), title="t",
+                                       command=["cmd"]))
+    text = out.read_text()
+    assert rc == 1
+    assert "3 kernel instantiations in the library, 2 dispatched during the run, 1 never: `norm_kernel<float, 8>`" in text
+    assert "| `gemm_tile_kernel<4, true, false>` | 12 |" in text and "| `norm_kernel<float, 8>` | 0 |" in text
