@@ -52,7 +52,7 @@ def parse():
     p.add_argument("--layers", type=int, default=None)
     p.add_argument("--skip-p", type=float, default=None)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-layers", type=int, default=2)
+    p.add_argument("--cpu-layers", type=int, default=4)
     p.add_argument("--no-secondary", action="store_true",
                    help="do not add the LLaVA-1.5-7B keep-128 step to the default line")
     p.add_argument("--copy-probe-mib", type=int, default=0,
